@@ -1,0 +1,205 @@
+/*
+ * lrcnn.h -- row-centric CNN training (LR-CNN, arXiv 2401.11471) on one
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The paper re-orders the training of a convolution stack from layer order
+ * ("column") to row order (Section III-A, Eqs. (4)-(5), Algorithm 1): the
+ * input is split into horizontal row bands, every band is pushed through all
+ * layers before the next one starts, and the feature maps of a band are
+ * dropped as soon as the band is done. Backward propagation walks the bands
+ * in reverse, recomputes each band's feature maps (Algorithm 1, BP loop) and
+ * accumulates the weight gradients g^l over bands. Convolution windows that
+ * straddle two bands (the "weak dependency", Section III-B) are handled in
+ * one of two ways:
+ *   LRCNN_CARRY      two-phase sharing (Section IV-A): rows of a feature map
+ *                    that a later band still needs are kept when the band
+ *                    that computed them finishes, and reused in FP and BP;
+ *                    in BP the error that a band sends to rows owned by an
+ *                    earlier band is carried to that band in float32.
+ *   LRCNN_RECOMPUTE  overlapping partitioning (Section IV-B): the last layer
+ *                    is split evenly and every band recomputes its whole
+ *                    receptive cone; each band back-propagates only its own
+ *                    rows of the upstream gradient and the partial gradients
+ *                    are summed (exact, by linearity).
+ * Padding is "semi-closed" (Section III-B): only the true image top and
+ * bottom are padded; band edges always see real rows.
+ *
+ * Results equal ordinary layer-by-layer training up to float rounding.
+ *
+ * Conventions for every entry point:
+ *  - Return value: LRCNN_OK (0) or a negative lrcnn_status; the message of the
+ *    last error on the calling thread is returned by lrcnn_last_error().
+ *  - Device pointers are caller-owned device memory (hipMalloc or a torch
+ *    tensor); the library never allocates or frees device memory and never
+ *    synchronises: all work is enqueued on `stream` (a hipStream_t; NULL is
+ *    the default stream).
+ *  - Tensors are dense NHWC: x is [B][H][W][C_in], y / dy are the last node's
+ *    output [B][H_L][W_L][C_L]. Weights are [C_out][kh][kw][C_in].
+ *    Storage type is the plan's dtype (float32 or bfloat16) for x, y, dy, dx
+ *    and weights; affine scale/shift and weight gradients are float32.
+ *  - Per-node arrays (w, aff_scale, aff_shift, dw, mask_out) are HOST arrays
+ *    of n_nodes device pointers indexed by node id; entries of nodes they do
+ *    not apply to are ignored and may be NULL.
+ *  - Device pointers must be 16-byte aligned.
+ *  - A plan must not be used from two streams or threads at once.
+ */
+#ifndef LRCNN_H
+#define LRCNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LRCNN_OK = 0,
+  LRCNN_EINVAL = -1,      /* null pointer, bad enum, misaligned pointer      */
+  LRCNN_ESHAPE = -2,      /* inconsistent graph or a layer with no output    */
+  LRCNN_EPARTITION = -3,  /* band bounds not monotone / out of range         */
+  LRCNN_EWORKSPACE = -4,  /* workspace smaller than the plan requires        */
+  LRCNN_ESTATE = -5,      /* backward_rows without a matching forward_rows   */
+  LRCNN_EDTYPE = -6,      /* unsupported dtype                               */
+  LRCNN_EHIP = -7,        /* a HIP launch failed                             */
+  LRCNN_EINFEASIBLE = -8  /* no band count fits the memory budget            */
+} lrcnn_status;
+
+/* Node kinds. Nodes are given in topological order; node 0 is the input. */
+enum {
+  LRCNN_OP_INPUT = 0,
+  LRCNN_OP_CONV = 1,    /* bias-free cross-correlation, Eq. (1); optional  */
+                        /* per-channel affine (fixed BatchNorm) and ReLU    */
+  LRCNN_OP_MAXPOOL = 2, /* kh x kw window, stride, -inf padding             */
+  LRCNN_OP_ADD = 3      /* elementwise in0 + in1 (residual), optional ReLU */
+};
+
+typedef struct {
+  int32_t op;
+  int32_t in0, in1;          /* producer node ids (in1 only for ADD), else -1 */
+  int32_t c_out;             /* CONV output channels (ignored otherwise)      */
+  int32_t kh, kw, sh, sw, ph, pw;
+  int32_t affine;            /* CONV: out = scale[c] * conv + shift[c]       */
+  int32_t relu;              /* CONV / ADD: ReLU after affine / sum           */
+} lrcnn_node;
+
+enum { LRCNN_F32 = 0, LRCNN_BF16 = 1 };
+enum { LRCNN_CARRY = 0, LRCNN_RECOMPUTE = 1 };
+/* Band placement. CARRY bands are ranges of input rows (Algorithm 1 splits
+ * the input); RECOMPUTE bands are ranges of the last node's rows (the paper
+ * divides the last layer evenly, Section IV-B).
+ *   EVEN      r * H / N boundaries
+ *   BALANCED  CARRY only: boundaries that minimise the largest per-band
+ *             cache of feature maps (the skew of Section IV-A)
+ *   EXPLICIT  the caller's `bounds` (n_bands + 1 non-decreasing values from
+ *             0 to the partitioned height; empty bands are allowed)       */
+enum { LRCNN_EVEN = 0, LRCNN_BALANCED = 1, LRCNN_EXPLICIT = 2 };
+
+typedef struct {
+  int32_t batch, in_c, in_h, in_w;
+  int32_t dtype;             /* LRCNN_F32 | LRCNN_BF16                        */
+  int32_t mode;              /* LRCNN_CARRY | LRCNN_RECOMPUTE                 */
+  int32_t n_bands;           /* N >= 1                                        */
+  int32_t policy;            /* LRCNN_EVEN | LRCNN_BALANCED | LRCNN_EXPLICIT  */
+  const int32_t *bounds;     /* host array, used when policy == EXPLICIT      */
+} lrcnn_config;
+
+/* Opaque plan handle (host memory only). */
+typedef struct lrcnn_plan_s lrcnn_plan_t;
+
+/* Analytic figures of a plan. Byte counts include the batch. */
+typedef struct {
+  int32_t n_nodes, n_bands, mode, dtype;
+  int32_t out_h, out_w, out_c;
+  size_t workspace_bytes;          /* forward_rows + backward_rows          */
+  size_t layerwise_workspace_bytes;/* lrcnn_layerwise_reference_gpu         */
+  size_t strip_bytes;              /* CARRY: shared rows kept FP -> BP      */
+  size_t band_cache_bytes;         /* largest band's cached feature maps    */
+  size_t delta_bytes;              /* float32 error windows (peak)          */
+  size_t carry_bytes;              /* CARRY: float32 error carried to r-1   */
+  size_t partial_bytes;            /* weight-gradient partial sums          */
+  double omega_bytes;              /* Eq. (3): all node outputs, full size  */
+  double omega_fp_bytes;           /* Eq. (7) analogue: peak of FP          */
+  double omega_bp_bytes;           /* Eq. (8) analogue: peak of BP          */
+  double flops_tau;                /* tau (Section IV-B): forward convs     */
+  double flops_rows;               /* FLOPs of forward_rows+backward_rows   */
+  double flops_layerwise;          /* 3 tau                                 */
+  int64_t shared_rows;             /* CARRY: sum of kept rows over bands    */
+  int64_t halo_rows;               /* RECOMPUTE: rows computed by more than */
+                                   /* one band, summed over nodes and bands */
+} lrcnn_plan_info;
+
+/* Build a plan: shapes of every node, per-band row intervals, workspace
+ * layout, analytic memory (Eqs. (3), (7), (8), (12)) and FLOPs (tau,
+ * Section IV-B). Pure host code; needs no GPU. `nodes`, `cfg` and
+ * `cfg->bounds` are read during the call only. On success *out owns a plan
+ * that the caller releases with lrcnn_plan_destroy.
+ * Errors: EINVAL (null pointer, bad enum), ESHAPE (bad ids, channel or size
+ * mismatch, a layer with empty output), EPARTITION (bad bounds). */
+int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
+               const lrcnn_config *cfg, lrcnn_plan_t **out);
+
+/* Fill *info. Errors: EINVAL on null. */
+int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info);
+
+/* Output shape of node `node`: shape = {H, W, C}. Errors: EINVAL. */
+int lrcnn_plan_node_shape(const lrcnn_plan_t *plan, int32_t node,
+                          int32_t shape[3]);
+
+/* Rows of node `node` in band `band` (0-based): rows[0..1] = the rows the
+ * band computes and owns [a, b); rows[2..3] = the rows it holds [lo, hi)
+ * (CARRY: own rows plus the rows shared from earlier bands; RECOMPUTE: the
+ * band's receptive cone). Errors: EINVAL. */
+int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t band, int32_t node,
+                         int32_t rows[4]);
+
+void lrcnn_plan_destroy(lrcnn_plan_t *plan);
+
+/* Row-centric FP (Algorithm 1, FP loop): writes y. In CARRY mode the rows
+ * shared between bands are left in `workspace` for lrcnn_backward_rows.
+ * mask_out (nullable host array; entries nullable): per node a device
+ * uint8 [B][H][W][C] buffer that receives the ReLU mask (1 where the output
+ * is > 0) of CONV/ADD nodes with ReLU and the argmax (row-major index inside
+ * the window) of MAXPOOL nodes.
+ * Errors: EINVAL, EWORKSPACE (ws_bytes < workspace_bytes), EHIP. */
+int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x,
+                       const void *const *w,
+                       const float *const *aff_scale,
+                       const float *const *aff_shift,
+                       void *y, void *workspace, size_t ws_bytes,
+                       void *const *mask_out, void *stream);
+
+/* Row-centric BP (Algorithm 1, BP loop), bands in reverse: recompute each
+ * band, propagate the error dy = dL/dy, overwrite dw[node] (float32,
+ * [C_out][kh][kw][C_in]) with the weight gradient of every conv node and,
+ * when dx != NULL, write dL/dx. CARRY mode needs the workspace of the
+ * preceding lrcnn_forward_rows on this plan, unchanged.
+ * Errors: EINVAL, EWORKSPACE, ESTATE (CARRY without a preceding forward on
+ * this plan and workspace), EHIP. */
+int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x,
+                        const void *const *w,
+                        const float *const *aff_scale,
+                        const float *const *aff_shift,
+                        const void *dy, float *const *dw, void *dx,
+                        void *workspace, size_t ws_bytes, void *stream);
+
+/* Layer-by-layer ("column", Eqs. (1)-(3)) training step on the GPU with the
+ * same kernels: full-height feature maps of every node are kept from FP to
+ * BP and nothing is recomputed. Writes y, dw and (if non-NULL) dx and
+ * mask_out as above. Needs layerwise_workspace_bytes of workspace.
+ * Errors: EINVAL, EWORKSPACE, EHIP. */
+int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
+                                  const void *const *w,
+                                  const float *const *aff_scale,
+                                  const float *const *aff_shift,
+                                  const void *dy, void *y, float *const *dw,
+                                  void *dx, void *workspace, size_t ws_bytes,
+                                  void *const *mask_out, void *stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char *lrcnn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LRCNN_H */

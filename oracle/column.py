@@ -149,10 +149,12 @@ def shapes(nodes, h, w, c):
     return out
 
 
-def apply_node(node, srcs, w, scale, shift, bf16):
-    """Forward of one node given its input tensors. Returns (out, argmax)."""
+def apply_node(node, srcs, w, scale, shift, bf16, want_pre=False):
+    """Forward of one node given its input tensors. Returns (out, argmax),
+    plus the value before ReLU (None for pooling) when ``want_pre``."""
     op, in0, in1, co, kh, kw, sh, sw, ph, pw, aff, rl = node
     idx = None
+    t = None
     if op == OP_CONV:
         t = conv_fwd(srcs[0], w, sh, sw, ph, pw)
         if aff:
@@ -167,20 +169,28 @@ def apply_node(node, srcs, w, scale, shift, bf16):
         raise ValueError("bad op")
     if bf16:
         out = round_bf16(out)
+    if want_pre:
+        return out, idx, t
     return out, idx
 
 
-def forward(nodes, x, weights, scales, shifts, bf16=False):
+def forward(nodes, x, weights, scales, shifts, bf16=False, keep_pre=False):
     """Column FP (Eq. (1) applied layer after layer). ``weights[v-1]`` etc.
-    belong to node v. Returns (acts, argmax) with acts[0] = x."""
+    belong to node v. Returns (acts, argmax) with acts[0] = x; with
+    ``keep_pre`` also the values before ReLU of every ReLU node (so a
+    ReLU decision of another implementation can be judged a near-tie)."""
     acts = [np.asarray(x, dtype=np.float64)]
     argmax = [None]
+    pre = [None]
     for v, node in enumerate(nodes[1:], start=1):
         srcs = [acts[node[1]]] + ([acts[node[2]]] if node[0] == OP_ADD else [])
-        out, idx = apply_node(node, srcs, weights[v - 1], scales[v - 1],
-                              shifts[v - 1], bf16)
+        out, idx, t = apply_node(node, srcs, weights[v - 1], scales[v - 1],
+                                 shifts[v - 1], bf16, want_pre=True)
+        pre.append(t if (keep_pre and node[11]) else None)
         acts.append(out)
         argmax.append(idx)
+    if keep_pre:
+        return acts, argmax, pre
     return acts, argmax
 
 

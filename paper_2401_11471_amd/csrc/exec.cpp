@@ -1,0 +1,489 @@
+// Band executor: walks the plan's bands and nodes and enqueues the kernels
+// of kernels.hip on the caller's stream. Implements the three entry points
+// lrcnn_forward_rows, lrcnn_backward_rows and
+// lrcnn_layerwise_reference_gpu (Algorithm 1 and its column baseline).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "plan.hpp"
+
+namespace lrcnn {
+namespace {
+
+enum Sched { S_CARRY, S_RECOMPUTE, S_LAYERWISE };
+
+// Dry-run mode (test hook): the executor walks the schedule and runs every
+// host-side check but enqueues nothing, so it runs without a GPU.
+thread_local bool g_dry = false;
+
+#define LAUNCH(call, what)                                                 \
+  do {                                                                     \
+    int e_ = g_dry ? 0 : (call);                                           \
+    if (e_ != 0)                                                           \
+      return lrcnn_fail(LRCNN_EHIP, std::string(what) + ": " +             \
+                                        hipGetErrorString((hipError_t)e_)); \
+  } while (0)
+
+struct Run {
+  Plan &P;
+  const Layout &L;
+  Sched sched;
+  char *ws;
+  const void *x;
+  const void *const *w;
+  const float *const *sc;
+  const float *const *sf;
+  void *stream;
+  int dt;
+  std::vector<View> act;   // current feature-map view of every node
+  std::vector<View> dlt;   // current float32 error view of every node
+  std::vector<int> first_consumer;
+
+  Run(Plan &p, const Layout &l, Sched s, void *wsp, const void *x_,
+      const void *const *w_, const float *const *sc_, const float *const *sf_,
+      void *st)
+      : P(p), L(l), sched(s), ws((char *)wsp), x(x_), w(w_), sc(sc_), sf(sf_),
+        stream(st), dt(p.cfg.dtype == LRCNN_BF16 ? DT_BF16 : DT_F32) {
+    act.resize(P.n);
+    dlt.resize(P.n);
+    first_consumer.assign(P.n, -1);
+    for (int v = 0; v < P.n; ++v)
+      for (int c : P.cons[v]) first_consumer[v] = std::max(first_consumer[v], c);
+    const Shape &s0 = P.shp[0];
+    act[0] = View{const_cast<void *>(x), (long long)s0.h * s0.w * s0.c, 0, s0.w, s0.c, s0.h};
+  }
+
+  View full(void *p, int v) const {
+    const Shape &s = P.shp[v];
+    return View{p, (long long)s.h * s.w * s.c, 0, s.w, s.c, s.h};
+  }
+  View win(size_t off, int v, int cap, int row0) const {
+    const Shape &s = P.shp[v];
+    return View{ws + off, (long long)cap * s.w * s.c, row0, s.w, s.c, cap};
+  }
+  // Host-side guard: every row a launch touches must be held by its view,
+  // so a planning error is reported instead of reaching the GPU.
+  static bool holds(const View &v, int r0, int r1) {
+    return r1 <= r0 || (r0 >= v.row0 && r1 <= v.row0 + v.rows);
+  }
+  // rows of the producer read by output rows [a, b) of a windowed op
+  static void in_rows(const lrcnn_node &d, int h_in, int a, int b, int &r0, int &r1) {
+    if (d.op == LRCNN_OP_ADD) {
+      r0 = a, r1 = b;
+    } else {
+      r0 = std::max(0, a * d.sh - d.ph);
+      r1 = std::min(h_in, (b - 1) * d.sh - d.ph + d.kh);
+    }
+  }
+
+  // Forward of node v over rows [a, b) into `dst`.
+  int node_fwd(int v, int a, int b, View dst, uint8_t *am, uint8_t *mask) {
+    if (b <= a) return LRCNN_OK;
+    const lrcnn_node &d = P.nodes[v];
+    const Shape &sv = P.shp[v], &su = P.shp[d.in0];
+    const int B = P.cfg.batch;
+    {
+      int r0, r1;
+      in_rows(d, su.h, a, b, r0, r1);
+      bool ok = holds(dst, a, b) && holds(act[d.in0], r0, r1);
+      if (d.op == LRCNN_OP_ADD) ok = ok && holds(act[d.in1], r0, r1);
+      if (!ok)
+        return lrcnn_fail(LRCNN_EINVAL, "internal: band rows of node " + std::to_string(v) +
+                                            " not held by its buffers");
+    }
+    if (d.op == LRCNN_OP_CONV) {
+      ConvArgs c{};
+      c.src = act[d.in0];
+      c.dst = dst;
+      c.w = w[v];
+      c.scale = d.affine ? sc[v] : nullptr;
+      c.shift = d.affine ? sf[v] : nullptr;
+      c.relu = d.relu;
+      c.mask = mask;
+      c.mask_h = sv.h;
+      c.B = B;
+      c.y0 = a;
+      c.y1 = b;
+      c.Wd = sv.w;
+      c.N = sv.c;
+      c.KC = su.c;
+      c.Hs = su.h;
+      c.Ws = su.w;
+      c.sy0 = 0;
+      c.sy1 = su.h;
+      c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
+      LAUNCH(launch_conv(dt, 0, c, stream), "conv forward");
+    } else if (d.op == LRCNN_OP_MAXPOOL) {
+      PoolArgs p{};
+      p.src = act[d.in0];
+      p.dst = dst;
+      p.am = am;
+      p.mask = mask;
+      p.mask_h = sv.h;
+      p.B = B;
+      p.y0 = a;
+      p.y1 = b;
+      p.Wd = sv.w;
+      p.C = sv.c;
+      p.Hs = su.h;
+      p.Ws = su.w;
+      p.kh = d.kh, p.kw = d.kw, p.sh = d.sh, p.sw = d.sw, p.ph = d.ph, p.pw = d.pw;
+      LAUNCH(launch_pool_fwd(dt, p, stream), "max-pool forward");
+    } else {
+      LAUNCH(launch_add_fwd(dt, act[d.in0], act[d.in1], dst, d.relu, mask, sv.h,
+                            B, a, b, sv.w, sv.c, stream),
+             "add forward");
+    }
+    return LRCNN_OK;
+  }
+
+  // Compute the feature maps of band `r` for every node (FP, or the BP
+  // recompute of Algorithm 1). The output node goes to `y` when given.
+  int band_fwd(int r, void *y, void *const *mask_out, bool bp) {
+    const int n = P.n;
+    for (int v = 1; v < n; ++v) {
+      const Rows q = band_rows(r, v);
+      View dst;
+      if (v == n - 1 && y) {
+        dst = full(y, v);
+      } else {
+        dst = win(L.win[v], v, L.win_cap[v], q.lo);
+      }
+      act[v] = dst;
+      if (sched == S_CARRY && r > 0 && q.a > q.lo) {
+        // rows shared from earlier bands (two-phase sharing)
+        View strip = win(L.strip[r - 1][v], v, q.a - q.lo, q.lo);
+        LAUNCH(launch_rows_copy(dt, dt, strip, dst, 0, P.cfg.batch, q.lo, q.a,
+                                P.shp[v].w, P.shp[v].c, stream),
+               "strip load");
+      }
+      uint8_t *am = (bp && P.nodes[v].op == LRCNN_OP_MAXPOOL) ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
+      uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
+      int st = node_fwd(v, q.a, q.b, dst, am, mk);
+      if (st != LRCNN_OK) return st;
+      if (sched == S_CARRY && !bp && r + 1 < P.nb && v != n - 1) {
+        const int t = P.tail[r][v];
+        if (q.b > t) {
+          View strip = win(L.strip[r][v], v, q.b - t, t);
+          LAUNCH(launch_rows_copy(dt, dt, dst, strip, 0, P.cfg.batch, t, q.b,
+                                  P.shp[v].w, P.shp[v].c, stream),
+                 "strip store");
+        }
+      }
+    }
+    return LRCNN_OK;
+  }
+
+  Rows band_rows(int r, int v) const {
+    if (sched == S_LAYERWISE) return Rows{0, P.shp[v].h, 0, P.shp[v].h};
+    return P.rows[r][v];
+  }
+
+  // Zero node u's error window for band r and bring in the error carried
+  // from band r+1 (CARRY).
+  int init_delta(int r, int u) {
+    const Rows q = band_rows(r, u);
+    const Shape &s = P.shp[u];
+    dlt[u] = win(L.delta[u], u, L.win_cap[u], q.lo);
+    int zhi = q.hi;
+    if (sched == S_CARRY && r + 1 < P.nb) {
+      const int t = P.tail[r][u];
+      if (q.b > t) {
+        View cv = View{ws + L.carry[u], (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
+                       L.carry_cap[u]};
+        if (!holds(cv, t, q.b) || !holds(dlt[u], t, q.b))
+          return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+        LAUNCH(launch_rows_copy(DT_F32, DT_F32, cv, dlt[u], 0, P.cfg.batch, t, q.b, s.w,
+                                s.c, stream),
+               "carry load");
+        zhi = t;
+      }
+    }
+    LAUNCH(launch_rows_zero(dlt[u], P.cfg.batch, q.lo, zhi, s.w, s.c, stream), "zero error");
+    return LRCNN_OK;
+  }
+
+  // Back-propagate node v's finished error rows [a, b) (Algorithm 1,
+  // Get_error and g^l += Gradient).
+  int node_bwd(int r, int v, float *const *dw, bool want_dx) {
+    const Rows q = band_rows(r, v);
+    const int a = q.a, b = q.b;
+    if (b <= a) return LRCNN_OK;
+    const lrcnn_node &d = P.nodes[v];
+    const Shape &sv = P.shp[v];
+    const int B = P.cfg.batch;
+    const int u = d.in0;
+    const Shape &su = P.shp[u];
+    {
+      int r0, r1;
+      in_rows(d, su.h, a, b, r0, r1);
+      bool ok = holds(act[v], a, b) && holds(dlt[v], a, b) && holds(act[u], r0, r1) &&
+                holds(dlt[u], r0, r1);
+      if (d.op == LRCNN_OP_ADD) ok = ok && holds(act[d.in1], r0, r1) && holds(dlt[d.in1], r0, r1);
+      if (!ok)
+        return lrcnn_fail(LRCNN_EINVAL, "internal: backward rows of node " + std::to_string(v) +
+                                            " not held by its buffers");
+    }
+    if (d.op == LRCNN_OP_CONV) {
+      void *dc = ws + L.dc;
+      LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a, b,
+                            sv.w, sv.c, stream),
+             "error operand");
+      WgradArgs g{};
+      g.dc = dc;
+      g.src = act[u];
+      g.out = (float *)(ws + L.part);
+      g.splits = (sched == S_LAYERWISE ? P.wsplit_lw : P.wsplit)[v];
+      g.B = B;
+      g.y0 = a;
+      g.y1 = b;
+      g.Wv = sv.w;
+      g.Co = sv.c;
+      g.Ci = su.c;
+      g.Hs = su.h;
+      g.Ws = su.w;
+      g.kh = d.kh, g.kw = d.kw, g.sh = d.sh, g.sw = d.sw, g.ph = d.ph, g.pw = d.pw;
+      LAUNCH(launch_wgrad(dt, g, dw[v], stream), "weight gradient");
+      if (u != 0 || want_dx) {
+        LAUNCH(launch_wtranspose(dt, w[v], ws + L.wt, sv.c, d.kh * d.kw, su.c, stream),
+               "weight transpose");
+        ConvArgs c{};
+        c.src = View{dc, (long long)(b - a) * sv.w * sv.c, a, sv.w, sv.c, b - a};
+        c.dst = dlt[u];
+        c.w = ws + L.wt;
+        c.B = B;
+        c.y0 = std::max(0, a * d.sh - d.ph);
+        c.y1 = std::min(su.h, (b - 1) * d.sh - d.ph + d.kh);
+        c.Wd = su.w;
+        c.N = su.c;
+        c.KC = sv.c;
+        c.Hs = sv.h;
+        c.Ws = sv.w;
+        c.sy0 = a;
+        c.sy1 = b;
+        c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
+        LAUNCH(launch_conv(dt, 1, c, stream), "input gradient");
+      }
+    } else if (d.op == LRCNN_OP_MAXPOOL) {
+      PoolBwdArgs p{};
+      p.dv = dlt[v];
+      p.du = dlt[u];
+      p.am = (const uint8_t *)(ws + L.argmax[v]);
+      p.B = B;
+      p.y0 = a;
+      p.y1 = b;
+      p.Wv = sv.w;
+      p.C = sv.c;
+      p.ua = std::max(0, a * d.sh - d.ph);
+      p.ub = std::min(su.h, (b - 1) * d.sh - d.ph + d.kh);
+      p.Wu = su.w;
+      p.kh = d.kh, p.kw = d.kw, p.sh = d.sh, p.sw = d.sw, p.ph = d.ph, p.pw = d.pw;
+      LAUNCH(launch_pool_bwd(p, stream), "max-pool backward");
+    } else {
+      LAUNCH(launch_add_bwd(dt, dlt[v], act[v], dlt[d.in0], dlt[d.in1], d.relu, B, a, b, sv.w,
+                            sv.c, stream),
+             "add backward");
+    }
+    return LRCNN_OK;
+  }
+
+  // BP of band r after its feature maps are in place.
+  int band_bwd(int r, const void *dy, float *const *dw, void *dx, float *dxacc) {
+    const int n = P.n, B = P.cfg.batch;
+    const bool want_dx = dx != nullptr;
+    // seed: the band's own rows of dL/dy
+    {
+      const Rows q = band_rows(r, n - 1);
+      int st = init_delta(r, n - 1);
+      if (st != LRCNN_OK) return st;
+      const Shape &s = P.shp[n - 1];
+      LAUNCH(launch_rows_copy(dt, DT_F32, full(const_cast<void *>(dy), n - 1), dlt[n - 1], 0, B,
+                              q.a, q.b, s.w, s.c, stream),
+             "seed error");
+    }
+    for (int v = n - 1; v >= 1; --v) {
+      const lrcnn_node &d = P.nodes[v];
+      int ins[2] = {d.in0, d.op == LRCNN_OP_ADD ? d.in1 : -1};
+      for (int u : ins)
+        if (u >= 0 && first_consumer[u] == v) {
+          int st = init_delta(r, u);
+          if (st != LRCNN_OK) return st;
+        }
+      int st = node_bwd(r, v, dw, want_dx);
+      if (st != LRCNN_OK) return st;
+      if (sched == S_CARRY && r > 0) {
+        const Rows q = band_rows(r, v);
+        if (q.a > q.lo) {
+          const Shape &s = P.shp[v];
+          View cv{ws + L.carry[v], (long long)L.carry_cap[v] * s.w * s.c, q.lo, s.w, s.c,
+                  L.carry_cap[v]};
+          if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+          LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[v], cv, 0, B, q.lo, q.a, s.w, s.c, stream),
+                 "carry store");
+        }
+      }
+    }
+    // input gradient rows
+    if (want_dx) {
+      const Rows q = band_rows(r, 0);
+      const Shape &s = P.shp[0];
+      if (sched == S_RECOMPUTE) {
+        View acc = dxacc ? full(dxacc, 0) : full(dx, 0);
+        LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[0], acc, 1, B, q.lo, q.hi, s.w, s.c, stream),
+               "input gradient accumulate");
+      } else {
+        LAUNCH(launch_rows_copy(DT_F32, dt, dlt[0], full(dx, 0), 0, B, q.a, q.b, s.w, s.c, stream),
+               "input gradient store");
+        if (sched == S_CARRY && r > 0 && q.a > q.lo) {
+          View cv{ws + L.carry[0], (long long)L.carry_cap[0] * s.w * s.c, q.lo, s.w, s.c,
+                  L.carry_cap[0]};
+          if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+          LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[0], cv, 0, B, q.lo, q.a, s.w, s.c, stream),
+                 "carry store");
+        }
+      }
+    }
+    return LRCNN_OK;
+  }
+
+  int zero_dw(float *const *dw) {
+    for (int v = 1; v < P.n; ++v)
+      if (P.nodes[v].op == LRCNN_OP_CONV) {
+        const lrcnn_node &d = P.nodes[v];
+        size_t cnt = (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c;
+        LAUNCH(launch_zero_f32(dw[v], cnt, stream), "zero dW");
+      }
+    return LRCNN_OK;
+  }
+};
+
+bool misaligned(const void *p) { return ((uintptr_t)p & 15u) != 0; }
+
+int check_params(const Plan &P, const void *x, const void *const *w, const float *const *sc,
+                 const float *const *sf) {
+  if (!x) return lrcnn_fail(LRCNN_EINVAL, "x is null");
+  if (misaligned(x)) return lrcnn_fail(LRCNN_EINVAL, "x is not 16-byte aligned");
+  if (!w) return lrcnn_fail(LRCNN_EINVAL, "weight array is null");
+  for (int v = 1; v < P.n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV) continue;
+    if (!w[v] || misaligned(w[v]))
+      return lrcnn_fail(LRCNN_EINVAL, "weights of node " + std::to_string(v) + " null or misaligned");
+    if (d.affine && (!sc || !sf || !sc[v] || !sf[v]))
+      return lrcnn_fail(LRCNN_EINVAL, "affine node " + std::to_string(v) + " needs scale and shift");
+  }
+  return LRCNN_OK;
+}
+
+int check_ws(const Layout &L, void *ws, size_t bytes) {
+  if (!ws) return lrcnn_fail(LRCNN_EINVAL, "workspace is null");
+  if (misaligned(ws)) return lrcnn_fail(LRCNN_EINVAL, "workspace is not 16-byte aligned");
+  if (bytes < L.total)
+    return lrcnn_fail(LRCNN_EWORKSPACE, "workspace needs " + std::to_string(L.total) +
+                                            " bytes, got " + std::to_string(bytes));
+  return LRCNN_OK;
+}
+
+int check_dw(const Plan &P, float *const *dw) {
+  if (!dw) return lrcnn_fail(LRCNN_EINVAL, "dw array is null");
+  for (int v = 1; v < P.n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_CONV && (!dw[v] || misaligned(dw[v])))
+      return lrcnn_fail(LRCNN_EINVAL, "dw of node " + std::to_string(v) + " null or misaligned");
+  return LRCNN_OK;
+}
+
+uint64_t g_epoch = 0;
+
+}  // namespace
+}  // namespace lrcnn
+
+using namespace lrcnn;
+
+extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void *const *w,
+                                  const float *const *aff_scale, const float *const *aff_shift,
+                                  void *y, void *workspace, size_t ws_bytes,
+                                  void *const *mask_out, void *stream) {
+  if (!plan) return lrcnn_fail(LRCNN_EINVAL, "plan is null");
+  Plan &P = *reinterpret_cast<Plan *>(plan);
+  int st = check_params(P, x, w, aff_scale, aff_shift);
+  if (st != LRCNN_OK) return st;
+  if (!y || misaligned(y)) return lrcnn_fail(LRCNN_EINVAL, "y null or misaligned");
+  if ((st = check_ws(P.rc, workspace, ws_bytes)) != LRCNN_OK) return st;
+  Run run(P, P.rc, P.cfg.mode == LRCNN_CARRY ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale,
+          aff_shift, stream);
+  P.fwd_workspace = nullptr;
+  for (int r = 0; r < P.nb; ++r)
+    if ((st = run.band_fwd(r, y, mask_out, false)) != LRCNN_OK) return st;
+  P.fwd_workspace = workspace;
+  P.fwd_epoch = ++g_epoch;
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void *const *w,
+                                   const float *const *aff_scale, const float *const *aff_shift,
+                                   const void *dy, float *const *dw, void *dx, void *workspace,
+                                   size_t ws_bytes, void *stream) {
+  if (!plan) return lrcnn_fail(LRCNN_EINVAL, "plan is null");
+  Plan &P = *reinterpret_cast<Plan *>(plan);
+  int st = check_params(P, x, w, aff_scale, aff_shift);
+  if (st != LRCNN_OK) return st;
+  if (!dy || misaligned(dy)) return lrcnn_fail(LRCNN_EINVAL, "dy null or misaligned");
+  if (dx && misaligned(dx)) return lrcnn_fail(LRCNN_EINVAL, "dx misaligned");
+  if ((st = check_dw(P, dw)) != LRCNN_OK) return st;
+  if ((st = check_ws(P.rc, workspace, ws_bytes)) != LRCNN_OK) return st;
+  const bool carry = P.cfg.mode == LRCNN_CARRY;
+  if (carry && P.fwd_workspace != workspace)
+    return lrcnn_fail(LRCNN_ESTATE,
+                      "CARRY backward needs a preceding lrcnn_forward_rows on this plan and workspace");
+  Run run(P, P.rc, carry ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale, aff_shift, stream);
+  if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
+  float *dxacc = nullptr;
+  if (!carry && dx) {
+    const Shape &s = P.shp[0];
+    size_t cnt = (size_t)P.cfg.batch * s.h * s.w * s.c;
+    dxacc = P.cfg.dtype == LRCNN_BF16 ? (float *)((char *)workspace + P.rc.dxacc) : (float *)dx;
+    int e = g_dry ? 0 : launch_zero_f32(dxacc, cnt, stream);
+    if (e) return lrcnn_fail(LRCNN_EHIP, "zero dX");
+  }
+  for (int r = P.nb - 1; r >= 0; --r) {
+    if ((st = run.band_fwd(r, nullptr, nullptr, true)) != LRCNN_OK) return st;
+    if ((st = run.band_bwd(r, dy, dw, dx, dxacc)) != LRCNN_OK) return st;
+  }
+  if (!carry && dx && P.cfg.dtype == LRCNN_BF16 && !g_dry) {
+    const Shape &s = P.shp[0];
+    int e = launch_rows_copy(DT_F32, DT_BF16, run.full(dxacc, 0), run.full(dx, 0), 0,
+                             P.cfg.batch, 0, s.h, s.w, s.c, stream);
+    if (e) return lrcnn_fail(LRCNN_EHIP, "store dX");
+  }
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
+                                             const void *const *w,
+                                             const float *const *aff_scale,
+                                             const float *const *aff_shift, const void *dy,
+                                             void *y, float *const *dw, void *dx,
+                                             void *workspace, size_t ws_bytes,
+                                             void *const *mask_out, void *stream) {
+  if (!plan) return lrcnn_fail(LRCNN_EINVAL, "plan is null");
+  Plan &P = *reinterpret_cast<Plan *>(plan);
+  int st = check_params(P, x, w, aff_scale, aff_shift);
+  if (st != LRCNN_OK) return st;
+  if (!y || misaligned(y)) return lrcnn_fail(LRCNN_EINVAL, "y null or misaligned");
+  if (!dy || misaligned(dy)) return lrcnn_fail(LRCNN_EINVAL, "dy null or misaligned");
+  if (dx && misaligned(dx)) return lrcnn_fail(LRCNN_EINVAL, "dx misaligned");
+  if ((st = check_dw(P, dw)) != LRCNN_OK) return st;
+  if ((st = check_ws(P.lw, workspace, ws_bytes)) != LRCNN_OK) return st;
+  Run run(P, P.lw, S_LAYERWISE, workspace, x, w, aff_scale, aff_shift, stream);
+  // FP keeps every node's full map; BP reads them without recomputing.
+  // The pool argmax is produced in FP (bp = true selects its buffer).
+  if ((st = run.band_fwd(0, y, mask_out, true)) != LRCNN_OK) return st;
+  if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
+  return run.band_bwd(0, dy, dw, dx, nullptr);
+}
+
+extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }

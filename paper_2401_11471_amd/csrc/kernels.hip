@@ -1,0 +1,765 @@
+// gfx950 (CDNA4) kernels for row-centric CNN training.
+//
+// Convolutions run as implicit GEMMs on the matrix cores:
+//   forward      (Eq. (1)):  M = B*rows*W_out pixels, N = C_out,
+//                            K = kh*kw*C_in (tap-major, channel-minor)
+//   input grad   (Get_error of Algorithm 1): the same kernel in gather form,
+//                            M = producer pixels, N = C_in, K = kh*kw*C_out
+//   weight grad  (g^l += Gradient, Eq. (2)): M = C_out, N = kh*kw*C_in,
+//                            K = B*rows*W_out pixels, split over workgroups
+//                            with a fixed-order reduction (deterministic)
+// Operands are NHWC, so one 64-byte K slice of a pixel or a weight row is
+// contiguous: tiles are fetched with 16-byte loads and staged in LDS as
+// [row][k] with an 80-byte pitch; every lane then reads its K slice with
+// 16-byte LDS reads. float32 uses v_mfma_f32_32x32x2_f32, bfloat16 uses
+// v_mfma_f32_32x32x16_bf16 with float32 accumulation. A K loop runs over
+// (tap, 64-byte channel chunk); rows of a band's window outside the image
+// read as zero (semi-closed padding), rows inside are real data.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "kernels.hpp"
+
+namespace lrcnn {
+
+typedef uint16_t bf16;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float ldf(const float *p) { return *p; }
+__device__ __forceinline__ float ldf(const bf16 *p) {
+  return __uint_as_float((uint32_t)(*p) << 16);
+}
+// float32 -> bfloat16, round to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
+    return (bf16)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+__device__ __forceinline__ void stf(float *p, float v) { *p = v; }
+__device__ __forceinline__ void stf(bf16 *p, float v) { *p = f2bf(v); }
+
+__device__ __forceinline__ int fdiv(int a, int b) {
+  return a >= 0 ? a / b : -((-a + b - 1) / b);
+}
+
+template <typename T>
+struct Cfg {
+  static constexpr int E = 16 / (int)sizeof(T);  // elements per 16 bytes
+  static constexpr int BK = 4 * E;                // K per tile row: 64 bytes
+  static constexpr int LDK = BK + E;              // LDS pitch: 80 bytes
+};
+
+constexpr int BM = 128;
+
+// ------------------------------------------------------------------ MFMA
+// One 128 x BN tile step. Wave w owns rows [wm, wm+64) and columns
+// [wn, wn+BN/2); lane l feeds row/column (l & 31) of each 32x32 block and
+// the K slice [KPL*(l>>5), KPL*(l>>5)+KPL) of the 64-byte tile row. The
+// same slice order is used for A and B, so every MFMA adds products of
+// matching K indices.
+template <int BN>
+__device__ __forceinline__ void mma_tile(const float *As, const float *Bs,
+                                         f32x16 (&acc)[2][BN / 64], int wm,
+                                         int wn, int lane) {
+  constexpr int LDK = Cfg<float>::LDK, NB = BN / 64;
+  const int r = lane & 31, g = lane >> 5;
+  float4 a[2][2], b[NB][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + 8 * g);
+    a[i][0] = p[0];
+    a[i][1] = p[1];
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + 8 * g);
+    b[j][0] = p[0];
+    b[j][1] = p[1];
+  }
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      float av = (s & 3) == 0 ? a[i][s >> 2].x : (s & 3) == 1 ? a[i][s >> 2].y
+               : (s & 3) == 2 ? a[i][s >> 2].z : a[i][s >> 2].w;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        float bv = (s & 3) == 0 ? b[j][s >> 2].x : (s & 3) == 1 ? b[j][s >> 2].y
+                 : (s & 3) == 2 ? b[j][s >> 2].z : b[j][s >> 2].w;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[i][j], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int BN>
+__device__ __forceinline__ void mma_tile(const bf16 *As, const bf16 *Bs,
+                                         f32x16 (&acc)[2][BN / 64], int wm,
+                                         int wn, int lane) {
+  constexpr int LDK = Cfg<bf16>::LDK, NB = BN / 64;
+  const int r = lane & 31, g = lane >> 5;
+  bf16x8 a[2][2], b[NB][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 16 * g);
+    a[i][0] = p[0];
+    a[i][1] = p[1];
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 16 * g);
+    b[j][0] = p[0];
+    b[j][1] = p[1];
+  }
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i][s], b[j][s],
+                                                            acc[i][j], 0, 0, 0);
+}
+
+// Row of the 32x32 accumulator block held in register v of lane l.
+__device__ __forceinline__ int acc_row(int v, int lane) {
+  return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+}
+
+// Load E consecutive elements (16 bytes) or zeros; `lim` = elements of the
+// vector that exist (scalar path for channel counts not a multiple of E).
+template <typename T, bool VEC>
+__device__ __forceinline__ uint4 load16(const T *p, bool ok, int lim) {
+  if (VEC) {
+    return ok ? *(const uint4 *)p : make_uint4(0, 0, 0, 0);
+  } else {
+    union {
+      uint4 u;
+      T e[Cfg<T>::E];
+    } r;
+    r.u = make_uint4(0, 0, 0, 0);
+    if (ok) {
+#pragma unroll
+      for (int e = 0; e < Cfg<T>::E; ++e)
+        if (e < lim) r.e[e] = p[e];
+    }
+    return r.u;
+  }
+}
+
+// ------------------------------------------- conv forward / input grad
+template <typename T, int BN, bool DGRAD, bool VEC>
+__global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
+  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
+  constexpr int NB = BN / 64;
+  __shared__ __align__(16) T As[2][BM * LDK];
+  __shared__ __align__(16) T Bs[2][BN * LDK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int R = a.y1 - a.y0;
+  const int M = a.B * R * a.Wd;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int taps = a.kh * a.kw;
+  const int CB = (a.KC + BK - 1) / BK;
+  const int KT = taps * CB;
+  const int kv = tid & 3;
+  const T *src = (const T *)a.src.p;
+  const T *w = (const T *)a.w;
+  const long long srow = (long long)a.src.W * a.src.C;
+
+  int ab[2], ay[2], ax[2];
+  bool am[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    int m = m0 + (tid >> 2) + 64 * i;
+    am[i] = m < M;
+    int mm = am[i] ? m : 0;
+    ax[i] = mm % a.Wd;
+    int t = mm / a.Wd;
+    ay[i] = a.y0 + t % R;
+    ab[i] = t / R;
+  }
+  const long long bns = DGRAD ? (long long)a.KC : (long long)taps * a.KC;
+  const long long bts = DGRAD ? (long long)a.N * a.KC : (long long)a.KC;
+  int bn[NB];
+  bool bvld[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    bn[j] = n0 + (tid >> 2) + 64 * j;
+    bvld[j] = bn[j] < a.N;
+  }
+
+  uint4 ra[2], rb[NB];
+  auto gload = [&](int kt) {
+    const int tap = kt / CB;
+    const int c0 = (kt - tap * CB) * BK + kv * E;
+    const int ti = tap / a.kw, tj = tap - ti * a.kw;
+    const bool cok = c0 < a.KC;
+    const int lim = a.KC - c0;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      int sy, sx;
+      bool ok;
+      if (DGRAD) {
+        int ty = ay[i] + a.ph - ti, tx = ax[i] + a.pw - tj;
+        ok = ty >= 0 && tx >= 0;
+        sy = ty / a.sh;
+        sx = tx / a.sw;
+        ok = ok && sy * a.sh == ty && sx * a.sw == tx;
+      } else {
+        sy = ay[i] * a.sh - a.ph + ti;
+        sx = ax[i] * a.sw - a.pw + tj;
+        ok = sx >= 0;
+      }
+      ok = ok && am[i] && cok && sy >= a.sy0 && sy < a.sy1 && sx < a.Ws;
+      const T *p = src;
+      if (ok)
+        p = src + ab[i] * a.src.bs + (sy - a.src.row0) * srow +
+            (long long)sx * a.src.C + c0;
+      ra[i] = load16<T, VEC>(p, ok, lim);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      bool ok = bvld[j] && cok;
+      const T *p = ok ? w + bn[j] * bns + tap * bts + c0 : w;
+      rb[j] = load16<T, VEC>(p, ok, lim);
+    }
+  };
+
+  f32x16 acc[2][NB];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
+  if (KT > 0) gload(0);
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      *(uint4 *)(&As[buf][((tid >> 2) + 64 * i) * LDK + kv * E]) = ra[i];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      *(uint4 *)(&Bs[buf][((tid >> 2) + 64 * j) * LDK + kv * E]) = rb[j];
+    __syncthreads();
+    if (kt + 1 < KT) gload(kt + 1);
+    mma_tile<BN>(As[buf], Bs[buf], acc, wm, wn, lane);
+  }
+
+  // epilogue
+  const int col = lane & 31;
+  const long long drow = (long long)a.Wd * a.N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + wm + 32 * i + acc_row(v, lane);
+      if (m >= M) continue;
+      const int x = m % a.Wd;
+      const int t = m / a.Wd;
+      const int y = a.y0 + t % R;
+      const int b = t / R;
+      const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int n = n0 + wn + 32 * j + col;
+        if (n >= a.N) continue;
+        float val = acc[i][j][v];
+        if (DGRAD) {
+          float *d = (float *)a.dst.p + off + n;
+          *d += val;
+        } else {
+          if (a.scale) val = val * a.scale[n] + a.shift[n];
+          if (a.relu) val = val > 0.f ? val : 0.f;
+          stf((T *)a.dst.p + off + n, val);
+          if (a.mask)
+            a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n] =
+                val > 0.f ? 1 : 0;
+        }
+      }
+    }
+  }
+}
+
+template <typename T, bool DGRAD>
+static int conv_dispatch(const ConvArgs &a, hipStream_t s) {
+  const int M = a.B * (a.y1 - a.y0) * a.Wd;
+  if (M <= 0 || a.N <= 0) return 0;
+  const bool vec = (a.KC % Cfg<T>::E) == 0;
+  const int bn = a.N <= 64 ? 64 : 128;
+  dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn);
+  if (bn == 64) {
+    if (vec) conv_gemm_kernel<T, 64, DGRAD, true><<<grid, 256, 0, s>>>(a);
+    else conv_gemm_kernel<T, 64, DGRAD, false><<<grid, 256, 0, s>>>(a);
+  } else {
+    if (vec) conv_gemm_kernel<T, 128, DGRAD, true><<<grid, 256, 0, s>>>(a);
+    else conv_gemm_kernel<T, 128, DGRAD, false><<<grid, 256, 0, s>>>(a);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream) {
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    return dgrad ? conv_dispatch<float, true>(a, s) : conv_dispatch<float, false>(a, s);
+  return dgrad ? conv_dispatch<bf16, true>(a, s) : conv_dispatch<bf16, false>(a, s);
+}
+
+// ------------------------------------------------------------ weight grad
+// A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
+// input pixel under tap; both are K-outer in memory, so tiles are written
+// to LDS transposed into the same [row][k] layout used above.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
+                                                    float *dw) {
+  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
+  constexpr int BN = 128, NB = 2;
+  constexpr int RV = BM / E;        // 16-byte vectors per 128-wide tile row
+  constexpr int KS = 256 / RV;      // pixels loaded per pass
+  __shared__ __align__(16) T As[2][BM * LDK];
+  __shared__ __align__(16) T Bs[2][BN * LDK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int R = a.y1 - a.y0;
+  const int K = a.B * R * a.Wv;
+  const int taps = a.kh * a.kw;
+  const int N = taps * a.Ci;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int kbeg = blockIdx.z * kchunk;
+  const int kend = min(K, kbeg + kchunk);
+  const int rv = tid % RV, kk0 = tid / RV;
+  const T *dc = (const T *)a.dc;
+  const T *src = (const T *)a.src.p;
+  const long long srow = (long long)a.src.W * a.src.C;
+
+  // this thread's B columns n0 + rv*E + e: (tap, channel) of each element
+  const int nb0 = n0 + rv * E;
+  int tapv = nb0 / a.Ci, cv = nb0 - (nb0 / a.Ci) * a.Ci;
+  const int tiv = tapv / a.kw, tjv = tapv - (tapv / a.kw) * a.kw;
+  const int ov = m0 + rv * E;
+
+  T ra[2][E], rb[2][E];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int p = k0 + kk0 + KS * i;
+      const bool pk = p < kend;
+      // A: E output channels of pixel p
+      if (VEC) {
+        uint4 u = (pk && ov < a.Co) ? *(const uint4 *)(dc + (long long)p * a.Co + ov)
+                                    : make_uint4(0, 0, 0, 0);
+        *(uint4 *)ra[i] = u;
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          ra[i][e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
+      }
+      // B: E input values of pixel p under the column's tap
+      int x = 0, y = 0, b = 0;
+      if (pk) {
+        x = p % a.Wv;
+        int t = p / a.Wv;
+        y = a.y0 + t % R;
+        b = t / R;
+      }
+      if (VEC) {
+        int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
+        bool ok = pk && nb0 < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
+        uint4 u = make_uint4(0, 0, 0, 0);
+        if (ok)
+          u = *(const uint4 *)(src + b * a.src.bs + (sy - a.src.row0) * srow +
+                               (long long)sx * a.src.C + cv);
+        *(uint4 *)rb[i] = u;
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int n = nb0 + e;
+          const int tap = n / a.Ci, c = n - (n / a.Ci) * a.Ci;
+          const int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
+          const int sy = y * a.sh - a.ph + ti, sx = x * a.sw - a.pw + tj;
+          const bool ok = pk && n < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
+          rb[i][e] = ok ? src[b * a.src.bs + (sy - a.src.row0) * srow +
+                              (long long)sx * a.src.C + c]
+                        : (T)0;
+        }
+      }
+    }
+  };
+
+  f32x16 acc[2][NB];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
+  const int KT = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (KT > 0) gload(kbeg);
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        As[buf][(rv * E + e) * LDK + kk0 + KS * i] = ra[i][e];
+        Bs[buf][(rv * E + e) * LDK + kk0 + KS * i] = rb[i][e];
+      }
+    __syncthreads();
+    if (kt + 1 < KT) gload(kbeg + (kt + 1) * BK);
+    mma_tile<BN>(As[buf], Bs[buf], acc, wm, wn, lane);
+  }
+
+  const int col = lane & 31;
+  float *out = gridDim.z == 1 ? dw : a.out + (long long)blockIdx.z * a.Co * N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + wm + 32 * i + acc_row(v, lane);
+      if (m >= a.Co) continue;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int n = n0 + wn + 32 * j + col;
+        if (n >= N) continue;
+        float *d = out + (long long)m * N + n;
+        if (gridDim.z == 1) *d += acc[i][j][v];
+        else *d = acc[i][j][v];
+      }
+    }
+}
+
+// dW += sum over splits, in split order (deterministic).
+__global__ void wgrad_reduce_kernel(const float *part, float *dw, long long mn,
+                                    int splits) {
+  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= mn) return;
+  float s = 0.f;
+  for (int z = 0; z < splits; ++z) s += part[z * mn + i];
+  dw[i] += s;
+}
+
+template <typename T>
+static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
+  const int K = a.B * (a.y1 - a.y0) * a.Wv;
+  const int N = a.kh * a.kw * a.Ci;
+  if (K <= 0) return 0;
+  constexpr int BK = Cfg<T>::BK;
+  int splits = a.splits < 1 ? 1 : a.splits;
+  int kchunk = (K + splits - 1) / splits;
+  kchunk = (kchunk + BK - 1) / BK * BK;
+  splits = (K + kchunk - 1) / kchunk;
+  const bool vec = (a.Co % Cfg<T>::E) == 0 && (a.Ci % Cfg<T>::E) == 0;
+  dim3 grid((a.Co + BM - 1) / BM, (N + 127) / 128, splits);
+  if (vec) wgrad_kernel<T, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  else wgrad_kernel<T, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  if (splits > 1) {
+    long long mn = (long long)a.Co * N;
+    wgrad_reduce_kernel<<<(unsigned)((mn + 255) / 256), 256, 0, s>>>(a.out, dw, mn, splits);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream) {
+  hipStream_t s = (hipStream_t)stream;
+  return dt == DT_F32 ? wgrad_dispatch<float>(a, dw, s) : wgrad_dispatch<bf16>(a, dw, s);
+}
+
+// ------------------------------------------------------------- max-pool
+template <typename T>
+__global__ void pool_fwd_kernel(PoolArgs a) {
+  const int R = a.y1 - a.y0;
+  const long long total = (long long)a.B * R * a.Wd * a.C;
+  const long long srow = (long long)a.src.W * a.src.C;
+  const long long drow = (long long)a.Wd * a.C;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % a.C);
+    long long t = idx / a.C;
+    const int x = (int)(t % a.Wd);
+    t /= a.Wd;
+    const int yy = (int)(t % R);
+    const int b = (int)(t / R);
+    const int y = a.y0 + yy;
+    const T *src = (const T *)a.src.p + b * a.src.bs;
+    float best = 0.f;
+    int bi = 0;
+    for (int i = 0; i < a.kh; ++i) {
+      const int sy = y * a.sh - a.ph + i;
+      for (int j = 0; j < a.kw; ++j) {
+        const int sx = x * a.sw - a.pw + j;
+        float v = -__builtin_huge_valf();
+        if (sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws)
+          v = ldf(src + (sy - a.src.row0) * srow + (long long)sx * a.src.C + c);
+        const int tp = i * a.kw + j;
+        if (tp == 0 || v > best) {
+          best = v;
+          bi = tp;
+        }
+      }
+    }
+    T *dst = (T *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.C + c;
+    stf(dst, best);
+    if (a.am) a.am[idx] = (uint8_t)bi;
+    if (a.mask)
+      a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.C + c] = (uint8_t)bi;
+  }
+}
+
+static unsigned grid_for(long long total) {
+  long long g = (total + 255) / 256;
+  if (g > 65536) g = 65536;
+  return (unsigned)(g < 1 ? 1 : g);
+}
+
+int launch_pool_fwd(int dt, const PoolArgs &a, void *stream) {
+  const long long total = (long long)a.B * (a.y1 - a.y0) * a.Wd * a.C;
+  if (total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32) pool_fwd_kernel<float><<<grid_for(total), 256, 0, s>>>(a);
+  else pool_fwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(a);
+  return (int)hipGetLastError();
+}
+
+__global__ void pool_bwd_kernel(PoolBwdArgs a) {
+  const int Ru = a.ub - a.ua, R = a.y1 - a.y0;
+  const long long total = (long long)a.B * Ru * a.Wu * a.C;
+  const long long vrow = (long long)a.Wv * a.C, urow = (long long)a.Wu * a.C;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % a.C);
+    long long t = idx / a.C;
+    const int xi = (int)(t % a.Wu);
+    t /= a.Wu;
+    const int yi = a.ua + (int)(t % Ru);
+    const int b = (int)(t / Ru);
+    // windows y with y*sh - ph <= yi < y*sh - ph + kh, inside [y0, y1)
+    const int ylo = max(a.y0, fdiv(yi + a.ph - a.kh, a.sh) + 1);
+    const int yhi = min(a.y1 - 1, fdiv(yi + a.ph, a.sh));
+    const int xlo = max(0, fdiv(xi + a.pw - a.kw, a.sw) + 1);
+    const int xhi = min(a.Wv - 1, fdiv(xi + a.pw, a.sw));
+    float sum = 0.f;
+    for (int y = ylo; y <= yhi; ++y)
+      for (int x = xlo; x <= xhi; ++x) {
+        const int tp = (yi - (y * a.sh - a.ph)) * a.kw + (xi - (x * a.sw - a.pw));
+        const long long ai = (((long long)b * R + (y - a.y0)) * a.Wv + x) * a.C + c;
+        if (a.am[ai] == tp)
+          sum += ((const float *)a.dv.p)[b * a.dv.bs + (y - a.dv.row0) * vrow +
+                                         (long long)x * a.C + c];
+      }
+    float *d = (float *)a.du.p + b * a.du.bs + (yi - a.du.row0) * urow + (long long)xi * a.C + c;
+    *d += sum;
+  }
+}
+
+int launch_pool_bwd(const PoolBwdArgs &a, void *stream) {
+  const long long total = (long long)a.B * (a.ub - a.ua) * a.Wu * a.C;
+  if (total <= 0) return 0;
+  pool_bwd_kernel<<<grid_for(total), 256, 0, (hipStream_t)stream>>>(a);
+  return (int)hipGetLastError();
+}
+
+// ------------------------------------------------------- elementwise rows
+struct RowIdx {
+  long long off;  // element offset of (b, row, inner) in a view
+};
+
+__device__ __forceinline__ long long view_off(const View &v, int b, int row,
+                                              int inner) {
+  return b * v.bs + (long long)(row - v.row0) * v.W * v.C + inner;
+}
+
+template <typename T>
+__global__ void add_fwd_kernel(View a, View bb, View z, int relu, uint8_t *mask,
+                               int mask_h, int B, int y0, int y1, int W, int C) {
+  const int R = y1 - y0;
+  const long long inner = (long long)W * C;
+  const long long total = (long long)B * R * inner;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int in = (int)(idx % inner);
+    const long long t = idx / inner;
+    const int y = y0 + (int)(t % R);
+    const int b = (int)(t / R);
+    float v = ldf((const T *)a.p + view_off(a, b, y, in)) +
+              ldf((const T *)bb.p + view_off(bb, b, y, in));
+    if (relu) v = v > 0.f ? v : 0.f;
+    stf((T *)z.p + view_off(z, b, y, in), v);
+    if (mask) mask[((long long)b * mask_h + y) * inner + in] = v > 0.f ? 1 : 0;
+  }
+}
+
+int launch_add_fwd(int dt, View a, View b, View z, int relu, uint8_t *mask,
+                   int mask_h, int B, int y0, int y1, int W, int C, void *stream) {
+  const long long total = (long long)B * (y1 - y0) * W * C;
+  if (total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    add_fwd_kernel<float><<<grid_for(total), 256, 0, s>>>(a, b, z, relu, mask, mask_h, B, y0, y1, W, C);
+  else
+    add_fwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(a, b, z, relu, mask, mask_h, B, y0, y1, W, C);
+  return (int)hipGetLastError();
+}
+
+template <typename T>
+__global__ void add_bwd_kernel(View dz, View z, View da, View db, int relu, int B,
+                               int y0, int y1, int W, int C) {
+  const int R = y1 - y0;
+  const long long inner = (long long)W * C;
+  const long long total = (long long)B * R * inner;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int in = (int)(idx % inner);
+    const long long t = idx / inner;
+    const int y = y0 + (int)(t % R);
+    const int b = (int)(t / R);
+    float d = ((const float *)dz.p)[view_off(dz, b, y, in)];
+    if (relu && !(ldf((const T *)z.p + view_off(z, b, y, in)) > 0.f)) d = 0.f;
+    ((float *)da.p)[view_off(da, b, y, in)] += d;
+    ((float *)db.p)[view_off(db, b, y, in)] += d;
+  }
+}
+
+int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
+                   int y0, int y1, int W, int C, void *stream) {
+  const long long total = (long long)B * (y1 - y0) * W * C;
+  if (total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    add_bwd_kernel<float><<<grid_for(total), 256, 0, s>>>(dz, z, da, db, relu, B, y0, y1, W, C);
+  else
+    add_bwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(dz, z, da, db, relu, B, y0, y1, W, C);
+  return (int)hipGetLastError();
+}
+
+template <typename T>
+__global__ void act_bwd_kernel(View dz, View z, const float *scale, int relu,
+                               T *dc, int B, int y0, int y1, int W, int C) {
+  const int R = y1 - y0;
+  const long long inner = (long long)W * C;
+  const long long total = (long long)B * R * inner;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int in = (int)(idx % inner);
+    const long long t = idx / inner;
+    const int y = y0 + (int)(t % R);
+    const int b = (int)(t / R);
+    float d = ((const float *)dz.p)[view_off(dz, b, y, in)];
+    if (relu && !(ldf((const T *)z.p + view_off(z, b, y, in)) > 0.f)) d = 0.f;
+    if (scale) d *= scale[in % C];
+    stf(dc + idx, d);
+  }
+}
+
+int launch_act_bwd(int dt, View dz, View z, const float *scale, int relu,
+                   void *dc, int B, int y0, int y1, int W, int C, void *stream) {
+  const long long total = (long long)B * (y1 - y0) * W * C;
+  if (total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    act_bwd_kernel<float><<<grid_for(total), 256, 0, s>>>(dz, z, scale, relu, (float *)dc, B, y0, y1, W, C);
+  else
+    act_bwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, B, y0, y1, W, C);
+  return (int)hipGetLastError();
+}
+
+template <typename TS, typename TD>
+__global__ void rows_copy_kernel(View src, View dst, int accumulate, int B,
+                                 int r0, int r1, int W, int C) {
+  const int R = r1 - r0;
+  const long long inner = (long long)W * C;
+  const long long total = (long long)B * R * inner;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int in = (int)(idx % inner);
+    const long long t = idx / inner;
+    const int y = r0 + (int)(t % R);
+    const int b = (int)(t / R);
+    float v = ldf((const TS *)src.p + view_off(src, b, y, in));
+    TD *d = (TD *)dst.p + view_off(dst, b, y, in);
+    if (accumulate) v += ldf(d);
+    stf(d, v);
+  }
+}
+
+int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate, int B,
+                     int r0, int r1, int W, int C, void *stream) {
+  const long long total = (long long)B * (r1 - r0) * W * C;
+  if (total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  unsigned g = grid_for(total);
+  if (st == DT_F32 && dtt == DT_F32)
+    rows_copy_kernel<float, float><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
+  else if (st == DT_F32)
+    rows_copy_kernel<float, bf16><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
+  else if (dtt == DT_F32)
+    rows_copy_kernel<bf16, float><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
+  else
+    rows_copy_kernel<bf16, bf16><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
+  return (int)hipGetLastError();
+}
+
+__global__ void rows_zero_kernel(View dst, int B, int r0, int r1, int W, int C) {
+  const int R = r1 - r0;
+  const long long inner = (long long)W * C;
+  const long long total = (long long)B * R * inner;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int in = (int)(idx % inner);
+    const long long t = idx / inner;
+    const int y = r0 + (int)(t % R);
+    const int b = (int)(t / R);
+    ((float *)dst.p)[view_off(dst, b, y, in)] = 0.f;
+  }
+}
+
+int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C, void *stream) {
+  const long long total = (long long)B * (r1 - r0) * W * C;
+  if (total <= 0) return 0;
+  rows_zero_kernel<<<grid_for(total), 256, 0, (hipStream_t)stream>>>(dst, B, r0, r1, W, C);
+  return (int)hipGetLastError();
+}
+
+__global__ void zero_kernel(float *p, long long n) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (long long)gridDim.x * blockDim.x)
+    p[i] = 0.f;
+}
+
+int launch_zero_f32(float *p, size_t n, void *stream) {
+  if (n == 0) return 0;
+  zero_kernel<<<grid_for((long long)n), 256, 0, (hipStream_t)stream>>>(p, (long long)n);
+  return (int)hipGetLastError();
+}
+
+template <typename T>
+__global__ void wtranspose_kernel(const T *w, T *wt, int co, int taps, int ci) {
+  const long long total = (long long)co * taps * ci;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % ci);
+    const long long t = i / ci;
+    const int tap = (int)(t % taps);
+    const int o = (int)(t / taps);
+    wt[((long long)tap * ci + c) * co + o] = w[i];
+  }
+}
+
+int launch_wtranspose(int dt, const void *w, void *wt, int co, int taps, int ci,
+                      void *stream) {
+  const long long total = (long long)co * taps * ci;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    wtranspose_kernel<float><<<grid_for(total), 256, 0, s>>>((const float *)w, (float *)wt, co, taps, ci);
+  else
+    wtranspose_kernel<bf16><<<grid_for(total), 256, 0, s>>>((const bf16 *)w, (bf16 *)wt, co, taps, ci);
+  return (int)hipGetLastError();
+}
+
+}  // namespace lrcnn

@@ -1,0 +1,538 @@
+// Planner: shapes, per-band row intervals, workspace layout and analytic
+// figures. Host only (no HIP calls), so it runs without a GPU.
+#include <algorithm>
+#include <climits>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "plan.hpp"
+
+namespace {
+thread_local std::string g_err;
+
+int floordiv(int a, int b) { return (a >= 0) ? a / b : -((-a + b - 1) / b); }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Alloc {
+  size_t top = 0;
+  size_t take(size_t bytes) {
+    size_t off = top;
+    top = align256(top + bytes);
+    return off;
+  }
+};
+}  // namespace
+
+int lrcnn_fail(int code, const std::string &msg) {
+  g_err = msg;
+  return code;
+}
+
+extern "C" const char *lrcnn_last_error(void) { return g_err.c_str(); }
+
+namespace lrcnn {
+
+// k, s, p of the window through which node v reads its input(s); an ADD
+// reads row y of each input for output row y.
+static void ksp(const lrcnn_node &nd, int &k, int &s, int &p) {
+  if (nd.op == LRCNN_OP_ADD) {
+    k = 1, s = 1, p = 0;
+  } else {
+    k = nd.kh, s = nd.sh, p = nd.ph;
+  }
+}
+
+int wgrad_splits(int64_t m, int64_t n, int64_t k) {
+  const int64_t bm = 128, bn = 128, min_k = 256, target = 1024;
+  int64_t tiles = ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
+  int64_t s = (target + tiles - 1) / tiles;
+  s = std::min<int64_t>(s, std::max<int64_t>(1, k / min_k));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(s, 512));
+}
+
+// Rows of node v's output that can be computed once rows [0, f) of its
+// input exist: output row y reads input rows [y*s-p, y*s-p+k) (clipped to
+// the image, whose top and bottom are padded; Section III-B).
+static int frontier(int f, int h_in, int h_out, int k, int s, int p) {
+  if (f >= h_in) return h_out;
+  int last = floordiv(f + p - k, s);
+  return std::max(0, std::min(h_out, last + 1));
+}
+
+// CARRY intervals for the given input-row bounds.
+static void carry_rows(Plan &P, const std::vector<int> &bounds) {
+  const int n = P.n, nb = (int)bounds.size() - 1;
+  std::vector<std::vector<int>> F(nb + 1, std::vector<int>(n, 0));
+  for (int r = 1; r <= nb; ++r) {
+    F[r][0] = bounds[r];
+    for (int v = 1; v < n; ++v) {
+      const lrcnn_node &nd = P.nodes[v];
+      if (nd.op == LRCNN_OP_ADD) {
+        F[r][v] = std::min(F[r][nd.in0], F[r][nd.in1]);
+      } else {
+        int k, s, p;
+        ksp(nd, k, s, p);
+        F[r][v] = frontier(F[r][nd.in0], P.shp[nd.in0].h, P.shp[v].h, k, s, p);
+      }
+    }
+  }
+  // first row of v that a later band may still read: consumers' next rows
+  // start at F[r][c], whose windows begin at F[r][c]*s - p
+  std::vector<std::vector<int>> T(nb + 1, std::vector<int>(n, 0));
+  for (int r = 1; r <= nb; ++r)
+    for (int v = 0; v < n; ++v) {
+      int t = F[r][v];
+      for (int c : P.cons[v]) {
+        int k, s, p;
+        ksp(P.nodes[c], k, s, p);
+        t = std::min(t, F[r][c] * s - p);
+      }
+      T[r][v] = std::max(0, std::min(t, F[r][v]));
+    }
+  P.rows.assign(nb, std::vector<Rows>(n));
+  P.tail.assign(nb, std::vector<int>(n));
+  for (int r = 1; r <= nb; ++r)
+    for (int v = 0; v < n; ++v) {
+      P.rows[r - 1][v] = Rows{F[r - 1][v], F[r][v], T[r - 1][v], F[r][v]};
+      P.tail[r - 1][v] = T[r][v];
+    }
+}
+
+// RECOMPUTE cones for the given output-row bounds (Eq. (15) read as an
+// interval recursion from the last layer down to the input).
+static void cone_rows(Plan &P, const std::vector<int> &bounds) {
+  const int n = P.n, nb = (int)bounds.size() - 1;
+  P.rows.assign(nb, std::vector<Rows>(n));
+  for (int r = 0; r < nb; ++r) {
+    std::vector<int> lo(n, 0), hi(n, 0);
+    lo[n - 1] = bounds[r];
+    hi[n - 1] = bounds[r + 1];
+    for (int v = n - 2; v >= 0; --v) {
+      int a = INT_MAX, b = INT_MIN;
+      for (int c : P.cons[v]) {
+        if (hi[c] <= lo[c]) continue;
+        int k, s, p;
+        ksp(P.nodes[c], k, s, p);
+        a = std::min(a, std::max(0, lo[c] * s - p));
+        b = std::max(b, std::min(P.shp[v].h, (hi[c] - 1) * s - p + k));
+      }
+      if (a == INT_MAX || b <= a) {
+        lo[v] = hi[v] = 0;
+      } else {
+        lo[v] = a;
+        hi[v] = b;
+      }
+    }
+    for (int v = 0; v < n; ++v) P.rows[r][v] = Rows{lo[v], hi[v], lo[v], hi[v]};
+  }
+}
+
+// Largest per-band cache (bytes of all held rows) for CARRY bounds.
+static double max_band_cache(Plan &P, const std::vector<int> &bounds) {
+  carry_rows(P, bounds);
+  double best = 0;
+  for (auto &br : P.rows) {
+    double tot = 0;
+    for (int v = 1; v < P.n; ++v)
+      tot += (double)P.elems(v, br[v].hi - br[v].lo) * P.es;
+    best = std::max(best, tot);
+  }
+  return best;
+}
+
+// BALANCED: smallest bound on the per-band cache that N bands can meet,
+// found by bisection; each band is extended greedily as far as the bound
+// allows (a band's cache grows with its end row and shrinks with its start
+// row, so the greedy extension is optimal).
+static std::vector<int> balanced_bounds(Plan &P, int H, int nb) {
+  auto cache_of = [&](int a, int b) {
+    std::vector<int> bd = {0, a, b, H};
+    if (a == 0) bd = {0, b, H};
+    carry_rows(P, bd);
+    const auto &br = P.rows[a == 0 ? 0 : 1];
+    double tot = 0;
+    for (int v = 1; v < P.n; ++v)
+      tot += (double)P.elems(v, br[v].hi - br[v].lo) * P.es;
+    return tot;
+  };
+  auto greedy = [&](double cap, std::vector<int> &out) {
+    out.assign(1, 0);
+    int a = 0;
+    for (int r = 0; r < nb && a < H; ++r) {
+      if (r == nb - 1) {
+        if (cache_of(a, H) > cap) return false;
+        a = H;
+        out.push_back(H);
+        break;
+      }
+      int lo = a, hi = H;  // largest b with cache_of(a, b) <= cap
+      while (lo < hi) {
+        int mid = lo + (hi - lo + 1) / 2;
+        if (cache_of(a, mid) <= cap) lo = mid; else hi = mid - 1;
+      }
+      a = lo;
+      out.push_back(a);
+    }
+    if (a < H) return false;
+    while ((int)out.size() < nb + 1) out.push_back(H);
+    return true;
+  };
+  std::vector<int> even(nb + 1), cur;
+  for (int r = 0; r <= nb; ++r) even[r] = (int)((int64_t)r * H / nb);
+  double hi = max_band_cache(P, even), lo = 0;
+  std::vector<int> best = even;
+  for (int it = 0; it < 60 && hi - lo > 1.0; ++it) {
+    double mid = 0.5 * (lo + hi);
+    if (greedy(mid, cur)) {
+      hi = mid;
+      best = cur;
+    } else {
+      lo = mid;
+    }
+  }
+  return best;
+}
+
+static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
+  if (!nodes || !cfg) return lrcnn_fail(LRCNN_EINVAL, "null nodes or config");
+  if (n < 2) return lrcnn_fail(LRCNN_ESHAPE, "need an input node and at least one layer");
+  if (nodes[0].op != LRCNN_OP_INPUT)
+    return lrcnn_fail(LRCNN_ESHAPE, "node 0 must be the input");
+  if (cfg->batch < 1 || cfg->in_c < 1 || cfg->in_h < 1 || cfg->in_w < 1)
+    return lrcnn_fail(LRCNN_ESHAPE, "batch and input sizes must be positive");
+  if (cfg->dtype != LRCNN_F32 && cfg->dtype != LRCNN_BF16)
+    return lrcnn_fail(LRCNN_EDTYPE, "dtype must be LRCNN_F32 or LRCNN_BF16");
+  if (cfg->mode != LRCNN_CARRY && cfg->mode != LRCNN_RECOMPUTE)
+    return lrcnn_fail(LRCNN_EINVAL, "mode must be LRCNN_CARRY or LRCNN_RECOMPUTE");
+  if (cfg->n_bands < 1) return lrcnn_fail(LRCNN_EPARTITION, "n_bands must be >= 1");
+  if (cfg->policy < LRCNN_EVEN || cfg->policy > LRCNN_EXPLICIT)
+    return lrcnn_fail(LRCNN_EINVAL, "bad partition policy");
+  if (cfg->policy == LRCNN_BALANCED && cfg->mode != LRCNN_CARRY)
+    return lrcnn_fail(LRCNN_EINVAL, "BALANCED applies to CARRY mode only");
+  if (cfg->policy == LRCNN_EXPLICIT && !cfg->bounds)
+    return lrcnn_fail(LRCNN_EINVAL, "EXPLICIT policy needs bounds");
+  for (int v = 1; v < n; ++v) {
+    const lrcnn_node &d = nodes[v];
+    std::string at = "node " + std::to_string(v) + ": ";
+    if (d.op < LRCNN_OP_CONV || d.op > LRCNN_OP_ADD)
+      return lrcnn_fail(LRCNN_ESHAPE, at + "bad op");
+    if (d.in0 < 0 || d.in0 >= v)
+      return lrcnn_fail(LRCNN_ESHAPE, at + "in0 must name an earlier node");
+    if (d.op == LRCNN_OP_ADD && (d.in1 < 0 || d.in1 >= v))
+      return lrcnn_fail(LRCNN_ESHAPE, at + "in1 must name an earlier node");
+    if (d.op == LRCNN_OP_CONV || d.op == LRCNN_OP_MAXPOOL) {
+      if (d.kh < 1 || d.kw < 1 || d.sh < 1 || d.sw < 1 || d.ph < 0 || d.pw < 0 ||
+          d.ph >= d.kh || d.pw >= d.kw)
+        return lrcnn_fail(LRCNN_ESHAPE, at + "need k >= 1, s >= 1, 0 <= p < k");
+    }
+    if (d.op == LRCNN_OP_CONV && d.c_out < 1)
+      return lrcnn_fail(LRCNN_ESHAPE, at + "c_out must be >= 1");
+    if (d.op == LRCNN_OP_MAXPOOL && d.kh * d.kw > 255)
+      return lrcnn_fail(LRCNN_ESHAPE, at + "pool window larger than 255");
+  }
+  return LRCNN_OK;
+}
+
+// Interval first-fit packing of buffers with [start, end] live steps.
+struct LiveBuf {
+  int start, end;
+  size_t bytes;
+  size_t off;
+};
+
+static size_t pack(std::vector<LiveBuf> &bufs) {
+  std::vector<int> order(bufs.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = (int)i;
+  std::sort(order.begin(), order.end(), [&](int a, int b) {
+    return bufs[a].bytes != bufs[b].bytes ? bufs[a].bytes > bufs[b].bytes : a < b;
+  });
+  std::vector<int> placed;
+  size_t peak = 0;
+  for (int i : order) {
+    LiveBuf &b = bufs[i];
+    // candidate offsets: 0 and the end of every overlapping placed buffer
+    std::vector<size_t> cand = {0};
+    for (int j : placed) {
+      const LiveBuf &o = bufs[j];
+      if (o.end < b.start || b.end < o.start) continue;
+      cand.push_back(align256(o.off + o.bytes));
+    }
+    std::sort(cand.begin(), cand.end());
+    for (size_t c : cand) {
+      bool ok = true;
+      for (int j : placed) {
+        const LiveBuf &o = bufs[j];
+        if (o.end < b.start || b.end < o.start) continue;
+        if (c < o.off + o.bytes && o.off < c + b.bytes) { ok = false; break; }
+      }
+      if (ok) { b.off = c; break; }
+    }
+    placed.push_back(i);
+    peak = std::max(peak, align256(b.off + b.bytes));
+  }
+  return peak;
+}
+
+// Lay out one workspace. `cap[v]` = window rows; `own[v]` = most rows a band
+// owns; `carry[v]` = rows of carried error (CARRY only); strips per band.
+static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
+                   const std::vector<int> &own, const std::vector<int> &carry,
+                   bool strips, bool layerwise, bool dxacc) {
+  const int n = P.n;
+  Alloc A;
+  L = Layout();
+  L.win.assign(n, 0);
+  L.win_cap = cap;
+  L.argmax.assign(n, 0);
+  L.argmax_cap.assign(n, 0);
+  L.delta.assign(n, 0);
+  L.carry.assign(n, 0);
+  L.carry_cap = carry;
+  L.strip.assign(P.nb, std::vector<size_t>(n, 0));
+  if (strips) {
+    size_t s0 = A.top;
+    for (int r = 0; r + 1 < P.nb; ++r)
+      for (int v = 1; v < n; ++v) {
+        int rows_ = P.rows[r][v].b - P.tail[r][v];
+        if (rows_ > 0) L.strip[r][v] = A.take(P.elems(v, rows_) * P.es);
+      }
+    L.strip_bytes = A.top - s0;
+  }
+  size_t c0 = A.top;
+  for (int v = 1; v < n; ++v) {
+    if (layerwise && v == n - 1) continue;  // the output node lives in y
+    L.win[v] = A.take(P.elems(v, cap[v]) * P.es);
+  }
+  L.cache_bytes = A.top - c0;
+  for (int v = 1; v < n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_MAXPOOL) {
+      L.argmax_cap[v] = own[v];
+      L.argmax[v] = A.take(P.elems(v, own[v]));
+    }
+  size_t k0 = A.top;
+  for (int v = 0; v < n; ++v)
+    if (carry[v] > 0) L.carry[v] = A.take(P.elems(v, carry[v]) * 4);
+  L.carry_bytes = A.top - k0;
+  // error windows: node v's window is live from the step of its first
+  // consumer in reverse order (the largest consumer id) to its own step
+  std::vector<LiveBuf> bufs(n);
+  for (int v = 0; v < n; ++v) {
+    int first = (v == n - 1) ? v : v;
+    for (int c : P.cons[v]) first = std::max(first, c);
+    bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, cap[v]) * 4, 0};
+  }
+  size_t dpeak = pack(bufs);
+  size_t d0 = A.take(dpeak);
+  for (int v = 0; v < n; ++v) L.delta[v] = d0 + bufs[v].off;
+  L.delta_bytes = dpeak;
+  size_t dc = 0, wt = 0;
+  for (int v = 1; v < n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_CONV) {
+      dc = std::max(dc, P.elems(v, own[v]) * P.es);
+      const lrcnn_node &d = P.nodes[v];
+      wt = std::max(wt, (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c * P.es);
+    }
+  L.dc_bytes = dc;
+  L.dc = A.take(dc);
+  L.wt_bytes = wt;
+  L.wt = A.take(wt);
+  size_t part = 0;
+  std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
+  splits.assign(n, 1);
+  for (int v = 1; v < n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_CONV) {
+      const lrcnn_node &d = P.nodes[v];
+      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * P.shp[d.in0].c;
+      int64_t k = (int64_t)P.cfg.batch * own[v] * P.shp[v].w;
+      int s = wgrad_splits(m, nn, k);
+      splits[v] = s;
+      if (s > 1) part = std::max(part, (size_t)s * m * nn * 4);
+    }
+  L.part_bytes = part;
+  L.part = A.take(part);
+  if (dxacc) {
+    L.dxacc_bytes = P.elems(0, P.shp[0].h) * 4;
+    L.dxacc = A.take(L.dxacc_bytes);
+  }
+  L.total = std::max<size_t>(A.top, 256);
+}
+
+static int build(Plan &P) {
+  const int n = P.n;
+  // shapes
+  P.shp.assign(n, Shape{});
+  P.shp[0] = Shape{P.cfg.in_h, P.cfg.in_w, P.cfg.in_c};
+  for (int v = 1; v < n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    const Shape &u = P.shp[d.in0];
+    std::string at = "node " + std::to_string(v) + ": ";
+    if (d.op == LRCNN_OP_ADD) {
+      const Shape &u1 = P.shp[d.in1];
+      if (u1.h != u.h || u1.w != u.w || u1.c != u.c)
+        return lrcnn_fail(LRCNN_ESHAPE, at + "ADD inputs differ in shape");
+      P.shp[v] = u;
+    } else {
+      int ho = floordiv(u.h + 2 * d.ph - d.kh, d.sh) + 1;
+      int wo = floordiv(u.w + 2 * d.pw - d.kw, d.sw) + 1;
+      if (ho < 1 || wo < 1) return lrcnn_fail(LRCNN_ESHAPE, at + "empty output");
+      P.shp[v] = Shape{ho, wo, d.op == LRCNN_OP_CONV ? d.c_out : u.c};
+    }
+  }
+  P.cons.assign(n, {});
+  for (int v = 1; v < n; ++v) {
+    P.cons[P.nodes[v].in0].push_back(v);
+    if (P.nodes[v].op == LRCNN_OP_ADD) P.cons[P.nodes[v].in1].push_back(v);
+  }
+  for (int v = 0; v + 1 < n; ++v)
+    if (P.cons[v].empty())
+      return lrcnn_fail(LRCNN_ESHAPE, "node " + std::to_string(v) +
+                                          " feeds nothing (only the last node is an output)");
+  // bounds
+  const bool carry = P.cfg.mode == LRCNN_CARRY;
+  const int H = carry ? P.shp[0].h : P.shp[n - 1].h;
+  const int nb = P.cfg.n_bands;
+  P.nb = nb;
+  std::vector<int> bd(nb + 1);
+  if (P.cfg.policy == LRCNN_EXPLICIT) {
+    for (int r = 0; r <= nb; ++r) bd[r] = P.cfg.bounds[r];
+    if (bd[0] != 0 || bd[nb] != H)
+      return lrcnn_fail(LRCNN_EPARTITION, "bounds must run from 0 to " + std::to_string(H));
+    for (int r = 0; r < nb; ++r)
+      if (bd[r + 1] < bd[r]) return lrcnn_fail(LRCNN_EPARTITION, "bounds must be non-decreasing");
+  } else if (P.cfg.policy == LRCNN_BALANCED) {
+    bd = balanced_bounds(P, H, nb);
+  } else {
+    for (int r = 0; r <= nb; ++r) bd[r] = (int)((int64_t)r * H / nb);
+  }
+  P.bounds = bd;
+  if (carry) carry_rows(P, bd); else cone_rows(P, bd);
+  // capacities
+  std::vector<int> cap(n, 0), own(n, 0), cry(n, 0);
+  for (int r = 0; r < nb; ++r)
+    for (int v = 0; v < n; ++v) {
+      const Rows &q = P.rows[r][v];
+      cap[v] = std::max(cap[v], q.hi - q.lo);
+      own[v] = std::max(own[v], q.b - q.a);
+      if (carry) cry[v] = std::max(cry[v], q.b - P.tail[r][v]);
+    }
+  layout(P, P.rc, cap, own, cry, carry, false,
+         !carry && P.cfg.dtype == LRCNN_BF16);
+  std::vector<int> full(n), zero(n, 0);
+  for (int v = 0; v < n; ++v) full[v] = P.shp[v].h;
+  layout(P, P.lw, full, full, zero, false, true, false);
+  // FLOPs: tau of Section IV-B, and the row-centric total
+  P.tau = 0;
+  double cone = 0;
+  for (int v = 1; v < n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_CONV) {
+      const lrcnn_node &d = P.nodes[v];
+      double per_row = 2.0 * d.kh * d.kw * P.cfg.batch * P.shp[d.in0].c * d.c_out * P.shp[v].w;
+      P.tau += per_row * P.shp[v].h;
+      for (int r = 0; r < nb; ++r) cone += per_row * (P.rows[r][v].b - P.rows[r][v].a);
+    }
+  P.flops_rows = 4.0 * cone;  // FP, BP recompute, input gradient, weight gradient
+  P.shared_rows = 0;
+  P.halo_rows = 0;
+  for (int r = 0; r < nb; ++r)
+    for (int v = 0; v < n; ++v) {
+      if (carry && r + 1 < nb) P.shared_rows += P.rows[r][v].b - P.tail[r][v];
+      if (!carry) P.halo_rows += P.rows[r][v].b - P.rows[r][v].a;
+    }
+  if (!carry)
+    for (int v = 0; v < n; ++v) P.halo_rows -= P.shp[v].h;
+  return LRCNN_OK;
+}
+
+}  // namespace lrcnn
+
+using lrcnn::Plan;
+
+extern "C" int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
+                          const lrcnn_config *cfg, lrcnn_plan_t **out) {
+  if (!out) return lrcnn_fail(LRCNN_EINVAL, "null output pointer");
+  *out = nullptr;
+  int st = lrcnn::validate(nodes, n_nodes, cfg);
+  if (st != LRCNN_OK) return st;
+  Plan *P = new (std::nothrow) Plan();
+  if (!P) return lrcnn_fail(LRCNN_EINVAL, "out of host memory");
+  P->nodes.assign(nodes, nodes + n_nodes);
+  P->cfg = *cfg;
+  P->cfg.bounds = nullptr;
+  P->n = n_nodes;
+  P->es = cfg->dtype == LRCNN_BF16 ? 2 : 4;
+  if (cfg->policy == LRCNN_EXPLICIT) {
+    // keep the caller's bounds only for the duration of build()
+    P->cfg.bounds = cfg->bounds;
+  }
+  st = lrcnn::build(*P);
+  P->cfg.bounds = nullptr;
+  if (st != LRCNN_OK) {
+    delete P;
+    return st;
+  }
+  *out = reinterpret_cast<lrcnn_plan_t *>(P);
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info) {
+  if (!plan || !info) return lrcnn_fail(LRCNN_EINVAL, "null plan or info");
+  const Plan &P = *reinterpret_cast<const Plan *>(plan);
+  std::memset(info, 0, sizeof(*info));
+  info->n_nodes = P.n;
+  info->n_bands = P.nb;
+  info->mode = P.cfg.mode;
+  info->dtype = P.cfg.dtype;
+  info->out_h = P.shp[P.n - 1].h;
+  info->out_w = P.shp[P.n - 1].w;
+  info->out_c = P.shp[P.n - 1].c;
+  info->workspace_bytes = P.rc.total;
+  info->layerwise_workspace_bytes = P.lw.total;
+  info->strip_bytes = P.rc.strip_bytes;
+  info->band_cache_bytes = P.rc.cache_bytes;
+  info->delta_bytes = P.rc.delta_bytes;
+  info->carry_bytes = P.rc.carry_bytes;
+  info->partial_bytes = P.rc.part_bytes;
+  double omega = 0;
+  for (int v = 1; v < P.n; ++v) omega += (double)P.elems(v, P.shp[v].h) * P.es;
+  double ybytes = (double)P.elems(P.n - 1, P.shp[P.n - 1].h) * P.es;
+  info->omega_bytes = omega;
+  info->omega_fp_bytes = (double)P.rc.strip_bytes + P.rc.cache_bytes + ybytes;
+  info->omega_bp_bytes = (double)P.rc.total + ybytes;
+  info->flops_tau = P.tau;
+  info->flops_rows = P.flops_rows;
+  info->flops_layerwise = 3.0 * P.tau;
+  info->shared_rows = P.shared_rows;
+  info->halo_rows = P.halo_rows;
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_plan_node_shape(const lrcnn_plan_t *plan, int32_t node,
+                                     int32_t shape[3]) {
+  if (!plan || !shape) return lrcnn_fail(LRCNN_EINVAL, "null argument");
+  const Plan &P = *reinterpret_cast<const Plan *>(plan);
+  if (node < 0 || node >= P.n) return lrcnn_fail(LRCNN_EINVAL, "node out of range");
+  shape[0] = P.shp[node].h;
+  shape[1] = P.shp[node].w;
+  shape[2] = P.shp[node].c;
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t band,
+                                    int32_t node, int32_t rows[4]) {
+  if (!plan || !rows) return lrcnn_fail(LRCNN_EINVAL, "null argument");
+  const Plan &P = *reinterpret_cast<const Plan *>(plan);
+  if (node < 0 || node >= P.n || band < 0 || band >= P.nb)
+    return lrcnn_fail(LRCNN_EINVAL, "band or node out of range");
+  const lrcnn::Rows &q = P.rows[band][node];
+  rows[0] = q.a;
+  rows[1] = q.b;
+  rows[2] = q.lo;
+  rows[3] = q.hi;
+  return LRCNN_OK;
+}
+
+extern "C" void lrcnn_plan_destroy(lrcnn_plan_t *plan) {
+  delete reinterpret_cast<Plan *>(plan);
+}

@@ -1,0 +1,73 @@
+// Internal plan structure shared by the planner (plan.cpp) and the band
+// executor (exec.cpp). Host memory only.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "lrcnn.h"
+
+namespace lrcnn {
+
+struct Shape {
+  int h, w, c;
+};
+
+// Rows of one node in one band: [a, b) computed and owned by the band,
+// [lo, hi) held in the band's window buffer (lo <= a, b == hi).
+struct Rows {
+  int a, b, lo, hi;
+};
+
+// Byte offsets of every buffer inside one workspace.
+struct Layout {
+  size_t total = 0;
+  std::vector<size_t> win;       // per node: feature-map window ([B][cap][W][C])
+  std::vector<int> win_cap;      // rows of each window
+  std::vector<size_t> argmax;    // per MAXPOOL node: uint8 argmax of own rows
+  std::vector<int> argmax_cap;
+  std::vector<size_t> delta;     // per node: float32 error window
+  std::vector<size_t> carry;     // per node: float32 error carried to band r-1
+  std::vector<int> carry_cap;
+  std::vector<std::vector<size_t>> strip;  // [band][node]: shared rows kept
+  size_t dc = 0, dc_bytes = 0;   // error operand of one conv (storage dtype)
+  size_t wt = 0, wt_bytes = 0;   // weights transposed for the input gradient
+  size_t part = 0, part_bytes = 0;  // weight-gradient partial sums
+  size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
+  size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;
+};
+
+struct Plan {
+  std::vector<lrcnn_node> nodes;
+  lrcnn_config cfg{};
+  int n = 0, nb = 0, es = 4;  // node count, band count, element size
+  std::vector<Shape> shp;
+  std::vector<std::vector<int>> cons;  // consumers of every node
+  std::vector<int> bounds;             // band bounds (input rows or output rows)
+  std::vector<std::vector<Rows>> rows; // [band][node]
+  std::vector<std::vector<int>> tail;  // CARRY: [band][node] first kept row
+  Layout rc;                           // row-centric workspace
+  Layout lw;                           // layer-wise workspace
+  std::vector<int> wsplit;             // per conv node: wgrad K splits (row-centric)
+  std::vector<int> wsplit_lw;          // per conv node: wgrad K splits (layer-wise)
+  double tau = 0, flops_rows = 0;
+  int64_t shared_rows = 0, halo_rows = 0;
+  // state for the FP -> BP hand-over of CARRY mode
+  const void *fwd_workspace = nullptr;
+  uint64_t fwd_epoch = 0;
+
+  size_t elems(int v, int rows_) const {
+    return (size_t)cfg.batch * rows_ * shp[v].w * shp[v].c;
+  }
+};
+
+// Weight-gradient split count for a conv with the given GEMM sizes: enough
+// workgroups to fill the chip, at least `min_k` reduction steps each.
+int wgrad_splits(int64_t m, int64_t n, int64_t k);
+
+}  // namespace lrcnn
+
+// Thread-local error reporting shared by all translation units.
+int lrcnn_fail(int code, const std::string &msg);

@@ -1,0 +1,188 @@
+"""ctypes binding of liblrcnn.so (include/lrcnn.h): argument marshalling only.
+
+Every step of row-centric training runs in the HIP library; this module
+converts Python values and torch tensors into the C ABI's plain pointers and
+sizes. Device memory comes from torch; streams are torch's current stream.
+If the library has not been built, importing this module raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblrcnn.so")
+
+OP_INPUT, OP_CONV, OP_MAXPOOL, OP_ADD = 0, 1, 2, 3
+F32, BF16 = 0, 1
+CARRY, RECOMPUTE = 0, 1
+EVEN, BALANCED, EXPLICIT = 0, 1, 2
+
+STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EPARTITION",
+          -4: "EWORKSPACE", -5: "ESTATE", -6: "EDTYPE", -7: "EHIP",
+          -8: "EINFEASIBLE"}
+
+
+class LrcnnError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class Node(C.Structure):
+    _fields_ = [(f, C.c_int32) for f in ("op", "in0", "in1", "c_out", "kh", "kw",
+                                         "sh", "sw", "ph", "pw", "affine", "relu")]
+
+
+class Config(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("in_c", C.c_int32), ("in_h", C.c_int32),
+                ("in_w", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
+                ("n_bands", C.c_int32), ("policy", C.c_int32),
+                ("bounds", C.POINTER(C.c_int32))]
+
+
+class PlanInfo(C.Structure):
+    _fields_ = [("n_nodes", C.c_int32), ("n_bands", C.c_int32), ("mode", C.c_int32),
+                ("dtype", C.c_int32), ("out_h", C.c_int32), ("out_w", C.c_int32),
+                ("out_c", C.c_int32),
+                ("workspace_bytes", C.c_size_t), ("layerwise_workspace_bytes", C.c_size_t),
+                ("strip_bytes", C.c_size_t), ("band_cache_bytes", C.c_size_t),
+                ("delta_bytes", C.c_size_t), ("carry_bytes", C.c_size_t),
+                ("partial_bytes", C.c_size_t),
+                ("omega_bytes", C.c_double), ("omega_fp_bytes", C.c_double),
+                ("omega_bp_bytes", C.c_double), ("flops_tau", C.c_double),
+                ("flops_rows", C.c_double), ("flops_layerwise", C.c_double),
+                ("shared_rows", C.c_int64), ("halo_rows", C.c_int64)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build the HIP library first "
+            "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = C.CDLL(LIB_PATH)
+    vp, sz, i32 = C.c_void_p, C.c_size_t, C.c_int32
+    pp = C.POINTER(C.c_void_p)
+    lib.lrcnn_plan.argtypes = [C.POINTER(Node), i32, C.POINTER(Config), C.POINTER(vp)]
+    lib.lrcnn_plan_query.argtypes = [vp, C.POINTER(PlanInfo)]
+    lib.lrcnn_plan_node_shape.argtypes = [vp, i32, C.POINTER(i32)]
+    lib.lrcnn_plan_band_rows.argtypes = [vp, i32, i32, C.POINTER(i32)]
+    lib.lrcnn_plan_destroy.argtypes = [vp]
+    lib.lrcnn_plan_destroy.restype = None
+    lib.lrcnn_forward_rows.argtypes = [vp, vp, pp, pp, pp, vp, vp, sz, pp, vp]
+    lib.lrcnn_backward_rows.argtypes = [vp, vp, pp, pp, pp, vp, pp, vp, vp, sz, vp]
+    lib.lrcnn_layerwise_reference_gpu.argtypes = [vp, vp, pp, pp, pp, vp, vp, pp, vp,
+                                                  vp, sz, pp, vp]
+    lib.lrcnn_last_error.restype = C.c_char_p
+    lib.lrcnn_debug_dry_run.argtypes = [C.c_int]
+    lib.lrcnn_debug_dry_run.restype = None
+    for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
+              "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
+              "lrcnn_layerwise_reference_gpu"):
+        getattr(lib, f).restype = C.c_int
+    return lib
+
+
+LIB = _load()
+
+# Names the header declares (checked by the tests against the shared object).
+EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
+           "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_forward_rows",
+           "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
+           "lrcnn_debug_dry_run")
+
+
+def _check(code):
+    if code != 0:
+        raise LrcnnError(code, LIB.lrcnn_last_error().decode())
+
+
+class Plan:
+    """Owns an lrcnn_plan_t handle."""
+
+    def __init__(self, handle, nodes):
+        self.handle = handle
+        self.nodes = list(nodes)
+        self.n = len(self.nodes)
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            LIB.lrcnn_plan_destroy(self.handle)
+            self.handle = None
+
+    def info(self):
+        inf = PlanInfo()
+        _check(LIB.lrcnn_plan_query(self.handle, C.byref(inf)))
+        return inf.as_dict()
+
+    def node_shape(self, v):
+        out = (C.c_int32 * 3)()
+        _check(LIB.lrcnn_plan_node_shape(self.handle, v, out))
+        return tuple(out)
+
+    def band_rows(self, band, v):
+        out = (C.c_int32 * 4)()
+        _check(LIB.lrcnn_plan_band_rows(self.handle, band, v, out))
+        return tuple(out)
+
+
+def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
+               policy=EVEN, bounds=None):
+    arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
+    cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None)
+    keep = None
+    if bounds is not None:
+        keep = (C.c_int32 * len(bounds))(*bounds)
+        cfg.bounds = C.cast(keep, C.POINTER(C.c_int32))
+    h = C.c_void_p()
+    _check(LIB.lrcnn_plan(arr, len(nodes), C.byref(cfg), C.byref(h)))
+    return Plan(h, nodes)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _ptr_array(ts):
+    return (C.c_void_p * len(ts))(*[None if t is None else t.data_ptr() for t in ts])
+
+
+def _stream(stream):
+    if stream is not None:
+        return C.c_void_p(stream)
+    import torch
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def lrcnn_forward_rows(plan, x, weights, scales, shifts, y, workspace, masks=None,
+                       stream=None):
+    """weights/scales/shifts/masks: per-node lists (None where unused)."""
+    _check(LIB.lrcnn_forward_rows(
+        plan.handle, _ptr(x), _ptr_array(weights), _ptr_array(scales),
+        _ptr_array(shifts), _ptr(y), _ptr(workspace), workspace.numel(),
+        _ptr_array(masks) if masks is not None else None, _stream(stream)))
+
+
+def lrcnn_backward_rows(plan, x, weights, scales, shifts, dy, dws, dx, workspace,
+                        stream=None):
+    _check(LIB.lrcnn_backward_rows(
+        plan.handle, _ptr(x), _ptr_array(weights), _ptr_array(scales),
+        _ptr_array(shifts), _ptr(dy), _ptr_array(dws), _ptr(dx), _ptr(workspace),
+        workspace.numel(), _stream(stream)))
+
+
+def lrcnn_layerwise_reference_gpu(plan, x, weights, scales, shifts, dy, y, dws, dx,
+                                  workspace, masks=None, stream=None):
+    _check(LIB.lrcnn_layerwise_reference_gpu(
+        plan.handle, _ptr(x), _ptr_array(weights), _ptr_array(scales),
+        _ptr_array(shifts), _ptr(dy), _ptr(y), _ptr_array(dws), _ptr(dx),
+        _ptr(workspace), workspace.numel(),
+        _ptr_array(masks) if masks is not None else None, _stream(stream)))
+
+
+def lrcnn_debug_dry_run(on):
+    """Test hook: walk schedules with all host checks but launch nothing."""
+    LIB.lrcnn_debug_dry_run(1 if on else 0)

@@ -1,0 +1,164 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on
+the same seeded inputs. Sizes span several 128-wide tiles with ragged tails,
+channel counts on and off the 16-byte vector paths, strides, pooling,
+residual adds, empty bands and every schedule (two-phase sharing,
+overlapping recompute, layer-wise)."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import assert_parity, gpu_run, rel
+from paper_2401_11471_amd import lrcnn as L
+from workloads import NetBuilder, Inputs, config_inputs, tiny_net, F32, BF16
+
+pytestmark = pytest.mark.gpu
+
+
+def vgg_like(c=(16, 24, 40)):
+    nb = NetBuilder()
+    v = nb.conv(0, c[0], 3, 1, 1)
+    v = nb.conv(v, c[0], 3, 1, 1)
+    v = nb.pool(v, 2, 2, 0)
+    v = nb.conv(v, c[1], 3, 1, 1)
+    v = nb.pool(v, 2, 2, 0)
+    v = nb.conv(v, c[2], 3, 1, 1)
+    return nb.nodes
+
+
+def wide_chain():
+    # N = 136 and 200 span two 128-wide tiles; C_in = 72 leaves a partial
+    # 16/32-element K chunk
+    nb = NetBuilder()
+    v = nb.conv(0, 72, 3, 1, 1)
+    v = nb.conv(v, 136, 3, 1, 1)
+    v = nb.conv(v, 200, 1, 1, 0, affine=1, relu=0)
+    return nb.nodes
+
+
+def odd_chain():
+    # channel counts off the vector paths, even windows, stride 3
+    nb = NetBuilder()
+    v = nb.conv(0, 5, 5, 2, 2)
+    v = nb.conv(v, 6, 2, 1, 0)
+    v = nb.pool(v, 3, 2, 1)
+    v = nb.conv(v, 3, 4, 3, 1)
+    nb.conv(v, 7, 1, 1, 0)
+    return nb.nodes
+
+
+def resnet_like():
+    nb = NetBuilder()
+    a = nb.conv(0, 16, 7, 2, 3, affine=1)
+    b = nb.pool(a, 3, 2, 1)
+    c1 = nb.conv(b, 16, 1, 1, 0, affine=1)
+    c2 = nb.conv(c1, 16, 3, 2, 1, affine=1)
+    c3 = nb.conv(c2, 64, 1, 1, 0, affine=1, relu=0)
+    sc = nb.conv(b, 64, 1, 2, 0, affine=1, relu=0)
+    s = nb.sum(c3, sc)
+    d1 = nb.conv(s, 16, 1, 1, 0, affine=1)
+    d2 = nb.conv(d1, 16, 3, 1, 1, affine=1)
+    d3 = nb.conv(d2, 64, 1, 1, 0, affine=1, relu=0)
+    nb.sum(d3, s)
+    return nb.nodes
+
+
+NETS = {"tiny": (tiny_net(), 32, 32), "vgg_like": (vgg_like(), 44, 37),
+        "wide": (wide_chain(), 29, 23), "odd": (odd_chain(), 47, 41),
+        "resnet_like": (resnet_like(), 61, 45)}
+
+
+def _inputs(name, dtype, batch=2, seed=0):
+    nodes, h, w = NETS[name]
+    return nodes, Inputs(nodes, batch, h, w, 3, dtype, seed=seed + 17)
+
+
+def test_config1_tiny_parity():
+    nodes, inp = config_inputs(1)
+    gpu = gpu_run(nodes, inp, L.CARRY, 4)
+    errs, nbad = assert_parity(nodes, inp, gpu)
+    assert nbad == 0, "config 1 ReLU masks must equal the oracle's"
+    print("config1", {k: f"{e:.1e}" for k, e in errs.items()})
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", list(NETS))
+def test_carry_parity(name, dtype):
+    nodes, inp = _inputs(name, dtype)
+    gpu = gpu_run(nodes, inp, L.CARRY, 3)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", ["vgg_like", "odd", "resnet_like"])
+def test_carry_uneven_and_empty_bands(name, dtype):
+    nodes, inp = _inputs(name, dtype, seed=3)
+    h = inp.x.shape[1]
+    bounds = [0, 0, 5, 5, 6, h // 2, h - 3, h, h]
+    gpu = gpu_run(nodes, inp, L.CARRY, len(bounds) - 1, L.EXPLICIT, bounds)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", list(NETS))
+def test_recompute_parity(name, dtype):
+    nodes, inp = _inputs(name, dtype, seed=5)
+    gpu = gpu_run(nodes, inp, L.RECOMPUTE, 4)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", list(NETS))
+def test_layerwise_parity(name, dtype):
+    nodes, inp = _inputs(name, dtype, seed=7)
+    gpu = gpu_run(nodes, inp, layerwise=True)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", ["vgg_like", "resnet_like", "wide"])
+def test_row_centric_forward_equals_layerwise_bitwise(name, dtype):
+    # the K-reduction order of every output element does not depend on the
+    # band, so forward outputs and every ReLU / argmax decision are identical
+    nodes, inp = _inputs(name, dtype, seed=9)
+    lw = gpu_run(nodes, inp, layerwise=True)
+    for mode, nb in ((L.CARRY, 5), (L.RECOMPUTE, 3)):
+        rc = gpu_run(nodes, inp, mode, nb)
+        np.testing.assert_array_equal(rc["y"], lw["y"])
+        for v, m in lw["masks"].items():
+            np.testing.assert_array_equal(rc["masks"][v], m)
+        # gradients agree to rounding (different reduction splits per band)
+        tol = 1e-5 if dtype == F32 else 1e-2
+        for v in range(1, len(nodes)):
+            if lw["dw"][v] is not None:
+                assert rel(rc["dw"][v], lw["dw"][v]) < tol
+        assert rel(rc["dx"], lw["dx"]) < tol
+
+
+def test_weight_gradients_are_deterministic():
+    nodes, inp = _inputs("resnet_like", F32, seed=11)
+    gpu = gpu_run(nodes, inp, L.CARRY, 4, repeat_bwd=2)
+    a, b = gpu["dw_runs"]
+    for v in range(1, len(nodes)):
+        if a[v] is not None:
+            np.testing.assert_array_equal(a[v], b[v])
+
+
+def test_no_input_gradient_requested():
+    nodes, inp = _inputs("vgg_like", F32, seed=13)
+    gpu = gpu_run(nodes, inp, L.CARRY, 3, want_dx=False)
+    assert gpu["dx"] is None
+    assert_parity(nodes, inp, gpu, check_dx=False)
+
+
+def test_backward_without_forward_is_rejected():
+    nodes, inp = _inputs("tiny", F32)
+    b, h, w, c = inp.x.shape
+    plan = L.lrcnn_plan(nodes, b, c, h, w, F32, L.CARRY, 2)
+    from paper_2401_11471_amd.device import DeviceModel
+    dm = DeviceModel.from_inputs(nodes, inp)
+    ws = dm.workspace(plan.info()["workspace_bytes"])
+    dy = dm.empty((b,) + plan.node_shape(len(nodes) - 1))
+    with pytest.raises(L.LrcnnError) as e:
+        L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, ws)
+    assert e.value.code == -5
+    torch.cuda.synchronize()
