@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of row-centric CNN training (LR-CNN) on one MI355X.
+
+One step = lrcnn_forward_rows + lrcnn_backward_rows over one batch of the
+workload (Algorithm 1's FP and BP over all row bands: forward, band
+recompute, input gradients, weight gradients). Inputs are synthetic N(0, 1)
+tensors with the paper's shapes (ImageNet is not available), resident in HBM
+before timing starts. Prints one JSON line.
+
+Default workload: VGG-16 conv trunk, float32, batch 8, 3x224x224, 4 row bands
+of 56 rows, two-phase sharing. Also reported: peak activation bytes of the
+row-centric step against the layer-wise baseline (same kernels, every
+feature map kept), the layer-wise step's speed, the overlapping-recompute
+mode's speed (halo overhead), a roofline line for the dominant kernel, and
+the CPU oracle's speed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"f32": ("mfma", 157.3, "TFLOP/s"), "bf16": ("mfma", 2500.0, "TFLOP/s")}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload id 1..5")
+    ap.add_argument("--mode", default="carry", choices=["carry", "balanced", "recompute"])
+    ap.add_argument("--bands", type=int, default=0, help="override the band count")
+    ap.add_argument("--batch", type=int, default=0, help="override the batch")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the layer-wise / recompute comparison runs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=4)
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2401_11471_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(cfg_id, n_img):
+    """Column oracle (float64, numpy/BLAS) FP+BP on n_img images of the
+    workload, one image at a time; weight gradients are summed."""
+    import numpy as np
+    import threadpoolctl
+    from oracle import column as OC
+    from workloads import config_inputs, BF16
+    nodes, inp = config_inputs(cfg_id, batch=n_img)
+    bf = inp.dtype == BF16
+    info = threadpoolctl.threadpool_info()
+    cores = max([i.get("num_threads", 1) for i in info] or [1])
+    t0 = time.perf_counter()
+    for i in range(n_img):
+        x = inp.x[i:i + 1]
+        acts, am = OC.forward(nodes, x, inp.weights, inp.scales, inp.shifts, bf16=bf)
+        g = np.zeros(acts[-1].shape) + 1.0
+        OC.backward(nodes, acts, am, inp.weights, inp.scales, g, bf16=bf, want_dx=False)
+    dt = time.perf_counter() - t0
+    return {"value": round(n_img / dt, 4), "unit": "images/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"{n_img} image(s) of the same workload, float64 column FP+BP "
+                      f"(numpy/BLAS), {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} "
+              f"(WORLD_SIZE={world}) is not supported. Multi-GPU sharding is a "
+              "design note, not an implemented path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2401_11471_amd import lrcnn as L
+    from paper_2401_11471_amd.device import DeviceModel
+    from workloads import CONFIGS, config_inputs, BF16
+
+    c = dict(CONFIGS[args.config])
+    if args.batch:
+        c["batch"] = args.batch
+    nb = args.bands or c["bands"]
+    mode = L.RECOMPUTE if args.mode == "recompute" else L.CARRY
+    policy = L.BALANCED if args.mode == "balanced" else L.EVEN
+    nodes, inp = config_inputs(args.config, batch=c["batch"])
+    B, H, W, Cin = inp.x.shape
+    dts = "bf16" if inp.dtype == BF16 else "f32"
+
+    plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy)
+    info = plan.info()
+    dm = DeviceModel.from_inputs(nodes, inp)
+    out_shape = (B,) + plan.node_shape(len(nodes) - 1)
+    dy = dm.to_device(inp.grad(out_shape))
+    torch.cuda.synchronize()
+
+    # --- peak activation bytes: everything the step allocates beyond the
+    # parameters, their gradients, the input and dL/dy
+    def measure(fn_alloc, fn_step):
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        bufs = fn_alloc()
+        fn_step(bufs)
+        torch.cuda.synchronize()
+        return torch.cuda.max_memory_allocated() - base, bufs
+
+    def rc_alloc():
+        return dict(ws=dm.workspace(info["workspace_bytes"]), y=dm.empty(out_shape))
+
+    def rc_step(b):
+        L.lrcnn_forward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, b["y"], b["ws"])
+        L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, b["ws"])
+
+    peak_rc, bufs = measure(rc_alloc, rc_step)
+
+    # --- timed region
+    for _ in range(args.warmup):
+        rc_step(bufs)
+    torch.cuda.synchronize()
+    L.lrcnn_debug_profile(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        rc_step(bufs)
+    e1.record()
+    torch.cuda.synchronize()
+    L.lrcnn_debug_profile(False)
+    ms = e0.elapsed_time(e1) / args.steps
+    kern = L.lrcnn_debug_profile_collect()
+    value = B * 1000.0 / ms
+
+    dom_name, (dom_n, dom_ms, dom_fl) = max(kern.items(), key=lambda kv: kv[1][1])
+    bound, peak, unit = PEAK[dts]
+    achieved = dom_fl / (dom_ms * 1e-3) / 1e12
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tpath):
+        try:
+            t = json.load(open(tpath))
+            ent = t.get(f"cfg{args.config}:{args.mode}:{nb}:{dom_name}")
+            if ent and ent.get("source_hash") == kernel_source_hash():
+                traffic = ent["bytes_per_launch"]
+        except (ValueError, KeyError):
+            traffic = None
+    roofline = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+                "frac": round(achieved / peak, 4), "traffic": traffic,
+                "kernel": dom_name, "launches_per_step": dom_n // args.steps,
+                "avg_launch_ms": round(dom_ms / dom_n, 4)}
+    all_mfma_ms = sum(v[1] for k, v in kern.items() if "reduce" not in k) / args.steps
+    all_mfma_fl = sum(v[2] for v in kern.values()) / args.steps
+
+    out = {
+        "metric": "training images/sec (FP+BP) + peak activation bytes vs layer-wise, 1 MI355X",
+        "value": round(value, 3), "unit": "images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": dts, "data": "synthetic N(0,1), paper's shapes (ImageNet not available)",
+        "config": {"workload": c["name"], "net": c["net"], "batch": B,
+                   "input": [Cin, H, W], "bands": nb, "mode": args.mode,
+                   "dx": False},
+        "roofline": roofline,
+        "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),
+        "mfma_kernels": {"ms_per_step": round(all_mfma_ms, 3),
+                         "tflops": round(all_mfma_fl / (all_mfma_ms * 1e-3) / 1e12, 2),
+                         "per_kernel": {k: {"launches": v[0] // args.steps,
+                                            "ms": round(v[1] / args.steps, 3),
+                                            "tflops": round(v[2] / max(v[1], 1e-9) / 1e9, 2)}
+                                        for k, v in sorted(kern.items())}},
+        "peak_act_bytes": int(peak_rc),
+        "analytic": {k: info[k] for k in ("workspace_bytes", "layerwise_workspace_bytes",
+                                          "strip_bytes", "band_cache_bytes", "delta_bytes",
+                                          "partial_bytes", "omega_bytes", "flops_tau",
+                                          "flops_rows", "shared_rows", "halo_rows")},
+    }
+    del bufs
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    if not args.no_extras:
+        # layer-wise baseline: same kernels, every feature map kept, no recompute
+        def lw_alloc():
+            return dict(ws=dm.workspace(info["layerwise_workspace_bytes"]),
+                        y=dm.empty(out_shape))
+
+        def lw_step(b):
+            L.lrcnn_layerwise_reference_gpu(plan, dm.x, dm.w, dm.sc, dm.sf, dy, b["y"],
+                                            dm.dw, None, b["ws"])
+        try:
+            peak_lw, lb = measure(lw_alloc, lw_step)
+            for _ in range(args.warmup):
+                lw_step(lb)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                lw_step(lb)
+            e1.record()
+            torch.cuda.synchronize()
+            lw_ms = e0.elapsed_time(e1) / args.steps
+            out["layerwise"] = {"images_per_s": round(B * 1000.0 / lw_ms, 3),
+                                "ms_per_step": round(lw_ms, 3),
+                                "peak_act_bytes": int(peak_lw)}
+            out["mem_ratio_layerwise_over_rows"] = round(peak_lw / peak_rc, 3)
+            del lb
+        except (RuntimeError, L.LrcnnError) as ex:
+            out["layerwise"] = {"error": str(ex)[:200]}
+        torch.cuda.empty_cache()
+        if mode == L.CARRY:
+            rplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.RECOMPUTE, nb)
+            rinfo = rplan.info()
+            rws = dm.workspace(rinfo["workspace_bytes"])
+            ry = dm.empty(out_shape)
+
+            def rstep():
+                L.lrcnn_forward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, ry, rws)
+                L.lrcnn_backward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, rws)
+            for _ in range(args.warmup):
+                rstep()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                rstep()
+            e1.record()
+            torch.cuda.synchronize()
+            r_ms = e0.elapsed_time(e1) / args.steps
+            out["recompute"] = {"images_per_s": round(B * 1000.0 / r_ms, 3),
+                                "ms_per_step": round(r_ms, 3),
+                                "time_over_carry": round(r_ms / ms, 3),
+                                "flops_over_4tau": round(rinfo["flops_rows"] /
+                                                         (4 * rinfo["flops_tau"]), 3),
+                                "workspace_bytes": rinfo["workspace_bytes"]}
+            del rws, ry
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_images, B))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

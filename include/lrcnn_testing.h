@@ -4,6 +4,8 @@
 #ifndef LRCNN_TESTING_H
 #define LRCNN_TESTING_H
 
+#include <stdint.h>
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -15,6 +17,23 @@ extern "C" {
  * never dereference a device pointer. Lets the executor's bookkeeping be
  * tested on a machine without a GPU. on == 0 restores normal operation. */
 void lrcnn_debug_dry_run(int on);
+
+/* on != 0: clear and start recording two events on the launch stream around
+ * every matrix-core kernel launch (convolution forward, input gradient,
+ * weight gradient), with each launch's algorithmic FLOPs; on == 0 stops
+ * recording. Timing only: results are unchanged. */
+void lrcnn_debug_profile(int on);
+
+/* After the recorded streams are synchronised: aggregate the records per
+ * kernel instantiation. Returns the number of kernels, or -1 on a HIP
+ * error. */
+int lrcnn_debug_profile_collect(void);
+
+/* Entry i of the aggregate: kernel name (valid until the next collect),
+ * launch count, summed launch durations in milliseconds and summed
+ * algorithmic FLOPs. Returns 0, or -1 if i is out of range. */
+int lrcnn_debug_profile_entry(int32_t i, const char **name, int64_t *launches,
+                              double *ms, double *flops);
 
 #ifdef __cplusplus
 }

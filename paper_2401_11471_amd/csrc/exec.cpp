@@ -116,6 +116,8 @@ struct Run {
       c.sy0 = 0;
       c.sy1 = su.h;
       c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
+      c.part = (float *)(ws + L.part);
+      c.part_bytes = L.part_bytes;
       LAUNCH(launch_conv(dt, 0, c, stream), "conv forward");
     } else if (d.op == LRCNN_OP_MAXPOOL) {
       PoolArgs p{};
@@ -249,12 +251,10 @@ struct Run {
       g.kh = d.kh, g.kw = d.kw, g.sh = d.sh, g.sw = d.sw, g.ph = d.ph, g.pw = d.pw;
       LAUNCH(launch_wgrad(dt, g, dw[v], stream), "weight gradient");
       if (u != 0 || want_dx) {
-        LAUNCH(launch_wtranspose(dt, w[v], ws + L.wt, sv.c, d.kh * d.kw, su.c, stream),
-               "weight transpose");
         ConvArgs c{};
         c.src = View{dc, (long long)(b - a) * sv.w * sv.c, a, sv.w, sv.c, b - a};
         c.dst = dlt[u];
-        c.w = ws + L.wt;
+        c.w = w[v];
         c.B = B;
         c.y0 = std::max(0, a * d.sh - d.ph);
         c.y1 = std::min(su.h, (b - 1) * d.sh - d.ph + d.kh);
@@ -266,6 +266,8 @@ struct Run {
         c.sy0 = a;
         c.sy1 = b;
         c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
+        c.part = (float *)(ws + L.part);
+        c.part_bytes = L.part_bytes;
         LAUNCH(launch_conv(dt, 1, c, stream), "input gradient");
       }
     } else if (d.op == LRCNN_OP_MAXPOOL) {
@@ -487,3 +489,10 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
 }
 
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
+
+extern "C" void lrcnn_debug_profile(int on) { lrcnn::profile_enable(on); }
+extern "C" int lrcnn_debug_profile_collect(void) { return lrcnn::profile_collect(); }
+extern "C" int lrcnn_debug_profile_entry(int32_t i, const char **name, int64_t *launches,
+                                         double *ms, double *flops) {
+  return lrcnn::profile_entry(i, name, launches, ms, flops);
+}

@@ -18,10 +18,88 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <map>
+#include <string>
+#include <vector>
 
 #include "kernels.hpp"
 
 namespace lrcnn {
+
+// ------------------------------------------------------------- profiling
+// Optional per-launch timing of the matrix-core kernels: two events on the
+// launch stream around each launch, aggregated per kernel instantiation
+// together with the launch's algorithmic FLOPs (what the convolution needs,
+// not what the tiles compute).
+namespace prof {
+struct Rec {
+  std::string name;
+  hipEvent_t a, b;
+  double flops;
+};
+static bool on = false;
+static std::vector<Rec> recs;
+static std::vector<hipEvent_t> pool;
+static size_t used = 0;
+
+static hipEvent_t take() {
+  if (used == pool.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    pool.push_back(e);
+  }
+  return pool[used++];
+}
+static int begin(const std::string &name, double flops, hipStream_t s) {
+  if (!on) return -1;
+  hipEvent_t a = take(), b = take();
+  if (!a || !b) return -1;
+  hipEventRecord(a, s);
+  recs.push_back(Rec{name, a, b, flops});
+  return (int)recs.size() - 1;
+}
+static void end(int i, hipStream_t s) {
+  if (i >= 0) hipEventRecord(recs[i].b, s);
+}
+struct Agg {
+  int64_t launches = 0;
+  double ms = 0, flops = 0;
+};
+static std::vector<std::pair<std::string, Agg>> table;
+}  // namespace prof
+
+void profile_enable(int enable) {
+  prof::on = enable != 0;
+  if (prof::on) {
+    prof::recs.clear();
+    prof::used = 0;
+    prof::table.clear();
+  }
+}
+
+// Aggregate the recorded launches (the caller has synchronised the streams).
+int profile_collect() {
+  std::map<std::string, prof::Agg> m;
+  for (auto &r : prof::recs) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return -1;
+    auto &g = m[r.name];
+    g.launches += 1;
+    g.ms += ms;
+    g.flops += r.flops;
+  }
+  prof::table.assign(m.begin(), m.end());
+  return (int)prof::table.size();
+}
+
+int profile_entry(int i, const char **name, int64_t *launches, double *ms, double *flops) {
+  if (i < 0 || i >= (int)prof::table.size()) return -1;
+  *name = prof::table[i].first.c_str();
+  *launches = prof::table[i].second.launches;
+  *ms = prof::table[i].second.ms;
+  *flops = prof::table[i].second.flops;
+  return 0;
+}
 
 typedef uint16_t bf16;
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -182,20 +260,30 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     ay[i] = a.y0 + t % R;
     ab[i] = t / R;
   }
-  const long long bns = DGRAD ? (long long)a.KC : (long long)taps * a.KC;
-  const long long bts = DGRAD ? (long long)a.N * a.KC : (long long)a.KC;
+  // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
+  // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output
+  // channel of the consumer), contiguous along n, so each 16-byte load
+  // holds E columns of one k and is written to LDS transposed.
+  constexpr int BV = BN / E;           // 16-byte vectors per k (input grad)
+  constexpr int BKS = 256 / BV;        // k rows per pass (input grad)
   int bn[NB];
   bool bvld[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    bn[j] = n0 + (tid >> 2) + 64 * j;
+    bn[j] = DGRAD ? n0 + (tid % BV) * E : n0 + (tid >> 2) + 64 * j;
     bvld[j] = bn[j] < a.N;
   }
+  const int bk0 = tid / BV;
+
+  // K iterations of this workgroup (split-K over blockIdx.z)
+  const int kbeg = blockIdx.z * a.kts;
+  const int kend = min(KT, kbeg + a.kts);
 
   uint4 ra[2], rb[NB];
   auto gload = [&](int kt) {
     const int tap = kt / CB;
-    const int c0 = (kt - tap * CB) * BK + kv * E;
+    const int cb = (kt - tap * CB) * BK;
+    const int c0 = cb + kv * E;
     const int ti = tap / a.kw, tj = tap - ti * a.kw;
     const bool cok = c0 < a.KC;
     const int lim = a.KC - c0;
@@ -223,9 +311,16 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      bool ok = bvld[j] && cok;
-      const T *p = ok ? w + bn[j] * bns + tap * bts + c0 : w;
-      rb[j] = load16<T, VEC>(p, ok, lim);
+      if (DGRAD) {
+        const int o = cb + bk0 + BKS * j;
+        const bool ok = bvld[j] && o < a.KC;
+        const T *p = ok ? w + ((long long)o * taps + tap) * a.N + bn[j] : w;
+        rb[j] = load16<T, VEC>(p, ok, a.N - bn[j]);
+      } else {
+        const bool ok = bvld[j] && cok;
+        const T *p = ok ? w + ((long long)bn[j] * taps + tap) * a.KC + c0 : w;
+        rb[j] = load16<T, VEC>(p, ok, lim);
+      }
     }
   };
 
@@ -238,18 +333,49 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
-  if (KT > 0) gload(0);
-  for (int kt = 0; kt < KT; ++kt) {
+  if (kend > kbeg) gload(kbeg);
+  for (int kt = kbeg; kt < kend; ++kt) {
     const int buf = kt & 1;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
       *(uint4 *)(&As[buf][((tid >> 2) + 64 * i) * LDK + kv * E]) = ra[i];
 #pragma unroll
-    for (int j = 0; j < NB; ++j)
-      *(uint4 *)(&Bs[buf][((tid >> 2) + 64 * j) * LDK + kv * E]) = rb[j];
+    for (int j = 0; j < NB; ++j) {
+      if (DGRAD) {
+        union {
+          uint4 u;
+          T e[E];
+        } t;
+        t.u = rb[j];
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          Bs[buf][((tid % BV) * E + e) * LDK + bk0 + BKS * j] = t.e[e];
+      } else {
+        *(uint4 *)(&Bs[buf][((tid >> 2) + 64 * j) * LDK + kv * E]) = rb[j];
+      }
+    }
     __syncthreads();
-    if (kt + 1 < KT) gload(kt + 1);
+    if (kt + 1 < kend) gload(kt + 1);
     mma_tile<BN>(As[buf], Bs[buf], acc, wm, wn, lane);
+  }
+
+  if (gridDim.z > 1) {
+    // split-K: raw partial sums, reduced in split order by the epilogue kernel
+    float *part = a.part + (long long)blockIdx.z * M * a.N;
+    const int col = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int m = m0 + wm + 32 * i + acc_row(v, lane);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int n = n0 + wn + 32 * j + col;
+          if (n < a.N) part[(long long)m * a.N + n] = acc[i][j][v];
+        }
+      }
+    return;
   }
 
   // epilogue
@@ -287,19 +413,75 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
 }
 
+// Sum the split-K partials of every output element in split order, then
+// apply the forward epilogue (affine, ReLU, store, mask) or add the input
+// gradient into the error window.
 template <typename T, bool DGRAD>
-static int conv_dispatch(const ConvArgs &a, hipStream_t s) {
+__global__ void conv_split_epilogue(ConvArgs a, int splits) {
+  const int R = a.y1 - a.y0;
+  const long long M = (long long)a.B * R * a.Wd;
+  const long long MN = M * a.N;
+  const long long drow = (long long)a.Wd * a.N;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < MN;
+       idx += (long long)gridDim.x * blockDim.x) {
+    float val = 0.f;
+    for (int z = 0; z < splits; ++z) val += a.part[z * MN + idx];
+    const int n = (int)(idx % a.N);
+    const long long m = idx / a.N;
+    const int x = (int)(m % a.Wd);
+    const long long t = m / a.Wd;
+    const int y = a.y0 + (int)(t % R);
+    const int b = (int)(t / R);
+    const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
+    if (DGRAD) {
+      ((float *)a.dst.p)[off] += val;
+    } else {
+      if (a.scale) val = val * a.scale[n] + a.shift[n];
+      if (a.relu) val = val > 0.f ? val : 0.f;
+      stf((T *)a.dst.p + off, val);
+      if (a.mask)
+        a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n] = val > 0.f ? 1 : 0;
+    }
+  }
+}
+
+static unsigned grid_for(long long total);
+
+template <typename T, bool DGRAD>
+static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
+  ConvArgs a = a0;
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
-  const bool vec = (a.KC % Cfg<T>::E) == 0;
+  const bool vec = (a.KC % Cfg<T>::E) == 0 && (!DGRAD || (a.N % Cfg<T>::E) == 0);
   const int bn = a.N <= 64 ? 64 : 128;
-  dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn);
+  const int KT = a.kh * a.kw * ((a.KC + Cfg<T>::BK - 1) / Cfg<T>::BK);
+  const int splits = conv_split_count(M, a.N, KT, a.part ? a.part_bytes : 0);
+  a.kts = (KT + splits - 1) / splits;
+  dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
+  int pr = -1;
+  if (prof::on) {
+    // algorithmic FLOPs: forward 2*M*N*K; input gradient 2 * consumer pixels
+    // * C_out * taps * C_in (taps that a stride skips are not counted)
+    const double taps = (double)a.kh * a.kw;
+    const double fl = DGRAD ? 2.0 * a.B * (a.sy1 - a.sy0) * a.Ws * a.KC * taps * a.N
+                            : 2.0 * M * a.N * taps * a.KC;
+    std::string nm = std::string("conv_gemm_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
+                     ", " + std::to_string(bn) + (DGRAD ? ", dgrad" : ", fwd") +
+                     (vec ? ", vec>" : ", scalar>");
+    pr = prof::begin(nm, fl, s);
+  }
   if (bn == 64) {
     if (vec) conv_gemm_kernel<T, 64, DGRAD, true><<<grid, 256, 0, s>>>(a);
     else conv_gemm_kernel<T, 64, DGRAD, false><<<grid, 256, 0, s>>>(a);
   } else {
     if (vec) conv_gemm_kernel<T, 128, DGRAD, true><<<grid, 256, 0, s>>>(a);
     else conv_gemm_kernel<T, 128, DGRAD, false><<<grid, 256, 0, s>>>(a);
+  }
+  prof::end(pr, s);
+  if (splits > 1) {
+    int p2 = prof::begin("conv_split_epilogue", 0.0, s);
+    conv_split_epilogue<T, DGRAD><<<grid_for((long long)M * a.N), 256, 0, s>>>(a, splits);
+    prof::end(p2, s);
   }
   return (int)hipGetLastError();
 }
@@ -457,11 +639,19 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   splits = (K + kchunk - 1) / kchunk;
   const bool vec = (a.Co % Cfg<T>::E) == 0 && (a.Ci % Cfg<T>::E) == 0;
   dim3 grid((a.Co + BM - 1) / BM, (N + 127) / 128, splits);
+  int pr = -1;
+  if (prof::on)
+    pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
+                         (vec ? ", vec>" : ", scalar>"),
+                     2.0 * K * a.Co * N, s);
   if (vec) wgrad_kernel<T, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
   else wgrad_kernel<T, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  prof::end(pr, s);
   if (splits > 1) {
     long long mn = (long long)a.Co * N;
+    int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
     wgrad_reduce_kernel<<<(unsigned)((mn + 255) / 256), 256, 0, s>>>(a.out, dw, mn, splits);
+    prof::end(p2, s);
   }
   return (int)hipGetLastError();
 }
@@ -735,30 +925,6 @@ __global__ void zero_kernel(float *p, long long n) {
 int launch_zero_f32(float *p, size_t n, void *stream) {
   if (n == 0) return 0;
   zero_kernel<<<grid_for((long long)n), 256, 0, (hipStream_t)stream>>>(p, (long long)n);
-  return (int)hipGetLastError();
-}
-
-template <typename T>
-__global__ void wtranspose_kernel(const T *w, T *wt, int co, int taps, int ci) {
-  const long long total = (long long)co * taps * ci;
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % ci);
-    const long long t = i / ci;
-    const int tap = (int)(t % taps);
-    const int o = (int)(t / taps);
-    wt[((long long)tap * ci + c) * co + o] = w[i];
-  }
-}
-
-int launch_wtranspose(int dt, const void *w, void *wt, int co, int taps, int ci,
-                      void *stream) {
-  const long long total = (long long)co * taps * ci;
-  hipStream_t s = (hipStream_t)stream;
-  if (dt == DT_F32)
-    wtranspose_kernel<float><<<grid_for(total), 256, 0, s>>>((const float *)w, (float *)wt, co, taps, ci);
-  else
-    wtranspose_kernel<bf16><<<grid_for(total), 256, 0, s>>>((const bf16 *)w, (bf16 *)wt, co, taps, ci);
   return (int)hipGetLastError();
 }
 

@@ -33,8 +33,34 @@ struct ConvArgs {
   int mask_h;
   int B, y0, y1, Wd, N, KC, Hs, Ws, sy0, sy1;
   int kh, kw, sh, sw, ph, pw;
+  float *part;        // split-K partial sums (nullable: no split)
+  size_t part_bytes;  // capacity of `part`
+  int kts;            // K iterations per split (set by the launcher)
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
+
+// Number of K splits of a conv launch with M x N outputs and KT K-iterations:
+// enough workgroups for two per CU when the output tiles alone are too few,
+// at least 8 K-iterations per split, and partial sums that fit in `cap`
+// bytes. Shared by the launcher and the planner's workspace sizing.
+inline int conv_split_count(long long M, int N, int KT, size_t cap) {
+  const long long bn = N <= 64 ? 64 : 128;
+  const long long tiles = ((M + 127) / 128) * ((N + bn - 1) / bn);
+  const long long target = 512;
+  if (tiles >= target || KT < 16) return 1;
+  long long s = (target + tiles - 1) / tiles;
+  s = s < KT / 8 ? s : KT / 8;
+  const long long per = M * (long long)N * 4;
+  if (per > 0 && s * per > (long long)cap) s = (long long)cap / per;
+  if (s < 2) return 1;
+  const long long kts = (KT + s - 1) / s;
+  return (int)((KT + kts - 1) / kts);
+}
+// K iterations of a conv for storage element size es (bytes).
+inline int conv_k_iters(int taps, int kc, int es) {
+  const int bk = 64 / es;
+  return taps * ((kc + bk - 1) / bk);
+}
 
 struct WgradArgs {
   const void *dc;  // error operand, own rows [B][R][Wv][Co], contiguous
@@ -86,8 +112,10 @@ int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate,
 int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C,
                      void *stream);
 int launch_zero_f32(float *p, size_t n, void *stream);
-// W[co][t][ci] -> Wt[t][ci][co]
-int launch_wtranspose(int dt, const void *w, void *wt, int co, int taps,
-                      int ci, void *stream);
+
+// Launch timing of the matrix-core kernels (test hook).
+void profile_enable(int enable);
+int profile_collect();
+int profile_entry(int i, const char **name, int64_t *launches, double *ms, double *flops);
 
 }  // namespace lrcnn

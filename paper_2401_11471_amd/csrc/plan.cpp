@@ -6,6 +6,7 @@
 #include <new>
 #include <string>
 
+#include "kernels.hpp"
 #include "plan.hpp"
 
 namespace {
@@ -45,7 +46,7 @@ static void ksp(const lrcnn_node &nd, int &k, int &s, int &p) {
 }
 
 int wgrad_splits(int64_t m, int64_t n, int64_t k) {
-  const int64_t bm = 128, bn = 128, min_k = 256, target = 1024;
+  const int64_t bm = 128, bn = 128, min_k = 256, target = 512;
   int64_t tiles = ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
   int64_t s = (target + tiles - 1) / tiles;
   s = std::min<int64_t>(s, std::max<int64_t>(1, k / min_k));
@@ -327,28 +328,40 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   size_t d0 = A.take(dpeak);
   for (int v = 0; v < n; ++v) L.delta[v] = d0 + bufs[v].off;
   L.delta_bytes = dpeak;
-  size_t dc = 0, wt = 0;
+  size_t dc = 0;
   for (int v = 1; v < n; ++v)
-    if (P.nodes[v].op == LRCNN_OP_CONV) {
-      dc = std::max(dc, P.elems(v, own[v]) * P.es);
-      const lrcnn_node &d = P.nodes[v];
-      wt = std::max(wt, (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c * P.es);
-    }
+    if (P.nodes[v].op == LRCNN_OP_CONV) dc = std::max(dc, P.elems(v, own[v]) * P.es);
   L.dc_bytes = dc;
   L.dc = A.take(dc);
-  L.wt_bytes = wt;
-  L.wt = A.take(wt);
+  // partial sums: weight-gradient splits, and split-K of the convolution
+  // forward / input gradient on launches with few output tiles
   size_t part = 0;
   std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
   splits.assign(n, 1);
+  const size_t conv_cap = (size_t)64 << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
-      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * P.shp[d.in0].c;
-      int64_t k = (int64_t)P.cfg.batch * own[v] * P.shp[v].w;
+      const Shape &su = P.shp[d.in0], &sv = P.shp[v];
+      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * su.c;
+      int64_t k = (int64_t)P.cfg.batch * own[v] * sv.w;
       int s = wgrad_splits(m, nn, k);
       splits[v] = s;
       if (s > 1) part = std::max(part, (size_t)s * m * nn * 4);
+      const int taps = d.kh * d.kw;
+      const int nbands = layerwise ? 1 : P.nb;
+      for (int r = 0; r < nbands; ++r) {
+        const Rows q = layerwise ? Rows{0, sv.h, 0, sv.h} : P.rows[r][v];
+        if (q.b <= q.a) continue;
+        long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
+        int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), conv_cap);
+        if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
+        int u0 = std::max(0, q.a * d.sh - d.ph);
+        int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
+        long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
+        int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), conv_cap);
+        if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
+      }
     }
   L.part_bytes = part;
   L.part = A.take(part);

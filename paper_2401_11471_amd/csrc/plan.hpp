@@ -33,7 +33,6 @@ struct Layout {
   std::vector<int> carry_cap;
   std::vector<std::vector<size_t>> strip;  // [band][node]: shared rows kept
   size_t dc = 0, dc_bytes = 0;   // error operand of one conv (storage dtype)
-  size_t wt = 0, wt_bytes = 0;   // weights transposed for the input gradient
   size_t part = 0, part_bytes = 0;  // weight-gradient partial sums
   size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
   size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;

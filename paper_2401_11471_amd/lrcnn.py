@@ -79,6 +79,13 @@ def _load():
     lib.lrcnn_last_error.restype = C.c_char_p
     lib.lrcnn_debug_dry_run.argtypes = [C.c_int]
     lib.lrcnn_debug_dry_run.restype = None
+    lib.lrcnn_debug_profile.argtypes = [C.c_int]
+    lib.lrcnn_debug_profile.restype = None
+    lib.lrcnn_debug_profile_collect.restype = C.c_int
+    lib.lrcnn_debug_profile_entry.argtypes = [i32, C.POINTER(C.c_char_p),
+                                              C.POINTER(C.c_int64),
+                                              C.POINTER(C.c_double), C.POINTER(C.c_double)]
+    lib.lrcnn_debug_profile_entry.restype = C.c_int
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
               "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
               "lrcnn_layerwise_reference_gpu"):
@@ -92,7 +99,8 @@ LIB = _load()
 EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_forward_rows",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
-           "lrcnn_debug_dry_run")
+           "lrcnn_debug_dry_run", "lrcnn_debug_profile", "lrcnn_debug_profile_collect",
+           "lrcnn_debug_profile_entry")
 
 
 def _check(code):
@@ -186,3 +194,22 @@ def lrcnn_layerwise_reference_gpu(plan, x, weights, scales, shifts, dy, y, dws, 
 def lrcnn_debug_dry_run(on):
     """Test hook: walk schedules with all host checks but launch nothing."""
     LIB.lrcnn_debug_dry_run(1 if on else 0)
+
+
+def lrcnn_debug_profile(on):
+    """Test hook: time every matrix-core kernel launch with HIP events."""
+    LIB.lrcnn_debug_profile(1 if on else 0)
+
+
+def lrcnn_debug_profile_collect():
+    """Per-kernel aggregate of the recorded launches (streams synchronised
+    by the caller): {name: (launches, ms, flops)}."""
+    n = LIB.lrcnn_debug_profile_collect()
+    if n < 0:
+        raise LrcnnError(-7, "profile collection failed")
+    out = {}
+    for i in range(n):
+        nm, la, ms, fl = C.c_char_p(), C.c_int64(), C.c_double(), C.c_double()
+        LIB.lrcnn_debug_profile_entry(i, C.byref(nm), C.byref(la), C.byref(ms), C.byref(fl))
+        out[nm.value.decode()] = (la.value, ms.value, fl.value)
+    return out

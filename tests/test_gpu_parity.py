@@ -116,22 +116,37 @@ def test_layerwise_parity(name, dtype):
 
 @pytest.mark.parametrize("dtype", [F32, BF16])
 @pytest.mark.parametrize("name", ["vgg_like", "resnet_like", "wide"])
-def test_row_centric_forward_equals_layerwise_bitwise(name, dtype):
-    # the K-reduction order of every output element does not depend on the
-    # band, so forward outputs and every ReLU / argmax decision are identical
+def test_row_centric_matches_layerwise(name, dtype):
+    # same kernels; only the split-K grouping of a reduction may differ with
+    # the launch size, so results agree to rounding and every differing
+    # ReLU / argmax decision is a certified near-tie of the oracle
+    from gpu_harness import check_masks, oracle_run
     nodes, inp = _inputs(name, dtype, seed=9)
     lw = gpu_run(nodes, inp, layerwise=True)
+    ref = oracle_run(nodes, inp, lw["g"])
+    tol = 2e-6 if dtype == F32 else 1e-2
     for mode, nb in ((L.CARRY, 5), (L.RECOMPUTE, 3)):
+        rc = gpu_run(nodes, inp, mode, nb)
+        assert rel(rc["y"], lw["y"]) < tol
+        check_masks(nodes, ref, rc["masks"], dtype, 1e-5 if dtype == F32 else 2e-3)
+        gtol = 1e-5 if dtype == F32 else 1e-2
+        for v in range(1, len(nodes)):
+            if lw["dw"][v] is not None:
+                assert rel(rc["dw"][v], lw["dw"][v]) < gtol
+        assert rel(rc["dx"], lw["dx"]) < gtol
+
+
+def test_forward_is_bitwise_band_invariant_without_splits():
+    # layers too short in K to split: every output element is reduced in the
+    # same order whatever the band, so row-centric forward equals layer-wise
+    # forward bit for bit
+    nodes, inp = _inputs("tiny", F32, seed=21)
+    lw = gpu_run(nodes, inp, layerwise=True)
+    for mode, nb in ((L.CARRY, 4), (L.RECOMPUTE, 3)):
         rc = gpu_run(nodes, inp, mode, nb)
         np.testing.assert_array_equal(rc["y"], lw["y"])
         for v, m in lw["masks"].items():
             np.testing.assert_array_equal(rc["masks"][v], m)
-        # gradients agree to rounding (different reduction splits per band)
-        tol = 1e-5 if dtype == F32 else 1e-2
-        for v in range(1, len(nodes)):
-            if lw["dw"][v] is not None:
-                assert rel(rc["dw"][v], lw["dw"][v]) < tol
-        assert rel(rc["dx"], lw["dx"]) < tol
 
 
 def test_weight_gradients_are_deterministic():
