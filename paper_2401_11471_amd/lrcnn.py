@@ -117,7 +117,7 @@ class Plan:
         self.n = len(self.nodes)
 
     def __del__(self):
-        if getattr(self, "handle", None):
+        if getattr(self, "handle", None) and LIB is not None:
             LIB.lrcnn_plan_destroy(self.handle)
             self.handle = None
 

@@ -129,7 +129,7 @@ def assert_parity(nodes, inp, gpu, frac_limit=None, check_dx=True):
     dt = inp.dtype
     tol = TOL[dt]
     if frac_limit is None:
-        frac_limit = 1e-5 if dt == L.F32 else 2e-3
+        frac_limit = 1e-5 if dt == L.F32 else 1e-2
     ref = oracle_run(nodes, inp, gpu["g"], masks=gpu["masks"])
     errs = {"y": rel(gpu["y"], ref["acts"][-1])}
     for v in range(1, len(nodes)):
