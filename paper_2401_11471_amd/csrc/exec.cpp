@@ -145,17 +145,24 @@ struct Run {
 
   // Compute the feature maps of band `r` for every node (FP, or the BP
   // recompute of Algorithm 1). The output node goes to `y` when given.
-  int band_fwd(int r, void *y, void *const *mask_out, bool bp) {
+  // `keep`: the band's maps stay in the window buffers for the BP that
+  // follows (the output node is computed into its window and copied to y,
+  // pool argmax bytes are recorded), so BP can skip recomputing this band.
+  // `views_only`: set the band's views without launching anything (the
+  // maps are already in place).
+  int band_fwd(int r, void *y, void *const *mask_out, bool bp, bool keep = false,
+               bool views_only = false) {
     const int n = P.n;
     for (int v = 1; v < n; ++v) {
       const Rows q = band_rows(r, v);
       View dst;
-      if (v == n - 1 && y) {
+      if (v == n - 1 && y && !keep) {
         dst = full(y, v);
       } else {
         dst = win(L.win[v], v, L.win_cap[v], q.lo);
       }
       act[v] = dst;
+      if (views_only) continue;
       if (sched == S_CARRY && r > 0 && q.a > q.lo) {
         // rows shared from earlier bands (two-phase sharing)
         View strip = win(L.strip[r - 1][v], v, q.a - q.lo, q.lo);
@@ -163,10 +170,15 @@ struct Run {
                                 P.shp[v].w, P.shp[v].c, stream),
                "strip load");
       }
-      uint8_t *am = (bp && P.nodes[v].op == LRCNN_OP_MAXPOOL) ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
+      uint8_t *am = ((bp || keep) && P.nodes[v].op == LRCNN_OP_MAXPOOL)
+                        ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
       uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
       int st = node_fwd(v, q.a, q.b, dst, am, mk);
       if (st != LRCNN_OK) return st;
+      if (v == n - 1 && y && keep)
+        LAUNCH(launch_rows_copy(dt, dt, dst, full(y, v), 0, P.cfg.batch, q.a, q.b,
+                                P.shp[v].w, P.shp[v].c, stream),
+               "output store");
       if (sched == S_CARRY && !bp && r + 1 < P.nb && v != n - 1) {
         const int t = P.tail[r][v];
         if (q.b > t) {
@@ -418,9 +430,11 @@ extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void 
   Run run(P, P.rc, P.cfg.mode == LRCNN_CARRY ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale,
           aff_shift, stream);
   P.fwd_workspace = nullptr;
+  P.last_band_kept = false;
   for (int r = 0; r < P.nb; ++r)
-    if ((st = run.band_fwd(r, y, mask_out, false)) != LRCNN_OK) return st;
+    if ((st = run.band_fwd(r, y, mask_out, false, r == P.nb - 1)) != LRCNN_OK) return st;
   P.fwd_workspace = workspace;
+  P.last_band_kept = true;
   P.fwd_epoch = ++g_epoch;
   return LRCNN_OK;
 }
@@ -451,8 +465,13 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
     int e = g_dry ? 0 : launch_zero_f32(dxacc, cnt, stream);
     if (e) return lrcnn_fail(LRCNN_EHIP, "zero dX");
   }
+  // the last band's maps are still in place after lrcnn_forward_rows on this
+  // workspace, so BP starts without recomputing it
+  const bool kept = P.last_band_kept && P.fwd_workspace == workspace;
+  P.last_band_kept = false;
   for (int r = P.nb - 1; r >= 0; --r) {
-    if ((st = run.band_fwd(r, nullptr, nullptr, true)) != LRCNN_OK) return st;
+    const bool skip = kept && r == P.nb - 1;
+    if ((st = run.band_fwd(r, nullptr, nullptr, true, false, skip)) != LRCNN_OK) return st;
     if ((st = run.band_bwd(r, dy, dw, dx, dxacc)) != LRCNN_OK) return st;
   }
   if (!carry && dx && P.cfg.dtype == LRCNN_BF16 && !g_dry) {

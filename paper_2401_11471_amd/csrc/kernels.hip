@@ -124,83 +124,99 @@ __device__ __forceinline__ int fdiv(int a, int b) {
   return a >= 0 ? a / b : -((-a + b - 1) / b);
 }
 
-template <typename T>
+// Tile geometry: a K tile row is KR 16-byte vectors (64 or 128 bytes) of one
+// pixel or one weight row, staged in LDS with one extra vector of pitch.
+template <typename T, int KR = 4>
 struct Cfg {
   static constexpr int E = 16 / (int)sizeof(T);  // elements per 16 bytes
-  static constexpr int BK = 4 * E;                // K per tile row: 64 bytes
-  static constexpr int LDK = BK + E;              // LDS pitch: 80 bytes
+  static constexpr int BK = KR * E;               // K elements per tile row
+  static constexpr int LDK = BK + E;              // LDS pitch in elements
 };
 
 constexpr int BM = 128;
 
 // ------------------------------------------------------------------ MFMA
-// One 128 x BN tile step. Wave w owns rows [wm, wm+64) and columns
-// [wn, wn+BN/2); lane l feeds row/column (l & 31) of each 32x32 block and
-// the K slice [KPL*(l>>5), KPL*(l>>5)+KPL) of the 64-byte tile row. The
-// same slice order is used for A and B, so every MFMA adds products of
-// matching K indices.
-template <int BN>
-__device__ __forceinline__ void mma_tile(const float *As, const float *Bs,
-                                         f32x16 (&acc)[2][BN / 64], int wm,
-                                         int wn, int lane) {
-  constexpr int LDK = Cfg<float>::LDK, NB = BN / 64;
-  const int r = lane & 31, g = lane >> 5;
-  float4 a[2][2], b[NB][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + 8 * g);
-    a[i][0] = p[0];
-    a[i][1] = p[1];
-  }
-#pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + 8 * g);
-    b[j][0] = p[0];
-    b[j][1] = p[1];
-  }
-#pragma unroll
-  for (int s = 0; s < 8; ++s) {
+// Operand fragments of one 128 x BN tile step. Wave w owns rows
+// [wm, wm+64) and columns [wn, wn+BN/2); lane l feeds row/column (l & 31) of
+// each 32x32 block and the K slice [S*(l>>5), S*(l>>5)+S), S = BK/2, of the
+// tile row. A and B use the same slice order, so every MFMA adds products of
+// matching K indices; the order in which K is summed is the same for every
+// output element and every band.
+template <typename T, int BN, int KR>
+struct Frag;
+
+template <int BN, int KR>
+struct Frag<float, BN, KR> {
+  static constexpr int LDK = Cfg<float, KR>::LDK, NB = BN / 64, NV = KR / 2;
+  float4 a[2][NV], b[NB][NV];
+  __device__ __forceinline__ void load(const float *As, const float *Bs, int wm, int wn,
+                                       int lane) {
+    const int r = lane & 31, g = lane >> 5;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      float av = (s & 3) == 0 ? a[i][s >> 2].x : (s & 3) == 1 ? a[i][s >> 2].y
-               : (s & 3) == 2 ? a[i][s >> 2].z : a[i][s >> 2].w;
+      const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + 4 * NV * g);
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        float bv = (s & 3) == 0 ? b[j][s >> 2].x : (s & 3) == 1 ? b[j][s >> 2].y
-                 : (s & 3) == 2 ? b[j][s >> 2].z : b[j][s >> 2].w;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bv, acc[i][j], 0, 0, 0);
-      }
+      for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + 4 * NV * g);
+#pragma unroll
+      for (int q = 0; q < NV; ++q) b[j][q] = p[q];
     }
   }
-}
+  __device__ __forceinline__ void mma(f32x16 (&acc)[2][NB]) const {
+#pragma unroll
+    for (int s = 0; s < 4 * NV; ++s)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][s >> 2][s & 3],
+                                                           b[j][s >> 2][s & 3], acc[i][j],
+                                                           0, 0, 0);
+  }
+};
 
-template <int BN>
-__device__ __forceinline__ void mma_tile(const bf16 *As, const bf16 *Bs,
-                                         f32x16 (&acc)[2][BN / 64], int wm,
-                                         int wn, int lane) {
-  constexpr int LDK = Cfg<bf16>::LDK, NB = BN / 64;
-  const int r = lane & 31, g = lane >> 5;
-  bf16x8 a[2][2], b[NB][2];
+template <int BN, int KR>
+struct Frag<bf16, BN, KR> {
+  static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
+  bf16x8 a[2][NV], b[NB][NV];
+  __device__ __forceinline__ void load(const bf16 *As, const bf16 *Bs, int wm, int wn,
+                                       int lane) {
+    const int r = lane & 31, g = lane >> 5;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 16 * g);
-    a[i][0] = p[0];
-    a[i][1] = p[1];
+    for (int i = 0; i < 2; ++i) {
+      const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 8 * NV * g);
+#pragma unroll
+      for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 8 * NV * g);
+#pragma unroll
+      for (int q = 0; q < NV; ++q) b[j][q] = p[q];
+    }
   }
+  __device__ __forceinline__ void mma(f32x16 (&acc)[2][NB]) const {
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 16 * g);
-    b[j][0] = p[0];
-    b[j][1] = p[1];
+    for (int s = 0; s < NV; ++s)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i][s], b[j][s], acc[i][j],
+                                                              0, 0, 0);
   }
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i][s], b[j][s],
-                                                            acc[i][j], 0, 0, 0);
+};
+
+template <int BN, int KR, typename T>
+__device__ __forceinline__ void mma_tile(const T *As, const T *Bs,
+                                         f32x16 (&acc)[2][BN / 64], int wm, int wn,
+                                         int lane) {
+  Frag<T, BN, KR> f;
+  f.load(As, Bs, wm, wn, lane);
+  f.mma(acc);
 }
 
 // Row of the 32x32 accumulator block held in register v of lane l.
@@ -229,13 +245,85 @@ __device__ __forceinline__ uint4 load16(const T *p, bool ok, int lim) {
   }
 }
 
+// ------------------------------------------------------- shared helpers
+static unsigned grid_for(long long total) {
+  long long g = (total + 255) / 256;
+  if (g > 65536) g = 65536;
+  return (unsigned)(g < 1 ? 1 : g);
+}
+
+__device__ __forceinline__ long long view_off(const View &v, int b, int row,
+                                              int inner) {
+  return b * v.bs + (long long)(row - v.row0) * v.W * v.C + inner;
+}
+
+__device__ __forceinline__ void ld4(const float *p, float (&v)[4]) {
+  const float4 q = *(const float4 *)p;
+  v[0] = q.x, v[1] = q.y, v[2] = q.z, v[3] = q.w;
+}
+__device__ __forceinline__ void ld4(const bf16 *p, float (&v)[4]) {
+  const uint2 q = *(const uint2 *)p;
+  v[0] = __uint_as_float(q.x << 16), v[1] = __uint_as_float(q.x & 0xffff0000u);
+  v[2] = __uint_as_float(q.y << 16), v[3] = __uint_as_float(q.y & 0xffff0000u);
+}
+__device__ __forceinline__ void st4(float *p, const float (&v)[4]) {
+  *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void st4(bf16 *p, const float (&v)[4]) {
+  uint2 q;
+  q.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+  q.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  *(uint2 *)p = q;
+}
+template <typename T, int V>
+__device__ __forceinline__ void ldv(const T *p, float (&v)[4]) {
+  if (V == 4) ld4(p, v);
+  else v[0] = ldf(p);
+}
+template <typename T, int V>
+__device__ __forceinline__ void stv(T *p, const float (&v)[4]) {
+  if (V == 4) st4(p, v);
+  else stf(p, v[0]);
+}
+
+// Decompose a flat index over B x rows x (W*C/V) into (b, row, inner).
+struct RowIter {
+  long long inner, total;
+  int R, r0;
+  __device__ __forceinline__ void at(long long idx, int V, int &b, int &y, int &in) const {
+    const long long i = idx % inner;
+    const long long t = idx / inner;
+    in = (int)(i * V);
+    y = r0 + (int)(t % R);
+    b = (int)(t / R);
+  }
+};
+static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
+  RowIter it;
+  it.inner = (long long)W * C / V;
+  it.R = r1 - r0;
+  it.r0 = r0;
+  it.total = (long long)B * it.R * it.inner;
+  return it;
+}
+#define GRID_STRIDE(idx, total)                                                   \
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; \
+       idx += (long long)gridDim.x * blockDim.x)
+
 // ------------------------------------------- conv forward / input grad
-template <typename T, int BN, bool DGRAD, bool VEC>
+template <typename T, int BN, int KR, bool DGRAD, bool VEC>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
-  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
+  using CF = Cfg<T, KR>;
+  constexpr int E = CF::E, BK = CF::BK, LDK = CF::LDK;
   constexpr int NB = BN / 64;
-  __shared__ __align__(16) T As[2][BM * LDK];
-  __shared__ __align__(16) T Bs[2][BN * LDK];
+  constexpr int NA = KR / 2;             // A rows loaded per thread
+  constexpr int NBL = BN * KR / 256;     // B vectors loaded per thread
+  constexpr int RS = 256 / KR;           // row stride between a thread's loads
+  // three LDS stages: while tile t is multiplied, the fragments of t+1 are
+  // read, tile t+2 is written and tile t+3 is fetched from global memory
+  constexpr int ST = 3;
+  __shared__ __align__(16) T As[ST][BM * LDK];
+  __shared__ __align__(16) T Bs[ST][BN * LDK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
@@ -243,22 +331,24 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   const int taps = a.kh * a.kw;
   const int CB = (a.KC + BK - 1) / BK;
   const int KT = taps * CB;
-  const int kv = tid & 3;
+  const int kv = tid % KR;
   const T *src = (const T *)a.src.p;
   const T *w = (const T *)a.w;
   const long long srow = (long long)a.src.W * a.src.C;
 
-  int ab[2], ay[2], ax[2];
-  bool am[2];
+  // pixels of this thread's A rows
+  int ay[NA], ax[NA];
+  long long abase[NA];
+  bool am[NA];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    int m = m0 + (tid >> 2) + 64 * i;
+  for (int i = 0; i < NA; ++i) {
+    int m = m0 + tid / KR + RS * i;
     am[i] = m < M;
     int mm = am[i] ? m : 0;
     ax[i] = mm % a.Wd;
     int t = mm / a.Wd;
     ay[i] = a.y0 + t % R;
-    ab[i] = t / R;
+    abase[i] = (long long)(t / R) * a.src.bs - (long long)a.src.row0 * srow;
   }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
   // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output
@@ -266,29 +356,30 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // holds E columns of one k and is written to LDS transposed.
   constexpr int BV = BN / E;           // 16-byte vectors per k (input grad)
   constexpr int BKS = 256 / BV;        // k rows per pass (input grad)
-  int bn[NB];
-  bool bvld[NB];
+  int bn[NBL];
+  bool bvld[NBL];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    bn[j] = DGRAD ? n0 + (tid % BV) * E : n0 + (tid >> 2) + 64 * j;
+  for (int j = 0; j < NBL; ++j) {
+    bn[j] = DGRAD ? n0 + (tid % BV) * E : n0 + tid / KR + RS * j;
     bvld[j] = bn[j] < a.N;
   }
   const int bk0 = tid / BV;
 
-  // K iterations of this workgroup (split-K over blockIdx.z)
+  // K iterations of this workgroup (split-K over blockIdx.z), walked as
+  // (tap, channel block) without divisions in the loop
   const int kbeg = blockIdx.z * a.kts;
   const int kend = min(KT, kbeg + a.kts);
+  int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
+  int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
 
-  uint4 ra[2], rb[NB];
-  auto gload = [&](int kt) {
-    const int tap = kt / CB;
-    const int cb = (kt - tap * CB) * BK;
+  uint4 ra[NA], rb[NBL];
+  auto gload = [&]() {
+    const int cb = cbi * BK;
     const int c0 = cb + kv * E;
-    const int ti = tap / a.kw, tj = tap - ti * a.kw;
     const bool cok = c0 < a.KC;
     const int lim = a.KC - c0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NA; ++i) {
       int sy, sx;
       bool ok;
       if (DGRAD) {
@@ -304,13 +395,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       }
       ok = ok && am[i] && cok && sy >= a.sy0 && sy < a.sy1 && sx < a.Ws;
       const T *p = src;
-      if (ok)
-        p = src + ab[i] * a.src.bs + (sy - a.src.row0) * srow +
-            (long long)sx * a.src.C + c0;
+      if (ok) p = src + abase[i] + sy * srow + (long long)sx * a.src.C + c0;
       ra[i] = load16<T, VEC>(p, ok, lim);
     }
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
+    for (int j = 0; j < NBL; ++j) {
       if (DGRAD) {
         const int o = cb + bk0 + BKS * j;
         const bool ok = bvld[j] && o < a.KC;
@@ -320,6 +409,15 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         const bool ok = bvld[j] && cok;
         const T *p = ok ? w + ((long long)bn[j] * taps + tap) * a.KC + c0 : w;
         rb[j] = load16<T, VEC>(p, ok, lim);
+      }
+    }
+    // advance to the next (tap, channel block)
+    if (++cbi == CB) {
+      cbi = 0;
+      ++tap;
+      if (++tj == a.kw) {
+        tj = 0;
+        ++ti;
       }
     }
   };
@@ -333,14 +431,12 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
-  if (kend > kbeg) gload(kbeg);
-  for (int kt = kbeg; kt < kend; ++kt) {
-    const int buf = kt & 1;
+  auto store = [&](int st) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      *(uint4 *)(&As[buf][((tid >> 2) + 64 * i) * LDK + kv * E]) = ra[i];
+    for (int i = 0; i < NA; ++i)
+      *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + kv * E]) = ra[i];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
+    for (int j = 0; j < NBL; ++j) {
       if (DGRAD) {
         union {
           uint4 u;
@@ -349,15 +445,43 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         t.u = rb[j];
 #pragma unroll
         for (int e = 0; e < E; ++e)
-          Bs[buf][((tid % BV) * E + e) * LDK + bk0 + BKS * j] = t.e[e];
+          Bs[st][((tid % BV) * E + e) * LDK + bk0 + BKS * j] = t.e[e];
       } else {
-        *(uint4 *)(&Bs[buf][((tid >> 2) + 64 * j) * LDK + kv * E]) = rb[j];
+        *(uint4 *)(&Bs[st][(tid / KR + RS * j) * LDK + kv * E]) = rb[j];
       }
     }
-    __syncthreads();
-    if (kt + 1 < kend) gload(kt + 1);
-    mma_tile<BN>(As[buf], Bs[buf], acc, wm, wn, lane);
+  };
+  const int n = kend - kbeg;
+  if (n > 0) {
+    gload();
+    store(0);
   }
+  if (n > 1) {
+    gload();
+    store(1);
+  }
+  if (n > 2) gload();
+  __syncthreads();
+  Frag<T, BN, KR> f0, f1;
+  if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
+  int s1 = 1, s2 = 2;  // stages of tiles t+1 and t+2
+  auto step = [&](int t, Frag<T, BN, KR> &cur, Frag<T, BN, KR> &nxt) {
+    if (t + 1 < n) nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    if (t + 2 < n) {
+      store(s2);
+      if (t + 3 < n) gload();
+    }
+    cur.mma(acc);
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < n; t += 2) {
+    step(t, f0, f1);
+    step(t + 1, f1, f0);
+  }
+  if (t < n) step(t, f0, f1);
 
   if (gridDim.z > 1) {
     // split-K: raw partial sums, reduced in split order by the epilogue kernel
@@ -416,16 +540,21 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 // Sum the split-K partials of every output element in split order, then
 // apply the forward epilogue (affine, ReLU, store, mask) or add the input
 // gradient into the error window.
-template <typename T, bool DGRAD>
+template <typename T, bool DGRAD, int V>
 __global__ void conv_split_epilogue(ConvArgs a, int splits) {
   const int R = a.y1 - a.y0;
   const long long M = (long long)a.B * R * a.Wd;
   const long long MN = M * a.N;
   const long long drow = (long long)a.Wd * a.N;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < MN;
-       idx += (long long)gridDim.x * blockDim.x) {
-    float val = 0.f;
-    for (int z = 0; z < splits; ++z) val += a.part[z * MN + idx];
+  GRID_STRIDE(i4, MN / V) {
+    const long long idx = i4 * V;
+    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int z = 0; z < splits; ++z) {
+      float q[4];
+      ldv<float, V>(a.part + z * MN + idx, q);
+#pragma unroll
+      for (int e = 0; e < V; ++e) val[e] += q[e];
+    }
     const int n = (int)(idx % a.N);
     const long long m = idx / a.N;
     const int x = (int)(m % a.Wd);
@@ -434,27 +563,40 @@ __global__ void conv_split_epilogue(ConvArgs a, int splits) {
     const int b = (int)(t / R);
     const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
     if (DGRAD) {
-      ((float *)a.dst.p)[off] += val;
+      float *d = (float *)a.dst.p + off;
+      float q[4];
+      ldv<float, V>(d, q);
+#pragma unroll
+      for (int e = 0; e < V; ++e) q[e] += val[e];
+      stv<float, V>(d, q);
     } else {
-      if (a.scale) val = val * a.scale[n] + a.shift[n];
-      if (a.relu) val = val > 0.f ? val : 0.f;
-      stf((T *)a.dst.p + off, val);
-      if (a.mask)
-        a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n] = val > 0.f ? 1 : 0;
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        if (a.scale) val[e] = val[e] * a.scale[n + e] + a.shift[n + e];
+        if (a.relu) val[e] = val[e] > 0.f ? val[e] : 0.f;
+        if (a.mask)
+          a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n + e] = val[e] > 0.f ? 1 : 0;
+      }
+      stv<T, V>((T *)a.dst.p + off, val);
     }
   }
 }
 
-static unsigned grid_for(long long total);
+
+#ifndef LRCNN_CONV_KR
+#define LRCNN_CONV_KR 4
+#endif
 
 template <typename T, bool DGRAD>
 static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
+  constexpr int KR = LRCNN_CONV_KR;
+  using CF = Cfg<T, KR>;
   ConvArgs a = a0;
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
-  const bool vec = (a.KC % Cfg<T>::E) == 0 && (!DGRAD || (a.N % Cfg<T>::E) == 0);
+  const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0);
   const int bn = a.N <= 64 ? 64 : 128;
-  const int KT = a.kh * a.kw * ((a.KC + Cfg<T>::BK - 1) / Cfg<T>::BK);
+  const int KT = a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
   const int splits = conv_split_count(M, a.N, KT, a.part ? a.part_bytes : 0);
   a.kts = (KT + splits - 1) / splits;
   dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
@@ -471,16 +613,19 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
     pr = prof::begin(nm, fl, s);
   }
   if (bn == 64) {
-    if (vec) conv_gemm_kernel<T, 64, DGRAD, true><<<grid, 256, 0, s>>>(a);
-    else conv_gemm_kernel<T, 64, DGRAD, false><<<grid, 256, 0, s>>>(a);
+    if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true><<<grid, 256, 0, s>>>(a);
+    else conv_gemm_kernel<T, 64, KR, DGRAD, false><<<grid, 256, 0, s>>>(a);
   } else {
-    if (vec) conv_gemm_kernel<T, 128, DGRAD, true><<<grid, 256, 0, s>>>(a);
-    else conv_gemm_kernel<T, 128, DGRAD, false><<<grid, 256, 0, s>>>(a);
+    if (vec) conv_gemm_kernel<T, 128, KR, DGRAD, true><<<grid, 256, 0, s>>>(a);
+    else conv_gemm_kernel<T, 128, KR, DGRAD, false><<<grid, 256, 0, s>>>(a);
   }
   prof::end(pr, s);
   if (splits > 1) {
     int p2 = prof::begin("conv_split_epilogue", 0.0, s);
-    conv_split_epilogue<T, DGRAD><<<grid_for((long long)M * a.N), 256, 0, s>>>(a, splits);
+    if (a.N % 4 == 0)
+      conv_split_epilogue<T, DGRAD, 4><<<grid_for((long long)M * a.N / 4), 256, 0, s>>>(a, splits);
+    else
+      conv_split_epilogue<T, DGRAD, 1><<<grid_for((long long)M * a.N), 256, 0, s>>>(a, splits);
     prof::end(p2, s);
   }
   return (int)hipGetLastError();
@@ -595,7 +740,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       }
     __syncthreads();
     if (kt + 1 < KT) gload(kbeg + (kt + 1) * BK);
-    mma_tile<BN>(As[buf], Bs[buf], acc, wm, wn, lane);
+    mma_tile<BN, 4>(As[buf], Bs[buf], acc, wm, wn, lane);
   }
 
   const int col = lane & 31;
@@ -618,13 +763,22 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
 }
 
 // dW += sum over splits, in split order (deterministic).
+template <int V>
 __global__ void wgrad_reduce_kernel(const float *part, float *dw, long long mn,
                                     int splits) {
-  long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= mn) return;
-  float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[z * mn + i];
-  dw[i] += s;
+  GRID_STRIDE(i4, mn / V) {
+    const long long i = i4 * V;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f}, q[4];
+    for (int z = 0; z < splits; ++z) {
+      ldv<float, V>(part + z * mn + i, q);
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e] += q[e];
+    }
+    ldv<float, V>(dw + i, q);
+#pragma unroll
+    for (int e = 0; e < V; ++e) q[e] += acc[e];
+    stv<float, V>(dw + i, q);
+  }
 }
 
 template <typename T>
@@ -650,7 +804,10 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   if (splits > 1) {
     long long mn = (long long)a.Co * N;
     int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
-    wgrad_reduce_kernel<<<(unsigned)((mn + 255) / 256), 256, 0, s>>>(a.out, dw, mn, splits);
+    if (mn % 4 == 0)
+      wgrad_reduce_kernel<4><<<grid_for(mn / 4), 256, 0, s>>>(a.out, dw, mn, splits);
+    else
+      wgrad_reduce_kernel<1><<<grid_for(mn), 256, 0, s>>>(a.out, dw, mn, splits);
     prof::end(p2, s);
   }
   return (int)hipGetLastError();
@@ -662,69 +819,82 @@ int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream) {
 }
 
 // ------------------------------------------------------------- max-pool
-template <typename T>
+template <typename T, int V>
 __global__ void pool_fwd_kernel(PoolArgs a) {
   const int R = a.y1 - a.y0;
-  const long long total = (long long)a.B * R * a.Wd * a.C;
+  const int CV = a.C / V;
+  const long long total = (long long)a.B * R * a.Wd * CV;
   const long long srow = (long long)a.src.W * a.src.C;
   const long long drow = (long long)a.Wd * a.C;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(idx % a.C);
-    long long t = idx / a.C;
+  GRID_STRIDE(idx, total) {
+    const int c = (int)(idx % CV) * V;
+    long long t = idx / CV;
     const int x = (int)(t % a.Wd);
     t /= a.Wd;
     const int yy = (int)(t % R);
     const int b = (int)(t / R);
     const int y = a.y0 + yy;
     const T *src = (const T *)a.src.p + b * a.src.bs;
-    float best = 0.f;
-    int bi = 0;
+    float best[4];
+    int bi[4] = {0, 0, 0, 0};
     for (int i = 0; i < a.kh; ++i) {
       const int sy = y * a.sh - a.ph + i;
       for (int j = 0; j < a.kw; ++j) {
         const int sx = x * a.sw - a.pw + j;
-        float v = -__builtin_huge_valf();
-        if (sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws)
-          v = ldf(src + (sy - a.src.row0) * srow + (long long)sx * a.src.C + c);
-        const int tp = i * a.kw + j;
-        if (tp == 0 || v > best) {
-          best = v;
-          bi = tp;
+        float v[4];
+        if (sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws) {
+          ldv<T, V>(src + (sy - a.src.row0) * srow + (long long)sx * a.src.C + c, v);
+        } else {
+#pragma unroll
+          for (int e = 0; e < V; ++e) v[e] = -__builtin_huge_valf();
         }
+        const int tp = i * a.kw + j;
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+          if (tp == 0 || v[e] > best[e]) {
+            best[e] = v[e];
+            bi[e] = tp;
+          }
       }
     }
-    T *dst = (T *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.C + c;
-    stf(dst, best);
-    if (a.am) a.am[idx] = (uint8_t)bi;
-    if (a.mask)
-      a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.C + c] = (uint8_t)bi;
+    const long long o = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.C + c;
+    stv<T, V>((T *)a.dst.p + o, best);
+    const long long flat = (((long long)b * R + yy) * a.Wd + x) * a.C + c;
+    const long long mfl = (((long long)b * a.mask_h + y) * a.Wd + x) * a.C + c;
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      if (a.am) a.am[flat + e] = (uint8_t)bi[e];
+      if (a.mask) a.mask[mfl + e] = (uint8_t)bi[e];
+    }
   }
 }
 
-static unsigned grid_for(long long total) {
-  long long g = (total + 255) / 256;
-  if (g > 65536) g = 65536;
-  return (unsigned)(g < 1 ? 1 : g);
-}
 
 int launch_pool_fwd(int dt, const PoolArgs &a, void *stream) {
   const long long total = (long long)a.B * (a.y1 - a.y0) * a.Wd * a.C;
   if (total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DT_F32) pool_fwd_kernel<float><<<grid_for(total), 256, 0, s>>>(a);
-  else pool_fwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(a);
+  const bool v4 = a.C % 4 == 0;
+  const unsigned g = grid_for(v4 ? total / 4 : total);
+  if (dt == DT_F32) {
+    if (v4) pool_fwd_kernel<float, 4><<<g, 256, 0, s>>>(a);
+    else pool_fwd_kernel<float, 1><<<g, 256, 0, s>>>(a);
+  } else {
+    if (v4) pool_fwd_kernel<bf16, 4><<<g, 256, 0, s>>>(a);
+    else pool_fwd_kernel<bf16, 1><<<g, 256, 0, s>>>(a);
+  }
   return (int)hipGetLastError();
 }
 
+template <int V>
 __global__ void pool_bwd_kernel(PoolBwdArgs a) {
   const int Ru = a.ub - a.ua, R = a.y1 - a.y0;
-  const long long total = (long long)a.B * Ru * a.Wu * a.C;
+  const int CV = a.C / V;
+  const long long total = (long long)a.B * Ru * a.Wu * CV;
   const long long vrow = (long long)a.Wv * a.C, urow = (long long)a.Wu * a.C;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(idx % a.C);
-    long long t = idx / a.C;
+  GRID_STRIDE(idx, total) {
+    const int c = (int)(idx % CV) * V;
+    long long t = idx / CV;
     const int xi = (int)(t % a.Wu);
     t /= a.Wu;
     const int yi = a.ua + (int)(t % Ru);
@@ -734,192 +904,219 @@ __global__ void pool_bwd_kernel(PoolBwdArgs a) {
     const int yhi = min(a.y1 - 1, fdiv(yi + a.ph, a.sh));
     const int xlo = max(0, fdiv(xi + a.pw - a.kw, a.sw) + 1);
     const int xhi = min(a.Wv - 1, fdiv(xi + a.pw, a.sw));
-    float sum = 0.f;
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
     for (int y = ylo; y <= yhi; ++y)
       for (int x = xlo; x <= xhi; ++x) {
         const int tp = (yi - (y * a.sh - a.ph)) * a.kw + (xi - (x * a.sw - a.pw));
         const long long ai = (((long long)b * R + (y - a.y0)) * a.Wv + x) * a.C + c;
-        if (a.am[ai] == tp)
-          sum += ((const float *)a.dv.p)[b * a.dv.bs + (y - a.dv.row0) * vrow +
-                                         (long long)x * a.C + c];
+        float dv[4];
+        ldv<float, V>((const float *)a.dv.p + b * a.dv.bs + (y - a.dv.row0) * vrow +
+                          (long long)x * a.C + c, dv);
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+          if (a.am[ai + e] == tp) sum[e] += dv[e];
       }
     float *d = (float *)a.du.p + b * a.du.bs + (yi - a.du.row0) * urow + (long long)xi * a.C + c;
-    *d += sum;
+    float q[4];
+    ldv<float, V>(d, q);
+#pragma unroll
+    for (int e = 0; e < V; ++e) q[e] += sum[e];
+    stv<float, V>(d, q);
   }
 }
 
 int launch_pool_bwd(const PoolBwdArgs &a, void *stream) {
   const long long total = (long long)a.B * (a.ub - a.ua) * a.Wu * a.C;
   if (total <= 0) return 0;
-  pool_bwd_kernel<<<grid_for(total), 256, 0, (hipStream_t)stream>>>(a);
+  if (a.C % 4 == 0)
+    pool_bwd_kernel<4><<<grid_for(total / 4), 256, 0, (hipStream_t)stream>>>(a);
+  else
+    pool_bwd_kernel<1><<<grid_for(total), 256, 0, (hipStream_t)stream>>>(a);
   return (int)hipGetLastError();
 }
 
 // ------------------------------------------------------- elementwise rows
-struct RowIdx {
-  long long off;  // element offset of (b, row, inner) in a view
-};
-
-__device__ __forceinline__ long long view_off(const View &v, int b, int row,
-                                              int inner) {
-  return b * v.bs + (long long)(row - v.row0) * v.W * v.C + inner;
-}
-
-template <typename T>
+// Row-range kernels over band windows. When a row's W*C elements are a
+// multiple of 4, every thread handles 4 consecutive elements with one
+// 16-byte (float32) or 8-byte (bfloat16) access per tensor.
+template <typename T, int V>
 __global__ void add_fwd_kernel(View a, View bb, View z, int relu, uint8_t *mask,
-                               int mask_h, int B, int y0, int y1, int W, int C) {
-  const int R = y1 - y0;
-  const long long inner = (long long)W * C;
-  const long long total = (long long)B * R * inner;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int in = (int)(idx % inner);
-    const long long t = idx / inner;
-    const int y = y0 + (int)(t % R);
-    const int b = (int)(t / R);
-    float v = ldf((const T *)a.p + view_off(a, b, y, in)) +
-              ldf((const T *)bb.p + view_off(bb, b, y, in));
-    if (relu) v = v > 0.f ? v : 0.f;
-    stf((T *)z.p + view_off(z, b, y, in), v);
-    if (mask) mask[((long long)b * mask_h + y) * inner + in] = v > 0.f ? 1 : 0;
+                               int mask_h, RowIter it) {
+  const long long rowlen = (long long)z.W * z.C;
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    float u[4], w[4];
+    ldv<T, V>((const T *)a.p + view_off(a, b, y, in), u);
+    ldv<T, V>((const T *)bb.p + view_off(bb, b, y, in), w);
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      u[e] += w[e];
+      if (relu) u[e] = u[e] > 0.f ? u[e] : 0.f;
+      if (mask) mask[((long long)b * mask_h + y) * rowlen + in + e] = u[e] > 0.f ? 1 : 0;
+    }
+    stv<T, V>((T *)z.p + view_off(z, b, y, in), u);
   }
 }
 
 int launch_add_fwd(int dt, View a, View b, View z, int relu, uint8_t *mask,
                    int mask_h, int B, int y0, int y1, int W, int C, void *stream) {
-  const long long total = (long long)B * (y1 - y0) * W * C;
-  if (total <= 0) return 0;
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, y0, y1, W, C, V);
+  if (it.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DT_F32)
-    add_fwd_kernel<float><<<grid_for(total), 256, 0, s>>>(a, b, z, relu, mask, mask_h, B, y0, y1, W, C);
-  else
-    add_fwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(a, b, z, relu, mask, mask_h, B, y0, y1, W, C);
+  const unsigned g = grid_for(it.total);
+  if (dt == DT_F32) {
+    if (V == 4) add_fwd_kernel<float, 4><<<g, 256, 0, s>>>(a, b, z, relu, mask, mask_h, it);
+    else add_fwd_kernel<float, 1><<<g, 256, 0, s>>>(a, b, z, relu, mask, mask_h, it);
+  } else {
+    if (V == 4) add_fwd_kernel<bf16, 4><<<g, 256, 0, s>>>(a, b, z, relu, mask, mask_h, it);
+    else add_fwd_kernel<bf16, 1><<<g, 256, 0, s>>>(a, b, z, relu, mask, mask_h, it);
+  }
   return (int)hipGetLastError();
 }
 
-template <typename T>
-__global__ void add_bwd_kernel(View dz, View z, View da, View db, int relu, int B,
-                               int y0, int y1, int W, int C) {
-  const int R = y1 - y0;
-  const long long inner = (long long)W * C;
-  const long long total = (long long)B * R * inner;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int in = (int)(idx % inner);
-    const long long t = idx / inner;
-    const int y = y0 + (int)(t % R);
-    const int b = (int)(t / R);
-    float d = ((const float *)dz.p)[view_off(dz, b, y, in)];
-    if (relu && !(ldf((const T *)z.p + view_off(z, b, y, in)) > 0.f)) d = 0.f;
-    ((float *)da.p)[view_off(da, b, y, in)] += d;
-    ((float *)db.p)[view_off(db, b, y, in)] += d;
+template <typename T, int V>
+__global__ void add_bwd_kernel(View dz, View z, View da, View db, int relu, RowIter it) {
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    float d[4], zz[4], x[4];
+    ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
+    if (relu) {
+      ldv<T, V>((const T *)z.p + view_off(z, b, y, in), zz);
+#pragma unroll
+      for (int e = 0; e < V; ++e)
+        if (!(zz[e] > 0.f)) d[e] = 0.f;
+    }
+    float *pa = (float *)da.p + view_off(da, b, y, in);
+    ldv<float, V>(pa, x);
+#pragma unroll
+    for (int e = 0; e < V; ++e) x[e] += d[e];
+    stv<float, V>(pa, x);
+    float *pb = (float *)db.p + view_off(db, b, y, in);
+    ldv<float, V>(pb, x);
+#pragma unroll
+    for (int e = 0; e < V; ++e) x[e] += d[e];
+    stv<float, V>(pb, x);
   }
 }
 
 int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
                    int y0, int y1, int W, int C, void *stream) {
-  const long long total = (long long)B * (y1 - y0) * W * C;
-  if (total <= 0) return 0;
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, y0, y1, W, C, V);
+  if (it.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DT_F32)
-    add_bwd_kernel<float><<<grid_for(total), 256, 0, s>>>(dz, z, da, db, relu, B, y0, y1, W, C);
-  else
-    add_bwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(dz, z, da, db, relu, B, y0, y1, W, C);
+  const unsigned g = grid_for(it.total);
+  if (dt == DT_F32) {
+    if (V == 4) add_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+    else add_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+  } else {
+    if (V == 4) add_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+    else add_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+  }
   return (int)hipGetLastError();
 }
 
-template <typename T>
-__global__ void act_bwd_kernel(View dz, View z, const float *scale, int relu,
-                               T *dc, int B, int y0, int y1, int W, int C) {
-  const int R = y1 - y0;
-  const long long inner = (long long)W * C;
-  const long long total = (long long)B * R * inner;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int in = (int)(idx % inner);
-    const long long t = idx / inner;
-    const int y = y0 + (int)(t % R);
-    const int b = (int)(t / R);
-    float d = ((const float *)dz.p)[view_off(dz, b, y, in)];
-    if (relu && !(ldf((const T *)z.p + view_off(z, b, y, in)) > 0.f)) d = 0.f;
-    if (scale) d *= scale[in % C];
-    stf(dc + idx, d);
+template <typename T, int V>
+__global__ void act_bwd_kernel(View dz, View z, const float *scale, int relu, T *dc,
+                               int C, RowIter it) {
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    float d[4], zz[4];
+    ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
+    if (relu) {
+      ldv<T, V>((const T *)z.p + view_off(z, b, y, in), zz);
+#pragma unroll
+      for (int e = 0; e < V; ++e)
+        if (!(zz[e] > 0.f)) d[e] = 0.f;
+    }
+    if (scale) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) d[e] *= scale[(in + e) % C];
+    }
+    stv<T, V>(dc + idx * V, d);
   }
 }
 
 int launch_act_bwd(int dt, View dz, View z, const float *scale, int relu,
                    void *dc, int B, int y0, int y1, int W, int C, void *stream) {
-  const long long total = (long long)B * (y1 - y0) * W * C;
-  if (total <= 0) return 0;
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, y0, y1, W, C, V);
+  if (it.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DT_F32)
-    act_bwd_kernel<float><<<grid_for(total), 256, 0, s>>>(dz, z, scale, relu, (float *)dc, B, y0, y1, W, C);
-  else
-    act_bwd_kernel<bf16><<<grid_for(total), 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, B, y0, y1, W, C);
+  const unsigned g = grid_for(it.total);
+  if (dt == DT_F32) {
+    if (V == 4) act_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it);
+    else act_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it);
+  } else {
+    if (V == 4) act_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it);
+    else act_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it);
+  }
   return (int)hipGetLastError();
 }
 
-template <typename TS, typename TD>
-__global__ void rows_copy_kernel(View src, View dst, int accumulate, int B,
-                                 int r0, int r1, int W, int C) {
-  const int R = r1 - r0;
-  const long long inner = (long long)W * C;
-  const long long total = (long long)B * R * inner;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int in = (int)(idx % inner);
-    const long long t = idx / inner;
-    const int y = r0 + (int)(t % R);
-    const int b = (int)(t / R);
-    float v = ldf((const TS *)src.p + view_off(src, b, y, in));
-    TD *d = (TD *)dst.p + view_off(dst, b, y, in);
-    if (accumulate) v += ldf(d);
-    stf(d, v);
+template <typename TS, typename TD, int V>
+__global__ void rows_copy_kernel(View src, View dst, int accumulate, RowIter it) {
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    float v[4], d[4];
+    ldv<TS, V>((const TS *)src.p + view_off(src, b, y, in), v);
+    TD *pd = (TD *)dst.p + view_off(dst, b, y, in);
+    if (accumulate) {
+      ldv<TD, V>(pd, d);
+#pragma unroll
+      for (int e = 0; e < V; ++e) v[e] += d[e];
+    }
+    stv<TD, V>(pd, v);
   }
+}
+
+template <typename TS, typename TD>
+static void rows_copy_go(View src, View dst, int acc, RowIter it, int V, hipStream_t s) {
+  const unsigned g = grid_for(it.total);
+  if (V == 4) rows_copy_kernel<TS, TD, 4><<<g, 256, 0, s>>>(src, dst, acc, it);
+  else rows_copy_kernel<TS, TD, 1><<<g, 256, 0, s>>>(src, dst, acc, it);
 }
 
 int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate, int B,
                      int r0, int r1, int W, int C, void *stream) {
-  const long long total = (long long)B * (r1 - r0) * W * C;
-  if (total <= 0) return 0;
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, r0, r1, W, C, V);
+  if (it.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  unsigned g = grid_for(total);
-  if (st == DT_F32 && dtt == DT_F32)
-    rows_copy_kernel<float, float><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
-  else if (st == DT_F32)
-    rows_copy_kernel<float, bf16><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
-  else if (dtt == DT_F32)
-    rows_copy_kernel<bf16, float><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
-  else
-    rows_copy_kernel<bf16, bf16><<<g, 256, 0, s>>>(src, dst, accumulate, B, r0, r1, W, C);
+  if (st == DT_F32 && dtt == DT_F32) rows_copy_go<float, float>(src, dst, accumulate, it, V, s);
+  else if (st == DT_F32) rows_copy_go<float, bf16>(src, dst, accumulate, it, V, s);
+  else if (dtt == DT_F32) rows_copy_go<bf16, float>(src, dst, accumulate, it, V, s);
+  else rows_copy_go<bf16, bf16>(src, dst, accumulate, it, V, s);
   return (int)hipGetLastError();
 }
 
-__global__ void rows_zero_kernel(View dst, int B, int r0, int r1, int W, int C) {
-  const int R = r1 - r0;
-  const long long inner = (long long)W * C;
-  const long long total = (long long)B * R * inner;
-  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (long long)gridDim.x * blockDim.x) {
-    const int in = (int)(idx % inner);
-    const long long t = idx / inner;
-    const int y = r0 + (int)(t % R);
-    const int b = (int)(t / R);
-    ((float *)dst.p)[view_off(dst, b, y, in)] = 0.f;
+template <int V>
+__global__ void rows_zero_kernel(View dst, RowIter it) {
+  const float z[4] = {0.f, 0.f, 0.f, 0.f};
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    stv<float, V>((float *)dst.p + view_off(dst, b, y, in), z);
   }
 }
 
 int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C, void *stream) {
-  const long long total = (long long)B * (r1 - r0) * W * C;
-  if (total <= 0) return 0;
-  rows_zero_kernel<<<grid_for(total), 256, 0, (hipStream_t)stream>>>(dst, B, r0, r1, W, C);
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, r0, r1, W, C, V);
+  if (it.total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (V == 4) rows_zero_kernel<4><<<grid_for(it.total), 256, 0, s>>>(dst, it);
+  else rows_zero_kernel<1><<<grid_for(it.total), 256, 0, s>>>(dst, it);
   return (int)hipGetLastError();
 }
 
 __global__ void zero_kernel(float *p, long long n) {
-  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-       i += (long long)gridDim.x * blockDim.x)
-    p[i] = 0.f;
+  GRID_STRIDE(i, n) p[i] = 0.f;
 }
 
 int launch_zero_f32(float *p, size_t n, void *stream) {

@@ -46,19 +46,38 @@ int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 inline int conv_split_count(long long M, int N, int KT, size_t cap) {
   const long long bn = N <= 64 ? 64 : 128;
   const long long tiles = ((M + 127) / 128) * ((N + bn - 1) / bn);
-  const long long target = 512;
-  if (tiles >= target || KT < 16) return 1;
-  long long s = (target + tiles - 1) / tiles;
-  s = s < KT / 8 ? s : KT / 8;
+  const long long cus = 256;
+  if (tiles >= 2 * cus || KT < 16) return 1;
   const long long per = M * (long long)N * 4;
-  if (per > 0 && s * per > (long long)cap) s = (long long)cap / per;
-  if (s < 2) return 1;
-  const long long kts = (KT + s - 1) / s;
+  // score: balance over the CUs (every CU gets the same number of
+  // workgroups), enough workgroups for two per CU, a small charge per
+  // split for the partial sums
+  auto score = [&](long long s) {
+    const long long wg = tiles * s;
+    const double bal = (double)wg / (double)(cus * ((wg + cus - 1) / cus));
+    const double fill = wg >= 2 * cus ? 1.0 : (double)wg / (2.0 * cus);
+    return bal * fill - 0.01 * (double)(s - 1);
+  };
+  long long best = 1;
+  double bs = score(1);
+  for (long long s = 2; s <= KT / 8 && s <= 64; ++s) {
+    if (per > 0 && s * per > (long long)cap) break;
+    const double sc = score(s);
+    if (sc > bs + 1e-9) {
+      bs = sc;
+      best = s;
+    }
+  }
+  const long long kts = (KT + best - 1) / best;
   return (int)((KT + kts - 1) / kts);
 }
-// K iterations of a conv for storage element size es (bytes).
+// K iterations of a conv for storage element size es (bytes); one
+// iteration covers LRCNN_CONV_KR 16-byte vectors of a tile row.
+#ifndef LRCNN_CONV_KR
+#define LRCNN_CONV_KR 4
+#endif
 inline int conv_k_iters(int taps, int kc, int es) {
-  const int bk = 64 / es;
+  const int bk = 16 * LRCNN_CONV_KR / es;
   return taps * ((kc + bk - 1) / bk);
 }
 

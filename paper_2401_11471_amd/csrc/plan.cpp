@@ -47,9 +47,11 @@ static void ksp(const lrcnn_node &nd, int &k, int &s, int &p) {
 
 int wgrad_splits(int64_t m, int64_t n, int64_t k) {
   const int64_t bm = 128, bn = 128, min_k = 256, target = 512;
+  const int64_t cap = (int64_t)24 << 20;  // bytes of partial sums
   int64_t tiles = ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
   int64_t s = (target + tiles - 1) / tiles;
   s = std::min<int64_t>(s, std::max<int64_t>(1, k / min_k));
+  s = std::min<int64_t>(s, std::max<int64_t>(1, cap / (m * n * 4)));
   return (int)std::max<int64_t>(1, std::min<int64_t>(s, 512));
 }
 
@@ -338,7 +340,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   size_t part = 0;
   std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
   splits.assign(n, 1);
-  const size_t conv_cap = (size_t)64 << 20;
+  const size_t conv_cap = (size_t)24 << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];

@@ -56,6 +56,7 @@ struct Plan {
   // state for the FP -> BP hand-over of CARRY mode
   const void *fwd_workspace = nullptr;
   uint64_t fwd_epoch = 0;
+  bool last_band_kept = false;  // FP left the last band's maps in place
 
   size_t elems(int v, int rows_) const {
     return (size_t)cfg.batch * rows_ * shp[v].w * shp[v].c;
