@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--config", type=int, default=2, help="workload id 1..5")
     ap.add_argument("--mode", default="carry", choices=["carry", "balanced", "recompute"])
     ap.add_argument("--bands", type=int, default=0, help="override the band count")
+    ap.add_argument("--bp-refine", type=int, default=1,
+                    help="backward bands per forward band (finer BP partition)")
     ap.add_argument("--batch", type=int, default=0, help="override the batch")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the layer-wise / recompute comparison runs")
@@ -101,7 +103,8 @@ def main():
     B, H, W, Cin = inp.x.shape
     dts = "bf16" if inp.dtype == BF16 else "f32"
 
-    plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy)
+    plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy,
+                        bp_refine=args.bp_refine)
     info = plan.info()
     dm = DeviceModel.from_inputs(nodes, inp)
     out_shape = (B,) + plan.node_shape(len(nodes) - 1)
@@ -173,8 +176,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": dts, "data": "synthetic N(0,1), paper's shapes (ImageNet not available)",
         "config": {"workload": c["name"], "net": c["net"], "batch": B,
-                   "input": [Cin, H, W], "bands": nb, "mode": args.mode,
-                   "dx": False},
+                   "input": [Cin, H, W], "bands": nb, "bp_bands": info["bp_bands"],
+                   "mode": args.mode, "dx": False},
         "roofline": roofline,
         "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),
         "mfma_kernels": {"ms_per_step": round(all_mfma_ms, 3),
@@ -185,7 +188,8 @@ def main():
                                         for k, v in sorted(kern.items())}},
         "peak_act_bytes": int(peak_rc),
         "analytic": {k: info[k] for k in ("workspace_bytes", "layerwise_workspace_bytes",
-                                          "strip_bytes", "band_cache_bytes", "delta_bytes",
+                                          "strip_bytes", "band_cache_bytes",
+                                          "fp_window_bytes", "delta_bytes",
                                           "partial_bytes", "omega_bytes", "flops_tau",
                                           "flops_rows", "shared_rows", "halo_rows")},
     }
@@ -222,7 +226,8 @@ def main():
             out["layerwise"] = {"error": str(ex)[:200]}
         torch.cuda.empty_cache()
         if mode == L.CARRY:
-            rplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.RECOMPUTE, nb)
+            rplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.RECOMPUTE, nb,
+                                 bp_refine=args.bp_refine)
             rinfo = rplan.info()
             rws = dm.workspace(rinfo["workspace_bytes"])
             ry = dm.empty(out_shape)

@@ -99,9 +99,13 @@ typedef struct {
   int32_t batch, in_c, in_h, in_w;
   int32_t dtype;             /* LRCNN_F32 | LRCNN_BF16                        */
   int32_t mode;              /* LRCNN_CARRY | LRCNN_RECOMPUTE                 */
-  int32_t n_bands;           /* N >= 1                                        */
+  int32_t n_bands;           /* N >= 1: bands of the forward pass             */
   int32_t policy;            /* LRCNN_EVEN | LRCNN_BALANCED | LRCNN_EXPLICIT  */
   const int32_t *bounds;     /* host array, used when policy == EXPLICIT      */
+  int32_t bp_refine;         /* >= 1 (0 reads as 1): the backward pass splits */
+                             /* every forward band evenly into bp_refine      */
+                             /* bands, N_BP = N * bp_refine (the paper's finer */
+                             /* BP granularity, Section III-C)                */
 } lrcnn_config;
 
 /* Opaque plan handle (host memory only). */
@@ -109,7 +113,7 @@ typedef struct lrcnn_plan_s lrcnn_plan_t;
 
 /* Analytic figures of a plan. Byte counts include the batch. */
 typedef struct {
-  int32_t n_nodes, n_bands, mode, dtype;
+  int32_t n_nodes, n_bands, mode, dtype;  /* n_bands: forward bands          */
   int32_t out_h, out_w, out_c;
   size_t workspace_bytes;          /* forward_rows + backward_rows          */
   size_t layerwise_workspace_bytes;/* lrcnn_layerwise_reference_gpu         */
@@ -127,6 +131,9 @@ typedef struct {
   int64_t shared_rows;             /* CARRY: sum of kept rows over bands    */
   int64_t halo_rows;               /* RECOMPUTE: rows computed by more than */
                                    /* one band, summed over nodes and bands */
+  int32_t bp_bands;                /* backward bands (n_bands * bp_refine)  */
+  size_t fp_window_bytes;          /* forward windows (lifetime-packed when */
+                                   /* bp_refine > 1, else the band cache)   */
 } lrcnn_plan_info;
 
 /* Build a plan: shapes of every node, per-band row intervals, workspace
@@ -146,12 +153,13 @@ int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info);
 int lrcnn_plan_node_shape(const lrcnn_plan_t *plan, int32_t node,
                           int32_t shape[3]);
 
-/* Rows of node `node` in band `band` (0-based): rows[0..1] = the rows the
- * band computes and owns [a, b); rows[2..3] = the rows it holds [lo, hi)
- * (CARRY: own rows plus the rows shared from earlier bands; RECOMPUTE: the
- * band's receptive cone). Errors: EINVAL. */
-int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t band, int32_t node,
-                         int32_t rows[4]);
+/* Rows of node `node` in band `band` (0-based) of the forward (phase 0) or
+ * backward (phase 1) partition: rows[0..1] = the rows the band computes and
+ * owns [a, b); rows[2..3] = the rows it holds [lo, hi) (CARRY: own rows plus
+ * the rows shared from earlier bands; RECOMPUTE: the band's receptive cone).
+ * Errors: EINVAL. */
+int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int32_t band,
+                         int32_t node, int32_t rows[4]);
 
 void lrcnn_plan_destroy(lrcnn_plan_t *plan);
 

@@ -145,6 +145,9 @@ struct Run {
 
   // Compute the feature maps of band `r` for every node (FP, or the BP
   // recompute of Algorithm 1). The output node goes to `y` when given.
+  // Feature maps of one band for every node: the forward pass (bp = false,
+  // forward band r) or the BP recompute (bp = true, backward band r) of
+  // Algorithm 1. The output node goes to `y` when given.
   // `keep`: the band's maps stay in the window buffers for the BP that
   // follows (the output node is computed into its window and copied to y,
   // pool argmax bytes are recorded), so BP can skip recomputing this band.
@@ -153,19 +156,28 @@ struct Run {
   int band_fwd(int r, void *y, void *const *mask_out, bool bp, bool keep = false,
                bool views_only = false) {
     const int n = P.n;
+    const bool fp = !bp && sched != S_LAYERWISE;
+    const bool packed = fp && L.fp_packed;
     for (int v = 1; v < n; ++v) {
-      const Rows q = band_rows(r, v);
+      const Rows q = fp ? P.rows_fp[r][v] : band_rows(r, v);
       View dst;
       if (v == n - 1 && y && !keep) {
         dst = full(y, v);
+      } else if (packed) {
+        dst = win(L.fwin[v], v, L.fwin_cap[v], q.lo);
       } else {
         dst = win(L.win[v], v, L.win_cap[v], q.lo);
       }
       act[v] = dst;
       if (views_only) continue;
       if (sched == S_CARRY && r > 0 && q.a > q.lo) {
-        // rows shared from earlier bands (two-phase sharing)
-        View strip = win(L.strip[r - 1][v], v, q.a - q.lo, q.lo);
+        // rows shared from earlier bands (two-phase sharing): kept at the
+        // backward boundary that ends where this band starts
+        const int sidx = fp ? r * P.refine - 1 : r - 1;
+        View strip = win(L.strip[sidx][v], v, q.a - q.lo, q.lo);
+        if (!holds(strip, P.tail[sidx][v], P.rows[sidx][v].b) || P.tail[sidx][v] != q.lo ||
+            P.rows[sidx][v].b != q.a)
+          return lrcnn_fail(LRCNN_EINVAL, "internal: strip rows do not match the band");
         LAUNCH(launch_rows_copy(dt, dt, strip, dst, 0, P.cfg.batch, q.lo, q.a,
                                 P.shp[v].w, P.shp[v].c, stream),
                "strip load");
@@ -179,11 +191,17 @@ struct Run {
         LAUNCH(launch_rows_copy(dt, dt, dst, full(y, v), 0, P.cfg.batch, q.a, q.b,
                                 P.shp[v].w, P.shp[v].c, stream),
                "output store");
-      if (sched == S_CARRY && !bp && r + 1 < P.nb && v != n - 1) {
-        const int t = P.tail[r][v];
-        if (q.b > t) {
-          View strip = win(L.strip[r][v], v, q.b - t, t);
-          LAUNCH(launch_rows_copy(dt, dt, dst, strip, 0, P.cfg.batch, t, q.b,
+      if (sched == S_CARRY && fp && v != n - 1) {
+        // keep the shared rows of every backward boundary inside this band
+        for (int j = 0; j < P.refine; ++j) {
+          const int sidx = r * P.refine + j;
+          if (sidx + 1 >= P.nb) break;
+          const int t = P.tail[sidx][v], e = P.rows[sidx][v].b;
+          if (e <= t) continue;
+          View strip = win(L.strip[sidx][v], v, e - t, t);
+          if (!holds(dst, t, e))
+            return lrcnn_fail(LRCNN_EINVAL, "internal: strip rows not in the band window");
+          LAUNCH(launch_rows_copy(dt, dt, dst, strip, 0, P.cfg.batch, t, e,
                                   P.shp[v].w, P.shp[v].c, stream),
                  "strip store");
         }
@@ -431,10 +449,14 @@ extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void 
           aff_shift, stream);
   P.fwd_workspace = nullptr;
   P.last_band_kept = false;
-  for (int r = 0; r < P.nb; ++r)
-    if ((st = run.band_fwd(r, y, mask_out, false, r == P.nb - 1)) != LRCNN_OK) return st;
+  // the last band's maps can serve the BP only when both passes use the
+  // same partition
+  const bool keep = P.refine == 1;
+  for (int r = 0; r < P.nb_fp; ++r)
+    if ((st = run.band_fwd(r, y, mask_out, false, keep && r == P.nb_fp - 1)) != LRCNN_OK)
+      return st;
   P.fwd_workspace = workspace;
-  P.last_band_kept = true;
+  P.last_band_kept = keep;
   P.fwd_epoch = ++g_epoch;
   return LRCNN_OK;
 }

@@ -142,44 +142,66 @@ constexpr int BM = 128;
 // tile row. A and B use the same slice order, so every MFMA adds products of
 // matching K indices; the order in which K is summed is the same for every
 // output element and every band.
-template <typename T, int BN, int KR>
+// AKM / BKM select the LDS layout of an operand: 0 = [row][k] (pitch
+// LDK), fragments read as 16-byte vectors; 1 = [k][row] (pitch rows + 4),
+// fragments read as 4-byte words. k-major staging lets operands whose global
+// layout is K-outer (the input gradient's weights, both weight-gradient
+// operands) be stored with 16-byte writes; it is used for float32, where
+// one element feeds one MFMA.
+template <typename T, int BN, int KR, int AKM = 0, int BKM = 0>
 struct Frag;
 
-template <int BN, int KR>
-struct Frag<float, BN, KR> {
+template <int BN, int KR, int AKM, int BKM>
+struct Frag<float, BN, KR, AKM, BKM> {
   static constexpr int LDK = Cfg<float, KR>::LDK, NB = BN / 64, NV = KR / 2;
-  float4 a[2][NV], b[NB][NV];
+  static constexpr int S = 4 * NV;            // K elements per lane group
+  static constexpr int PA = BM + 4, PB = BN + 4;
+  float a[2][S], b[NB][S];
   __device__ __forceinline__ void load(const float *As, const float *Bs, int wm, int wn,
                                        int lane) {
     const int r = lane & 31, g = lane >> 5;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + 4 * NV * g);
+      if (AKM) {
 #pragma unroll
-      for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+        for (int s = 0; s < S; ++s) a[i][s] = As[(S * g + s) * PA + wm + 32 * i + r];
+      } else {
+        const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + S * g);
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+          const float4 t = p[q];
+          a[i][4 * q] = t.x, a[i][4 * q + 1] = t.y, a[i][4 * q + 2] = t.z, a[i][4 * q + 3] = t.w;
+        }
+      }
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + 4 * NV * g);
+      if (BKM) {
 #pragma unroll
-      for (int q = 0; q < NV; ++q) b[j][q] = p[q];
+        for (int s = 0; s < S; ++s) b[j][s] = Bs[(S * g + s) * PB + wn + 32 * j + r];
+      } else {
+        const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + S * g);
+#pragma unroll
+        for (int q = 0; q < NV; ++q) {
+          const float4 t = p[q];
+          b[j][4 * q] = t.x, b[j][4 * q + 1] = t.y, b[j][4 * q + 2] = t.z, b[j][4 * q + 3] = t.w;
+        }
+      }
     }
   }
   __device__ __forceinline__ void mma(f32x16 (&acc)[2][NB]) const {
 #pragma unroll
-    for (int s = 0; s < 4 * NV; ++s)
+    for (int s = 0; s < S; ++s)
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < NB; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][s >> 2][s & 3],
-                                                           b[j][s >> 2][s & 3], acc[i][j],
-                                                           0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][s], b[j][s], acc[i][j], 0, 0, 0);
   }
 };
 
 template <int BN, int KR>
-struct Frag<bf16, BN, KR> {
+struct Frag<bf16, BN, KR, 0, 0> {
   static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
   bf16x8 a[2][NV], b[NB][NV];
   __device__ __forceinline__ void load(const bf16 *As, const bf16 *Bs, int wm, int wn,
@@ -210,14 +232,6 @@ struct Frag<bf16, BN, KR> {
   }
 };
 
-template <int BN, int KR, typename T>
-__device__ __forceinline__ void mma_tile(const T *As, const T *Bs,
-                                         f32x16 (&acc)[2][BN / 64], int wm, int wn,
-                                         int lane) {
-  Frag<T, BN, KR> f;
-  f.load(As, Bs, wm, wn, lane);
-  f.mma(acc);
-}
 
 // Row of the 32x32 accumulator block held in register v of lane l.
 __device__ __forceinline__ int acc_row(int v, int lane) {
@@ -322,8 +336,12 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // three LDS stages: while tile t is multiplied, the fragments of t+1 are
   // read, tile t+2 is written and tile t+3 is fetched from global memory
   constexpr int ST = 3;
+  // float32 input gradient: weights staged k-major (16-byte stores)
+  constexpr int BKM = (DGRAD && sizeof(T) == 4) ? 1 : 0;
+  constexpr int PB = BN + 4;
+  constexpr int BSZ = BKM ? BK * PB : BN * LDK;
   __shared__ __align__(16) T As[ST][BM * LDK];
-  __shared__ __align__(16) T Bs[ST][BN * LDK];
+  __shared__ __align__(16) T Bs[ST][BSZ];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
@@ -437,7 +455,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + kv * E]) = ra[i];
 #pragma unroll
     for (int j = 0; j < NBL; ++j) {
-      if (DGRAD) {
+      if (BKM) {
+        *(uint4 *)(&Bs[st][(bk0 + BKS * j) * PB + (tid % BV) * E]) = rb[j];
+      } else if (DGRAD) {
         union {
           uint4 u;
           T e[E];
@@ -462,10 +482,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
   if (n > 2) gload();
   __syncthreads();
-  Frag<T, BN, KR> f0, f1;
+  using FR = Frag<T, BN, KR, 0, BKM>;
+  FR f0, f1;
   if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
   int s1 = 1, s2 = 2;  // stages of tiles t+1 and t+2
-  auto step = [&](int t, Frag<T, BN, KR> &cur, Frag<T, BN, KR> &nxt) {
+  auto step = [&](int t, FR &cur, FR &nxt) {
     if (t + 1 < n) nxt.load(As[s1], Bs[s1], wm, wn, lane);
     if (t + 2 < n) {
       store(s2);
@@ -649,8 +670,14 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
   constexpr int BN = 128, NB = 2;
   constexpr int RV = BM / E;        // 16-byte vectors per 128-wide tile row
   constexpr int KS = 256 / RV;      // pixels loaded per pass
-  __shared__ __align__(16) T As[2][BM * LDK];
-  __shared__ __align__(16) T Bs[2][BN * LDK];
+  // float32: both operands staged k-major with 16-byte stores; bfloat16:
+  // transposed element stores into the [row][k] layout
+  constexpr int KM = sizeof(T) == 4 ? 1 : 0;
+  constexpr int PA = BM + 4, PB = BN + 4;
+  constexpr int ASZ = KM ? BK * PA : BM * LDK, BSZ = KM ? BK * PB : BN * LDK;
+  constexpr int ST = 3;
+  __shared__ __align__(16) T As[ST][ASZ];
+  __shared__ __align__(16) T Bs[ST][BSZ];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int K = a.B * R * a.Wv;
@@ -666,25 +693,29 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
 
   // this thread's B columns n0 + rv*E + e: (tap, channel) of each element
   const int nb0 = n0 + rv * E;
-  int tapv = nb0 / a.Ci, cv = nb0 - (nb0 / a.Ci) * a.Ci;
+  const int tapv = nb0 / a.Ci, cv = nb0 - (nb0 / a.Ci) * a.Ci;
   const int tiv = tapv / a.kw, tjv = tapv - (tapv / a.kw) * a.kw;
   const int ov = m0 + rv * E;
 
-  T ra[2][E], rb[2][E];
-  auto gload = [&](int k0) {
+  union V16 {
+    uint4 u;
+    T e[E];
+  };
+  V16 ra[2], rb[2];
+  int k0 = kbeg;
+  auto gload = [&]() {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int p = k0 + kk0 + KS * i;
       const bool pk = p < kend;
       // A: E output channels of pixel p
       if (VEC) {
-        uint4 u = (pk && ov < a.Co) ? *(const uint4 *)(dc + (long long)p * a.Co + ov)
+        ra[i].u = (pk && ov < a.Co) ? *(const uint4 *)(dc + (long long)p * a.Co + ov)
                                     : make_uint4(0, 0, 0, 0);
-        *(uint4 *)ra[i] = u;
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e)
-          ra[i][e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
+          ra[i].e[e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
       }
       // B: E input values of pixel p under the column's tap
       int x = 0, y = 0, b = 0;
@@ -697,11 +728,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       if (VEC) {
         int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
         bool ok = pk && nb0 < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (ok)
-          u = *(const uint4 *)(src + b * a.src.bs + (sy - a.src.row0) * srow +
-                               (long long)sx * a.src.C + cv);
-        *(uint4 *)rb[i] = u;
+        rb[i].u = ok ? *(const uint4 *)(src + b * a.src.bs + (sy - a.src.row0) * srow +
+                                        (long long)sx * a.src.C + cv)
+                     : make_uint4(0, 0, 0, 0);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -710,9 +739,26 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
           const int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
           const int sy = y * a.sh - a.ph + ti, sx = x * a.sw - a.pw + tj;
           const bool ok = pk && n < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
-          rb[i][e] = ok ? src[b * a.src.bs + (sy - a.src.row0) * srow +
-                              (long long)sx * a.src.C + c]
-                        : (T)0;
+          rb[i].e[e] = ok ? src[b * a.src.bs + (sy - a.src.row0) * srow +
+                                (long long)sx * a.src.C + c]
+                          : (T)0;
+        }
+      }
+    }
+    k0 += BK;
+  };
+  auto store = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int kk = kk0 + KS * i;
+      if (KM) {
+        *(uint4 *)(&As[st][kk * PA + rv * E]) = ra[i].u;
+        *(uint4 *)(&Bs[st][kk * PB + rv * E]) = rb[i].u;
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          As[st][(rv * E + e) * LDK + kk] = ra[i].e[e];
+          Bs[st][(rv * E + e) * LDK + kk] = rb[i].e[e];
         }
       }
     }
@@ -727,21 +773,38 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
-  const int KT = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
-  if (KT > 0) gload(kbeg);
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        As[buf][(rv * E + e) * LDK + kk0 + KS * i] = ra[i][e];
-        Bs[buf][(rv * E + e) * LDK + kk0 + KS * i] = rb[i][e];
-      }
-    __syncthreads();
-    if (kt + 1 < KT) gload(kbeg + (kt + 1) * BK);
-    mma_tile<BN, 4>(As[buf], Bs[buf], acc, wm, wn, lane);
+  const int n = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (n > 0) {
+    gload();
+    store(0);
   }
+  if (n > 1) {
+    gload();
+    store(1);
+  }
+  if (n > 2) gload();
+  __syncthreads();
+  using FR = Frag<T, BN, 4, KM, KM>;
+  FR f0, f1;
+  if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
+  int s1 = 1, s2 = 2;
+  auto step = [&](int t, FR &cur, FR &nxt) {
+    if (t + 1 < n) nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    if (t + 2 < n) {
+      store(s2);
+      if (t + 3 < n) gload();
+    }
+    cur.mma(acc);
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < n; t += 2) {
+    step(t, f0, f1);
+    step(t + 1, f1, f0);
+  }
+  if (t < n) step(t, f0, f1);
 
   const int col = lane & 31;
   float *out = gridDim.z == 1 ? dw : a.out + (long long)blockIdx.z * a.Co * N;
@@ -753,9 +816,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       if (m >= a.Co) continue;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
-        const int n = n0 + wn + 32 * j + col;
-        if (n >= N) continue;
-        float *d = out + (long long)m * N + n;
+        const int nn = n0 + wn + 32 * j + col;
+        if (nn >= N) continue;
+        float *d = out + (long long)m * N + nn;
         if (gridDim.z == 1) *d += acc[i][j][v];
         else *d = acc[i][j][v];
       }

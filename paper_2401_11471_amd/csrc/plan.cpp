@@ -216,6 +216,8 @@ static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
     return lrcnn_fail(LRCNN_EINVAL, "BALANCED applies to CARRY mode only");
   if (cfg->policy == LRCNN_EXPLICIT && !cfg->bounds)
     return lrcnn_fail(LRCNN_EINVAL, "EXPLICIT policy needs bounds");
+  if (cfg->bp_refine < 0 || cfg->bp_refine > 64)
+    return lrcnn_fail(LRCNN_EINVAL, "bp_refine must be in [0, 64]");
   for (int v = 1; v < n; ++v) {
     const lrcnn_node &d = nodes[v];
     std::string at = "node " + std::to_string(v) + ": ";
@@ -278,11 +280,16 @@ static size_t pack(std::vector<LiveBuf> &bufs) {
   return peak;
 }
 
-// Lay out one workspace. `cap[v]` = window rows; `own[v]` = most rows a band
-// owns; `carry[v]` = rows of carried error (CARRY only); strips per band.
+// Lay out one workspace. Backward (and, unless packed, forward) windows
+// hold cap[v] rows, a band owns at most own[v] rows, carry[v] rows of error
+// are carried (CARRY). `bands` lists the row intervals of every launch
+// (forward and backward partitions) for sizing the partial sums; `fpw`
+// (nullable) gives the forward windows' rows when they are packed by
+// lifetime.
 static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
                    const std::vector<int> &own, const std::vector<int> &carry,
-                   bool strips, bool layerwise, bool dxacc) {
+                   const std::vector<const std::vector<std::vector<Rows>> *> &bands,
+                   bool strips, bool layerwise, bool dxacc, const std::vector<int> *fpw) {
   const int n = P.n;
   Alloc A;
   L = Layout();
@@ -294,6 +301,9 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   L.carry.assign(n, 0);
   L.carry_cap = carry;
   L.strip.assign(P.nb, std::vector<size_t>(n, 0));
+  L.fwin.assign(n, 0);
+  L.fwin_cap.assign(n, 0);
+  // strips: shared rows kept from FP to BP at every backward band boundary
   if (strips) {
     size_t s0 = A.top;
     for (int r = 0; r + 1 < P.nb; ++r)
@@ -303,6 +313,42 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
       }
     L.strip_bytes = A.top - s0;
   }
+  // partial sums (used by FP and BP): weight-gradient splits, and split-K
+  // of the convolution forward / input gradient on launches with few tiles
+  size_t part = 0;
+  std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
+  splits.assign(n, 1);
+  const size_t conv_cap = (size_t)24 << 20;
+  for (int v = 1; v < n; ++v)
+    if (P.nodes[v].op == LRCNN_OP_CONV) {
+      const lrcnn_node &d = P.nodes[v];
+      const Shape &su = P.shp[d.in0], &sv = P.shp[v];
+      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * su.c;
+      int64_t k = (int64_t)P.cfg.batch * own[v] * sv.w;
+      int s = wgrad_splits(m, nn, k);
+      splits[v] = s;
+      if (s > 1) part = std::max(part, (size_t)s * m * nn * 4);
+      const int taps = d.kh * d.kw;
+      std::vector<Rows> qs;
+      if (layerwise) qs.push_back(Rows{0, sv.h, 0, sv.h});
+      for (auto *tab : bands)
+        for (auto &br : *tab) qs.push_back(br[v]);
+      for (const Rows &q : qs) {
+        if (q.b <= q.a) continue;
+        long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
+        int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), conv_cap);
+        if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
+        int u0 = std::max(0, q.a * d.sh - d.ph);
+        int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
+        long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
+        int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), conv_cap);
+        if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
+      }
+    }
+  L.part_bytes = part;
+  L.part = A.take(part);
+  const size_t ubase = A.top;
+  // --- backward region (also the forward windows unless packed)
   size_t c0 = A.top;
   for (int v = 1; v < n; ++v) {
     if (layerwise && v == n - 1) continue;  // the output node lives in y
@@ -322,7 +368,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   // consumer in reverse order (the largest consumer id) to its own step
   std::vector<LiveBuf> bufs(n);
   for (int v = 0; v < n; ++v) {
-    int first = (v == n - 1) ? v : v;
+    int first = v;
     for (int c : P.cons[v]) first = std::max(first, c);
     bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, cap[v]) * 4, 0};
   }
@@ -335,43 +381,32 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
     if (P.nodes[v].op == LRCNN_OP_CONV) dc = std::max(dc, P.elems(v, own[v]) * P.es);
   L.dc_bytes = dc;
   L.dc = A.take(dc);
-  // partial sums: weight-gradient splits, and split-K of the convolution
-  // forward / input gradient on launches with few output tiles
-  size_t part = 0;
-  std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
-  splits.assign(n, 1);
-  const size_t conv_cap = (size_t)24 << 20;
-  for (int v = 1; v < n; ++v)
-    if (P.nodes[v].op == LRCNN_OP_CONV) {
-      const lrcnn_node &d = P.nodes[v];
-      const Shape &su = P.shp[d.in0], &sv = P.shp[v];
-      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * su.c;
-      int64_t k = (int64_t)P.cfg.batch * own[v] * sv.w;
-      int s = wgrad_splits(m, nn, k);
-      splits[v] = s;
-      if (s > 1) part = std::max(part, (size_t)s * m * nn * 4);
-      const int taps = d.kh * d.kw;
-      const int nbands = layerwise ? 1 : P.nb;
-      for (int r = 0; r < nbands; ++r) {
-        const Rows q = layerwise ? Rows{0, sv.h, 0, sv.h} : P.rows[r][v];
-        if (q.b <= q.a) continue;
-        long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
-        int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), conv_cap);
-        if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
-        int u0 = std::max(0, q.a * d.sh - d.ph);
-        int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
-        long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
-        int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), conv_cap);
-        if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
-      }
-    }
-  L.part_bytes = part;
-  L.part = A.take(part);
   if (dxacc) {
     L.dxacc_bytes = P.elems(0, P.shp[0].h) * 4;
     L.dxacc = A.take(L.dxacc_bytes);
   }
-  L.total = std::max<size_t>(A.top, 256);
+  const size_t bp_end = A.top;
+  // --- forward windows packed by lifetime: node v's window lives from its
+  // own step to its last consumer's step (topological order); they reuse
+  // the backward region, which FP does not touch
+  size_t fp_end = ubase;
+  if (fpw) {
+    L.fp_packed = true;
+    L.fwin_cap = *fpw;
+    std::vector<LiveBuf> fb;
+    std::vector<int> ids;
+    for (int v = 1; v + 1 < n; ++v) {
+      int last = v;
+      for (int c : P.cons[v]) last = std::max(last, c);
+      fb.push_back(LiveBuf{v, last, P.elems(v, (*fpw)[v]) * P.es, 0});
+      ids.push_back(v);
+    }
+    size_t fpeak = pack(fb);
+    for (size_t t = 0; t < ids.size(); ++t) L.fwin[ids[t]] = ubase + fb[t].off;
+    L.fwin_bytes = fpeak;
+    fp_end = ubase + align256(fpeak);
+  }
+  L.total = std::max<size_t>(std::max(bp_end, fp_end), 256);
 }
 
 static int build(Plan &P) {
@@ -404,27 +439,39 @@ static int build(Plan &P) {
     if (P.cons[v].empty())
       return lrcnn_fail(LRCNN_ESHAPE, "node " + std::to_string(v) +
                                           " feeds nothing (only the last node is an output)");
-  // bounds
+  // bounds of the forward partition, refined evenly for the backward one
   const bool carry = P.cfg.mode == LRCNN_CARRY;
   const int H = carry ? P.shp[0].h : P.shp[n - 1].h;
-  const int nb = P.cfg.n_bands;
-  P.nb = nb;
-  std::vector<int> bd(nb + 1);
+  const int nbf = P.cfg.n_bands;
+  const int refine = P.cfg.bp_refine > 1 ? P.cfg.bp_refine : 1;
+  std::vector<int> bd(nbf + 1);
   if (P.cfg.policy == LRCNN_EXPLICIT) {
-    for (int r = 0; r <= nb; ++r) bd[r] = P.cfg.bounds[r];
-    if (bd[0] != 0 || bd[nb] != H)
+    for (int r = 0; r <= nbf; ++r) bd[r] = P.cfg.bounds[r];
+    if (bd[0] != 0 || bd[nbf] != H)
       return lrcnn_fail(LRCNN_EPARTITION, "bounds must run from 0 to " + std::to_string(H));
-    for (int r = 0; r < nb; ++r)
+    for (int r = 0; r < nbf; ++r)
       if (bd[r + 1] < bd[r]) return lrcnn_fail(LRCNN_EPARTITION, "bounds must be non-decreasing");
   } else if (P.cfg.policy == LRCNN_BALANCED) {
-    bd = balanced_bounds(P, H, nb);
+    bd = balanced_bounds(P, H, nbf);
   } else {
-    for (int r = 0; r <= nb; ++r) bd[r] = (int)((int64_t)r * H / nb);
+    for (int r = 0; r <= nbf; ++r) bd[r] = (int)((int64_t)r * H / nbf);
   }
-  P.bounds = bd;
+  std::vector<int> bb;
+  for (int r = 0; r < nbf; ++r)
+    for (int j = 0; j < refine; ++j)
+      bb.push_back(bd[r] + (int)((int64_t)(bd[r + 1] - bd[r]) * j / refine));
+  bb.push_back(H);
+  P.nb_fp = nbf;
+  P.refine = refine;
+  P.nb = nbf * refine;
+  P.bounds_fp = bd;
+  P.bounds = bb;
   if (carry) carry_rows(P, bd); else cone_rows(P, bd);
+  P.rows_fp = P.rows;
+  if (carry) carry_rows(P, bb); else cone_rows(P, bb);
+  const int nb = P.nb;
   // capacities
-  std::vector<int> cap(n, 0), own(n, 0), cry(n, 0);
+  std::vector<int> cap(n, 0), own(n, 0), cry(n, 0), fcap(n, 0);
   for (int r = 0; r < nb; ++r)
     for (int v = 0; v < n; ++v) {
       const Rows &q = P.rows[r][v];
@@ -432,22 +479,32 @@ static int build(Plan &P) {
       own[v] = std::max(own[v], q.b - q.a);
       if (carry) cry[v] = std::max(cry[v], q.b - P.tail[r][v]);
     }
-  layout(P, P.rc, cap, own, cry, carry, false,
-         !carry && P.cfg.dtype == LRCNN_BF16);
+  for (int r = 0; r < nbf; ++r)
+    for (int v = 0; v < n; ++v) {
+      const Rows &q = P.rows_fp[r][v];
+      fcap[v] = std::max(fcap[v], q.hi - q.lo);
+    }
+  std::vector<const std::vector<std::vector<Rows>> *> tabs = {&P.rows, &P.rows_fp};
+  layout(P, P.rc, cap, own, cry, tabs, carry, false, !carry && P.cfg.dtype == LRCNN_BF16,
+         refine > 1 ? &fcap : nullptr);
   std::vector<int> full(n), zero(n, 0);
   for (int v = 0; v < n; ++v) full[v] = P.shp[v].h;
-  layout(P, P.lw, full, full, zero, false, true, false);
-  // FLOPs: tau of Section IV-B, and the row-centric total
+  layout(P, P.lw, full, full, zero, {}, false, true, false, nullptr);
+  // FLOPs: tau of Section IV-B and the row-centric total (FP over the
+  // forward bands; BP recompute, input and weight gradient over the backward
+  // bands; without recomputing the last band when FP left it in place)
   P.tau = 0;
-  double cone = 0;
+  double fp = 0, bp = 0, last = 0;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
       double per_row = 2.0 * d.kh * d.kw * P.cfg.batch * P.shp[d.in0].c * d.c_out * P.shp[v].w;
       P.tau += per_row * P.shp[v].h;
-      for (int r = 0; r < nb; ++r) cone += per_row * (P.rows[r][v].b - P.rows[r][v].a);
+      for (int r = 0; r < nbf; ++r) fp += per_row * (P.rows_fp[r][v].b - P.rows_fp[r][v].a);
+      for (int r = 0; r < nb; ++r) bp += per_row * (P.rows[r][v].b - P.rows[r][v].a);
+      last += per_row * (P.rows[nb - 1][v].b - P.rows[nb - 1][v].a);
     }
-  P.flops_rows = 4.0 * cone;  // FP, BP recompute, input gradient, weight gradient
+  P.flops_rows = fp + 3.0 * bp - (refine == 1 ? last : 0.0);
   P.shared_rows = 0;
   P.halo_rows = 0;
   for (int r = 0; r < nb; ++r)
@@ -496,7 +553,9 @@ extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info)
   const Plan &P = *reinterpret_cast<const Plan *>(plan);
   std::memset(info, 0, sizeof(*info));
   info->n_nodes = P.n;
-  info->n_bands = P.nb;
+  info->n_bands = P.nb_fp;
+  info->bp_bands = P.nb;
+  info->fp_window_bytes = P.rc.fp_packed ? P.rc.fwin_bytes : P.rc.cache_bytes;
   info->mode = P.cfg.mode;
   info->dtype = P.cfg.dtype;
   info->out_h = P.shp[P.n - 1].h;
@@ -513,7 +572,8 @@ extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info)
   for (int v = 1; v < P.n; ++v) omega += (double)P.elems(v, P.shp[v].h) * P.es;
   double ybytes = (double)P.elems(P.n - 1, P.shp[P.n - 1].h) * P.es;
   info->omega_bytes = omega;
-  info->omega_fp_bytes = (double)P.rc.strip_bytes + P.rc.cache_bytes + ybytes;
+  info->omega_fp_bytes = (double)P.rc.strip_bytes + P.rc.part_bytes +
+                         (P.rc.fp_packed ? P.rc.fwin_bytes : P.rc.cache_bytes) + ybytes;
   info->omega_bp_bytes = (double)P.rc.total + ybytes;
   info->flops_tau = P.tau;
   info->flops_rows = P.flops_rows;
@@ -534,13 +594,14 @@ extern "C" int lrcnn_plan_node_shape(const lrcnn_plan_t *plan, int32_t node,
   return LRCNN_OK;
 }
 
-extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t band,
+extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int32_t band,
                                     int32_t node, int32_t rows[4]) {
   if (!plan || !rows) return lrcnn_fail(LRCNN_EINVAL, "null argument");
   const Plan &P = *reinterpret_cast<const Plan *>(plan);
-  if (node < 0 || node >= P.n || band < 0 || band >= P.nb)
-    return lrcnn_fail(LRCNN_EINVAL, "band or node out of range");
-  const lrcnn::Rows &q = P.rows[band][node];
+  const int nbands = phase == 0 ? P.nb_fp : P.nb;
+  if (node < 0 || node >= P.n || band < 0 || band >= nbands || (phase != 0 && phase != 1))
+    return lrcnn_fail(LRCNN_EINVAL, "phase, band or node out of range");
+  const lrcnn::Rows &q = phase == 0 ? P.rows_fp[band][node] : P.rows[band][node];
   rows[0] = q.a;
   rows[1] = q.b;
   rows[2] = q.lo;

@@ -36,17 +36,27 @@ struct Layout {
   size_t part = 0, part_bytes = 0;  // weight-gradient partial sums
   size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
   size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;
+  // forward windows packed by lifetime (when the forward partition is
+  // coarser than the backward one); they share memory with the buffers that
+  // only the backward pass uses
+  bool fp_packed = false;
+  std::vector<size_t> fwin;
+  std::vector<int> fwin_cap;
+  size_t fwin_bytes = 0;
 };
 
 struct Plan {
   std::vector<lrcnn_node> nodes;
   lrcnn_config cfg{};
-  int n = 0, nb = 0, es = 4;  // node count, band count, element size
+  int n = 0, nb = 0, es = 4;  // node count, backward band count, element size
+  int nb_fp = 0, refine = 1;  // forward band count, backward bands per forward band
   std::vector<Shape> shp;
   std::vector<std::vector<int>> cons;  // consumers of every node
-  std::vector<int> bounds;             // band bounds (input rows or output rows)
-  std::vector<std::vector<Rows>> rows; // [band][node]
-  std::vector<std::vector<int>> tail;  // CARRY: [band][node] first kept row
+  std::vector<int> bounds;             // backward band bounds (input or output rows)
+  std::vector<int> bounds_fp;          // forward band bounds
+  std::vector<std::vector<Rows>> rows; // [backward band][node]
+  std::vector<std::vector<Rows>> rows_fp;  // [forward band][node]
+  std::vector<std::vector<int>> tail;  // CARRY: [backward band][node] first kept row
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   std::vector<int> wsplit;             // per conv node: wgrad K splits (row-centric)

@@ -38,7 +38,7 @@ class Config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("in_c", C.c_int32), ("in_h", C.c_int32),
                 ("in_w", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
                 ("n_bands", C.c_int32), ("policy", C.c_int32),
-                ("bounds", C.POINTER(C.c_int32))]
+                ("bounds", C.POINTER(C.c_int32)), ("bp_refine", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
@@ -52,7 +52,8 @@ class PlanInfo(C.Structure):
                 ("omega_bytes", C.c_double), ("omega_fp_bytes", C.c_double),
                 ("omega_bp_bytes", C.c_double), ("flops_tau", C.c_double),
                 ("flops_rows", C.c_double), ("flops_layerwise", C.c_double),
-                ("shared_rows", C.c_int64), ("halo_rows", C.c_int64)]
+                ("shared_rows", C.c_int64), ("halo_rows", C.c_int64),
+                ("bp_bands", C.c_int32), ("fp_window_bytes", C.c_size_t)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
@@ -69,7 +70,7 @@ def _load():
     lib.lrcnn_plan.argtypes = [C.POINTER(Node), i32, C.POINTER(Config), C.POINTER(vp)]
     lib.lrcnn_plan_query.argtypes = [vp, C.POINTER(PlanInfo)]
     lib.lrcnn_plan_node_shape.argtypes = [vp, i32, C.POINTER(i32)]
-    lib.lrcnn_plan_band_rows.argtypes = [vp, i32, i32, C.POINTER(i32)]
+    lib.lrcnn_plan_band_rows.argtypes = [vp, i32, i32, i32, C.POINTER(i32)]
     lib.lrcnn_plan_destroy.argtypes = [vp]
     lib.lrcnn_plan_destroy.restype = None
     lib.lrcnn_forward_rows.argtypes = [vp, vp, pp, pp, pp, vp, vp, sz, pp, vp]
@@ -131,16 +132,18 @@ class Plan:
         _check(LIB.lrcnn_plan_node_shape(self.handle, v, out))
         return tuple(out)
 
-    def band_rows(self, band, v):
+    def band_rows(self, band, v, phase=1):
+        """Rows (a, b, lo, hi) of node v in a backward (phase 1) or forward
+        (phase 0) band."""
         out = (C.c_int32 * 4)()
-        _check(LIB.lrcnn_plan_band_rows(self.handle, band, v, out))
+        _check(LIB.lrcnn_plan_band_rows(self.handle, phase, band, v, out))
         return tuple(out)
 
 
 def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
-               policy=EVEN, bounds=None):
+               policy=EVEN, bounds=None, bp_refine=1):
     arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
-    cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None)
+    cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None, bp_refine)
     keep = None
     if bounds is not None:
         keep = (C.c_int32 * len(bounds))(*bounds)

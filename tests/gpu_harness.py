@@ -27,9 +27,9 @@ def rel(a, b):
 
 
 def gpu_run(nodes, inp, mode=L.CARRY, nb=1, policy=L.EVEN, bounds=None,
-            layerwise=False, want_dx=True, masks=True, repeat_bwd=1):
+            layerwise=False, want_dx=True, masks=True, repeat_bwd=1, bp_refine=1):
     b, h, w, c = inp.x.shape
-    plan = L.lrcnn_plan(nodes, b, c, h, w, inp.dtype, mode, nb, policy, bounds)
+    plan = L.lrcnn_plan(nodes, b, c, h, w, inp.dtype, mode, nb, policy, bounds, bp_refine)
     info = plan.info()
     dm = DeviceModel.from_inputs(nodes, inp)
     out_shape = (b,) + plan.node_shape(len(nodes) - 1)

@@ -110,7 +110,13 @@ def test_tau_and_omega(cid):
     info = p.info()
     tau = OC.flops_forward(nodes, c["batch"], c["h"], c["w"], 3)
     assert info["flops_tau"] == tau
-    assert info["flops_rows"] == 4 * tau          # 2PS: 4 tau (Section IV-B)
+    # 2PS costs 4 tau (Section IV-B); the last band's BP recompute is
+    # skipped because FP leaves its maps in place
+    shp = OC.shapes(nodes, c["h"], c["w"], 3)
+    F, _ = OR.carry_intervals(nodes, shp, OR.even_bounds(c["h"], c["bands"]))
+    last = sum(2 * nd[4] * nd[5] * c["batch"] * shp[nd[1]][2] * nd[3] * shp[v][1] *
+               (F[-1][v] - F[-2][v]) for v, nd in enumerate(nodes) if nd[0] == 1)
+    assert info["flops_rows"] == 4 * tau - last
     assert info["flops_layerwise"] == 3 * tau
     es = 2 if c["dtype"] == L.BF16 else 4
     shp = OC.shapes(nodes, c["h"], c["w"], 3)
@@ -129,8 +135,10 @@ def test_recompute_flops_include_overlap():
     p1 = L.lrcnn_plan(nodes, 1, 3, 224, 224, L.F32, L.RECOMPUTE, 1)
     p4 = L.lrcnn_plan(nodes, 1, 3, 224, 224, L.F32, L.RECOMPUTE, 4)
     i1, i4 = p1.info(), p4.info()
-    assert i1["flops_rows"] == 4 * i1["flops_tau"] and i1["halo_rows"] == 0
-    assert i4["flops_rows"] > 4 * i4["flops_tau"] and i4["halo_rows"] > 0  # 4(tau+iota)
+    # one band: FP + input and weight gradients, its maps kept for BP
+    assert i1["flops_rows"] == 3 * i1["flops_tau"] and i1["halo_rows"] == 0
+    # four bands: 4(tau + iota) less the kept last band's recompute
+    assert i4["flops_rows"] > 3.5 * i4["flops_tau"] and i4["halo_rows"] > 0
 
 
 def test_shared_rows_eq12_term():
@@ -243,8 +251,8 @@ class _Fake:
 
 
 def dry_run(nodes, batch, h, w, dtype, mode, nb, policy=L.EVEN, bounds=None,
-            dx=True):
-    p = L.lrcnn_plan(nodes, batch, 3, h, w, dtype, mode, nb, policy, bounds)
+            dx=True, bp_refine=1):
+    p = L.lrcnn_plan(nodes, batch, 3, h, w, dtype, mode, nb, policy, bounds, bp_refine)
     f = _Fake(1 << 30)
     per = [None] + [f if nd[0] == L.OP_CONV else None for nd in nodes[1:]]
     aff = [None] + [f if (nd[0] == L.OP_CONV and nd[10]) else None for nd in nodes[1:]]
@@ -262,12 +270,13 @@ def dry_run(nodes, batch, h, w, dtype, mode, nb, policy=L.EVEN, bounds=None,
 
 @pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 @pytest.mark.parametrize("mode", ["carry", "balanced", "recompute"])
-def test_executor_dry_run_configs(cid, mode):
+@pytest.mark.parametrize("refine", [1, 2, 3])
+def test_executor_dry_run_configs(cid, mode, refine):
     c = CONFIGS[cid]
     m = L.RECOMPUTE if mode == "recompute" else L.CARRY
     pol = L.BALANCED if mode == "balanced" else L.EVEN
     dry_run(net_nodes(c["net"]), c["batch"], c["h"], c["w"], c["dtype"], m,
-            c["bands"], pol)
+            c["bands"], pol, bp_refine=refine)
 
 
 @pytest.mark.parametrize("name", list(NETS))
@@ -279,5 +288,44 @@ def test_executor_dry_run_random_partitions(name, seed):
     nb = int(rng.integers(1, 9))
     cuts = sorted(rng.integers(0, h + 1, nb - 1).tolist())
     dry_run(nodes, 2, h, w, L.F32, L.CARRY, nb, L.EXPLICIT, [0] + cuts + [h],
-            dx=bool(seed % 2))
-    dry_run(nodes, 2, h, w, L.BF16, L.RECOMPUTE, nb, dx=bool(seed % 2))
+            dx=bool(seed % 2), bp_refine=1 + seed % 3)
+    dry_run(nodes, 2, h, w, L.BF16, L.RECOMPUTE, nb, dx=bool(seed % 2),
+            bp_refine=1 + (seed + 1) % 3)
+
+
+@pytest.mark.parametrize("refine", [2, 3])
+def test_backward_partition_refines_forward(refine):
+    # Section III-C: BP may use a finer partition than FP. Each forward band
+    # is split evenly; frontiers of both partitions agree at shared
+    # boundaries, and the plan's rows match the oracle's intervals for each.
+    nodes = NETS["dag"]
+    h, w = 61, 9
+    bounds = [0, 7, 30, 61]
+    p = L.lrcnn_plan(nodes, 1, 3, h, w, L.F32, L.CARRY, 3, L.EXPLICIT, bounds, refine)
+    inf = p.info()
+    assert inf["n_bands"] == 3 and inf["bp_bands"] == 3 * refine
+    shp = OC.shapes(nodes, h, w, 3)
+    bb = []
+    for r in range(3):
+        for j in range(refine):
+            bb.append(bounds[r] + (bounds[r + 1] - bounds[r]) * j // refine)
+    bb.append(h)
+    Ff, Tf = OR.carry_intervals(nodes, shp, bounds)
+    Fb, Tb = OR.carry_intervals(nodes, shp, bb)
+    for v in range(len(nodes)):
+        for r in range(3):
+            assert p.band_rows(r, v, phase=0) == (Ff[r][v], Ff[r + 1][v], Tf[r][v], Ff[r + 1][v])
+        for q in range(3 * refine):
+            assert p.band_rows(q, v, phase=1) == (Fb[q][v], Fb[q + 1][v], Tb[q][v], Fb[q + 1][v])
+        for r in range(1, 3):
+            assert Fb[r * refine][v] == Ff[r][v] and Tb[r * refine][v] == Tf[r][v]
+
+
+def test_finer_backward_bands_cut_memory_on_vgg():
+    c = CONFIGS[2]
+    nodes = net_nodes("vgg16")
+    one = L.lrcnn_plan(nodes, 8, 3, 224, 224, L.F32, L.CARRY, 4).info()
+    two = L.lrcnn_plan(nodes, 8, 3, 224, 224, L.F32, L.CARRY, 4, bp_refine=2).info()
+    assert two["workspace_bytes"] < one["workspace_bytes"]
+    assert two["band_cache_bytes"] < one["band_cache_bytes"]
+    assert two["layerwise_workspace_bytes"] > 3 * two["workspace_bytes"]

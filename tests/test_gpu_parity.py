@@ -107,6 +107,16 @@ def test_recompute_parity(name, dtype):
 
 
 @pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", ["vgg_like", "odd", "resnet_like"])
+@pytest.mark.parametrize("mode", [L.CARRY, L.RECOMPUTE])
+def test_finer_backward_partition_parity(name, dtype, mode):
+    # Section III-C: BP bands refine the FP bands (N_BP = 3 N_FP here)
+    nodes, inp = _inputs(name, dtype, seed=15)
+    gpu = gpu_run(nodes, inp, mode, 3, bp_refine=3)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
 @pytest.mark.parametrize("name", list(NETS))
 def test_layerwise_parity(name, dtype):
     nodes, inp = _inputs(name, dtype, seed=7)
