@@ -269,7 +269,7 @@ struct Run {
       g.dc = dc;
       g.src = act[u];
       g.out = (float *)(ws + L.part);
-      g.splits = (sched == S_LAYERWISE ? P.wsplit_lw : P.wsplit)[v];
+      g.part_bytes = L.part_bytes;
       g.B = B;
       g.y0 = a;
       g.y1 = b;

@@ -618,7 +618,7 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0);
   const int bn = a.N <= 64 ? 64 : 128;
   const int KT = a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
-  const int splits = conv_split_count(M, a.N, KT, a.part ? a.part_bytes : 0);
+  const int splits = conv_split_count(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
   a.kts = (KT + splits - 1) / splits;
   dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
   int pr = -1;
@@ -850,9 +850,9 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   const int N = a.kh * a.kw * a.Ci;
   if (K <= 0) return 0;
   constexpr int BK = Cfg<T>::BK;
-  int splits = a.splits < 1 ? 1 : a.splits;
-  int kchunk = (K + splits - 1) / splits;
-  kchunk = (kchunk + BK - 1) / BK * BK;
+  int splits = wgrad_split_count(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
+  const int KT = (K + BK - 1) / BK;
+  const int kchunk = (KT + splits - 1) / splits * BK;
   splits = (K + kchunk - 1) / kchunk;
   const bool vec = (a.Co % Cfg<T>::E) == 0 && (a.Ci % Cfg<T>::E) == 0;
   dim3 grid((a.Co + BM - 1) / BM, (N + 127) / 128, splits);

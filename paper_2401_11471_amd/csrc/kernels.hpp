@@ -39,37 +39,59 @@ struct ConvArgs {
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 
-// Number of K splits of a conv launch with M x N outputs and KT K-iterations:
-// enough workgroups for two per CU when the output tiles alone are too few,
-// at least 8 K-iterations per split, and partial sums that fit in `cap`
-// bytes. Shared by the launcher and the planner's workspace sizing.
-inline int conv_split_count(long long M, int N, int KT, size_t cap) {
-  const long long bn = N <= 64 ? 64 : 128;
-  const long long tiles = ((M + 127) / 128) * ((N + bn - 1) / bn);
-  const long long cus = 256;
-  if (tiles >= 2 * cus || KT < 16) return 1;
-  const long long per = M * (long long)N * 4;
-  // score: balance over the CUs (every CU gets the same number of
-  // workgroups), enough workgroups for two per CU, a small charge per
-  // split for the partial sums
-  auto score = [&](long long s) {
+// Split-K selection. A launch of `tiles` output tiles whose K loop has KT
+// iterations runs split s ways as tiles*s workgroups of ceil(KT/s)
+// iterations each, plus a pass that adds the s partial sums in a fixed
+// order. The estimated duration of each choice is
+//   K loop:   iterations * (workgroups on the busiest of the 256 CUs)
+//             * time of one iteration, which falls when two workgroups
+//             share a CU (latency hiding) and does not improve beyond
+//             that;
+//   fixed:    prologue, pipeline fill and epilogue of a workgroup;
+//   splits:   the extra launch and the partial sums written and read back
+//             (they stay in the last-level cache at these sizes).
+// The constants are measured on gfx950 for the 128-row tiles of the
+// kernels in kernels.hip. The count is the cheapest estimate whose partial
+// sums fit in `cap` bytes; it is shared by the launchers and the planner's
+// workspace sizing, so both always agree.
+struct SplitCost {
+  double step_us;   // one K iteration of a lone workgroup
+  int occ;          // workgroups one CU holds (LDS bound)
+  double fixed_us;  // per-launch fixed cost
+};
+inline int split_count(long long tiles, int KT, long long part_elems, size_t cap,
+                       const SplitCost &c) {
+  if (tiles <= 0 || KT <= 1) return 1;
+  auto cost = [&](long long s) {
     const long long wg = tiles * s;
-    const double bal = (double)wg / (double)(cus * ((wg + cus - 1) / cus));
-    const double fill = wg >= 2 * cus ? 1.0 : (double)wg / (2.0 * cus);
-    return bal * fill - 0.01 * (double)(s - 1);
+    const long long per_cu = (wg + 255) / 256;
+    const long long kts = (KT + s - 1) / s;
+    const double share = per_cu >= 2 && c.occ >= 2 ? 0.8 : 1.0;
+    double t = (double)kts * (double)per_cu * c.step_us * share + c.fixed_us;
+    if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
+    return t;
   };
   long long best = 1;
-  double bs = score(1);
-  for (long long s = 2; s <= KT / 8 && s <= 64; ++s) {
-    if (per > 0 && s * per > (long long)cap) break;
-    const double sc = score(s);
-    if (sc > bs + 1e-9) {
-      bs = sc;
+  double bt = cost(1);
+  for (long long s = 2; s <= 128 && s <= KT / 2; ++s) {
+    if ((size_t)s * (size_t)part_elems * 4 > cap) break;
+    const long long kts = (KT + s - 1) / s;
+    if ((KT + kts - 1) / kts != s) continue;  // same work as a smaller s
+    const double t = cost(s);
+    if (t < bt * 0.98) {
+      bt = t;
       best = s;
     }
   }
-  const long long kts = (KT + best - 1) / best;
-  return (int)((KT + kts - 1) / kts);
+  return (int)best;
+}
+// conv forward / input gradient: M x N outputs, KT K iterations
+inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
+  const bool wide = N > 64;
+  const long long tiles = ((M + 127) / 128) * ((N + (wide ? 127 : 63)) / (wide ? 128 : 64));
+  SplitCost c{wide ? 1.35 : 0.75, wide ? 2 : 3, 5.0};
+  if (es == 2) c.step_us *= 0.75;
+  return split_count(tiles, KT, M * (long long)N, cap, c);
 }
 // K iterations of a conv for storage element size es (bytes); one
 // iteration covers LRCNN_CONV_KR 16-byte vectors of a tile row.
@@ -84,12 +106,20 @@ inline int conv_k_iters(int taps, int kc, int es) {
 struct WgradArgs {
   const void *dc;  // error operand, own rows [B][R][Wv][Co], contiguous
   View src;        // producer window
-  float *out;      // dW [Co][kh*kw*Ci] (split == 1) or partial sums
-  int splits;
+  float *out;         // partial sums of a split launch
+  size_t part_bytes;  // capacity of `out`
   int B, y0, y1, Wv, Co, Ci, Hs, Ws;
   int kh, kw, sh, sw, ph, pw;
 };
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
+// K iterations of a weight-gradient launch over K pixels
+inline int wgrad_k_iters(long long K, int es) { return (int)((K + 64 / es - 1) / (64 / es)); }
+// weight gradient: Co x N outputs (N = taps * C_in) over K pixels
+inline int wgrad_split_count(int Co, long long N, long long K, size_t cap, int es) {
+  const long long tiles = ((Co + 127) / 128) * ((N + 127) / 128);
+  SplitCost c{es == 2 ? 1.1 : 1.5, 3, 12.0};
+  return split_count(tiles, wgrad_k_iters(K, es), (long long)Co * N, cap, c);
+}
 
 struct PoolArgs {
   View src, dst;

@@ -45,16 +45,6 @@ static void ksp(const lrcnn_node &nd, int &k, int &s, int &p) {
   }
 }
 
-int wgrad_splits(int64_t m, int64_t n, int64_t k) {
-  const int64_t bm = 128, bn = 128, min_k = 256, target = 512;
-  const int64_t cap = (int64_t)24 << 20;  // bytes of partial sums
-  int64_t tiles = ((m + bm - 1) / bm) * ((n + bn - 1) / bn);
-  int64_t s = (target + tiles - 1) / tiles;
-  s = std::min<int64_t>(s, std::max<int64_t>(1, k / min_k));
-  s = std::min<int64_t>(s, std::max<int64_t>(1, cap / (m * n * 4)));
-  return (int)std::max<int64_t>(1, std::min<int64_t>(s, 512));
-}
-
 // Rows of node v's output that can be computed once rows [0, f) of its
 // input exist: output row y reads input rows [y*s-p, y*s-p+k) (clipped to
 // the image, whose top and bottom are padded; Section III-B).
@@ -313,35 +303,32 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
       }
     L.strip_bytes = A.top - s0;
   }
-  // partial sums (used by FP and BP): weight-gradient splits, and split-K
-  // of the convolution forward / input gradient on launches with few tiles
+  // partial sums (used by FP and BP): split-K of the weight gradient and of
+  // the convolution forward / input gradient, for every launch the
+  // schedule makes, with the launchers' own split rule
   size_t part = 0;
-  std::vector<int> &splits = layerwise ? P.wsplit_lw : P.wsplit;
-  splits.assign(n, 1);
-  const size_t conv_cap = (size_t)24 << 20;
+  const size_t pcap = (size_t)24 << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
       const Shape &su = P.shp[d.in0], &sv = P.shp[v];
-      int64_t m = d.c_out, nn = (int64_t)d.kh * d.kw * su.c;
-      int64_t k = (int64_t)P.cfg.batch * own[v] * sv.w;
-      int s = wgrad_splits(m, nn, k);
-      splits[v] = s;
-      if (s > 1) part = std::max(part, (size_t)s * m * nn * 4);
       const int taps = d.kh * d.kw;
+      const int64_t nw = (int64_t)taps * su.c;
       std::vector<Rows> qs;
       if (layerwise) qs.push_back(Rows{0, sv.h, 0, sv.h});
       for (auto *tab : bands)
         for (auto &br : *tab) qs.push_back(br[v]);
       for (const Rows &q : qs) {
         if (q.b <= q.a) continue;
-        long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
-        int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), conv_cap);
+        const long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
+        const int sw_ = wgrad_split_count(d.c_out, nw, mf, pcap, P.es);
+        if (sw_ > 1) part = std::max(part, (size_t)sw_ * d.c_out * nw * 4);
+        const int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), pcap, P.es);
         if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
-        int u0 = std::max(0, q.a * d.sh - d.ph);
-        int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
-        long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
-        int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), conv_cap);
+        const int u0 = std::max(0, q.a * d.sh - d.ph);
+        const int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
+        const long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
+        const int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), pcap, P.es);
         if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
       }
     }

@@ -59,8 +59,6 @@ struct Plan {
   std::vector<std::vector<int>> tail;  // CARRY: [backward band][node] first kept row
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
-  std::vector<int> wsplit;             // per conv node: wgrad K splits (row-centric)
-  std::vector<int> wsplit_lw;          // per conv node: wgrad K splits (layer-wise)
   double tau = 0, flops_rows = 0;
   int64_t shared_rows = 0, halo_rows = 0;
   // state for the FP -> BP hand-over of CARRY mode
@@ -75,7 +73,6 @@ struct Plan {
 
 // Weight-gradient split count for a conv with the given GEMM sizes: enough
 // workgroups to fill the chip, at least `min_k` reduction steps each.
-int wgrad_splits(int64_t m, int64_t n, int64_t k);
 
 }  // namespace lrcnn
 
