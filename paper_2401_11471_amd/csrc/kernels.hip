@@ -156,6 +156,9 @@ struct Frag<float, BN, KR, AKM, BKM> {
   static constexpr int LDK = Cfg<float, KR>::LDK, NB = BN / 64, NV = KR / 2;
   static constexpr int S = 4 * NV;            // K elements per lane group
   static constexpr int PA = BM + 4, PB = BN + 4;
+  // instructions per tile step: MFMAs and LDS reads of one fragment load
+  static constexpr int NMFMA = S * 2 * NB;
+  static constexpr int NDSR = (AKM ? 2 * S : 2 * NV) + (BKM ? NB * S : NB * NV);
   float a[2][S], b[NB][S];
   __device__ __forceinline__ void load(const float *As, const float *Bs, int wm, int wn,
                                        int lane) {
@@ -203,6 +206,8 @@ struct Frag<float, BN, KR, AKM, BKM> {
 template <int BN, int KR>
 struct Frag<bf16, BN, KR, 0, 0> {
   static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
+  static constexpr int NMFMA = NV * 2 * NB;
+  static constexpr int NDSR = 2 * NV + NB * NV;
   bf16x8 a[2][NV], b[NB][NV];
   __device__ __forceinline__ void load(const bf16 *As, const bf16 *Bs, int wm, int wn,
                                        int lane) {
@@ -256,6 +261,49 @@ __device__ __forceinline__ uint4 load16(const T *p, bool ok, int lim) {
         if (e < lim) r.e[e] = p[e];
     }
     return r.u;
+  }
+}
+
+// Branch-free 16-byte load: an element outside the operand reads a
+// 16-byte block of zeros instead, so the loads of a tile step stay in one
+// basic block and can be scheduled among the MFMAs. The block is a mutable
+// global that nothing writes, so the compiler cannot fold its value and
+// turn the load back into a conditional one.
+__device__ __align__(16) uint4 g_zero16[1] = {};
+__device__ __forceinline__ uint4 load16z(const void *base, long long off_bytes, bool ok) {
+  const uint4 *q = ok ? (const uint4 *)((const char *)base + off_bytes) : &g_zero16[0];
+  return *q;
+}
+
+// Instruction schedule of one steady-state tile step: the MFMAs of the
+// current fragments are interleaved with the LDS reads of the next
+// fragments, the LDS writes of tile t+2 and the global loads (with their
+// address arithmetic) of tile t+3, so the matrix pipe is not left idle
+// while the wave issues memory work.
+template <int NMF, int DSR, int DSW, int VMR>
+__device__ __forceinline__ void interleave_step() {
+  constexpr int Q = NMF / 4 > 0 ? NMF / 4 : 1;
+  constexpr int R1 = (DSR + Q - 1) / Q, W1 = (DSW + Q - 1) / Q, V1 = (VMR + Q - 1) / Q;
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, R1, 0);  // LDS read
+  }
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x200, W1, 0);  // LDS write
+  }
+#pragma unroll
+  for (int i = 0; i < Q; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);   // VALU
+    __builtin_amdgcn_sched_group_barrier(0x020, V1, 0);  // global load
+  }
+#pragma unroll
+  for (int i = 0; i < NMF - 3 * Q; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
   }
 }
 
@@ -325,7 +373,7 @@ static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
        idx += (long long)gridDim.x * blockDim.x)
 
 // ------------------------------------------- conv forward / input grad
-template <typename T, int BN, int KR, bool DGRAD, bool VEC>
+template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1>
 __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   using CF = Cfg<T, KR>;
   constexpr int E = CF::E, BK = CF::BK, LDK = CF::LDK;
@@ -391,6 +439,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
 
   uint4 ra[NA], rb[NBL];
+  // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
     const int cb = cbi * BK;
     const int c0 = cb + kv * E;
@@ -401,43 +450,60 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       int sy, sx;
       bool ok;
       if (DGRAD) {
-        int ty = ay[i] + a.ph - ti, tx = ax[i] + a.pw - tj;
-        ok = ty >= 0 && tx >= 0;
-        sy = ty / a.sh;
-        sx = tx / a.sw;
-        ok = ok && sy * a.sh == ty && sx * a.sw == tx;
+        const int ty = ay[i] + a.ph - ti, tx = ax[i] + a.pw - tj;
+        ok = (ty >= 0) & (tx >= 0);
+        if (S1) {
+          sy = ty, sx = tx;
+        } else {
+          sy = ty / a.sh;
+          sx = tx / a.sw;
+          ok = ok & (sy * a.sh == ty) & (sx * a.sw == tx);
+        }
       } else {
         sy = ay[i] * a.sh - a.ph + ti;
         sx = ax[i] * a.sw - a.pw + tj;
         ok = sx >= 0;
       }
-      ok = ok && am[i] && cok && sy >= a.sy0 && sy < a.sy1 && sx < a.Ws;
-      const T *p = src;
-      if (ok) p = src + abase[i] + sy * srow + (long long)sx * a.src.C + c0;
-      ra[i] = load16<T, VEC>(p, ok, lim);
+      ok = ok & am[i] & cok & (sy >= a.sy0) & (sy < a.sy1) & (sx < a.Ws);
+      const long long off = abase[i] + sy * srow + (long long)sx * a.src.C + c0;
+      if (VEC) {
+        ra[i] = load16z(src, off * (long long)sizeof(T), ok);
+      } else {
+        const T *p = src;
+        if (ok) p = src + off;
+        ra[i] = load16<T, VEC>(p, ok, lim);
+      }
     }
 #pragma unroll
     for (int j = 0; j < NBL; ++j) {
+      bool ok;
+      long long off;
+      int blim;
       if (DGRAD) {
         const int o = cb + bk0 + BKS * j;
-        const bool ok = bvld[j] && o < a.KC;
-        const T *p = ok ? w + ((long long)o * taps + tap) * a.N + bn[j] : w;
-        rb[j] = load16<T, VEC>(p, ok, a.N - bn[j]);
+        ok = bvld[j] & (o < a.KC);
+        off = ((long long)o * taps + tap) * a.N + bn[j];
+        blim = a.N - bn[j];
       } else {
-        const bool ok = bvld[j] && cok;
-        const T *p = ok ? w + ((long long)bn[j] * taps + tap) * a.KC + c0 : w;
-        rb[j] = load16<T, VEC>(p, ok, lim);
+        ok = bvld[j] & cok;
+        off = ((long long)bn[j] * taps + tap) * a.KC + c0;
+        blim = lim;
+      }
+      if (VEC) {
+        rb[j] = load16z(w, off * (long long)sizeof(T), ok);
+      } else {
+        const T *p = ok ? w + off : w;
+        rb[j] = load16<T, VEC>(p, ok, blim);
       }
     }
-    // advance to the next (tap, channel block)
-    if (++cbi == CB) {
-      cbi = 0;
-      ++tap;
-      if (++tj == a.kw) {
-        tj = 0;
-        ++ti;
-      }
-    }
+    // advance to the next (tap, channel block) without branches
+    const bool wrap = ++cbi == CB;
+    cbi = wrap ? 0 : cbi;
+    tap += wrap ? 1 : 0;
+    tj += wrap ? 1 : 0;
+    const bool wrow = tj == a.kw;
+    tj = wrow ? 0 : tj;
+    ti += wrow ? 1 : 0;
   };
 
   f32x16 acc[2][NB];
@@ -497,7 +563,24 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
   };
+  // steady state: every part of the step exists, so the step is one
+  // straight-line block with an explicit instruction interleave
+  constexpr int NDSW = NA + ((DGRAD && !BKM) ? NBL * E : NBL);
+  auto step_full = [&](FR &cur, FR &nxt) {
+    nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    store(s2);
+    gload();
+    cur.mma(acc);
+    interleave_step<FR::NMFMA, FR::NDSR, NDSW, NA + NBL>();
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
   int t = 0;
+  for (; t + 4 < n; t += 2) {
+    step_full(f0, f1);
+    step_full(f1, f0);
+  }
   for (; t + 1 < n; t += 2) {
     step(t, f0, f1);
     step(t + 1, f1, f0);
@@ -633,12 +716,26 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
                      (vec ? ", vec>" : ", scalar>");
     pr = prof::begin(nm, fl, s);
   }
+  // the input gradient of a strided convolution divides by the stride
+  const bool s1 = !DGRAD || (a.sh == 1 && a.sw == 1);
   if (bn == 64) {
-    if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true><<<grid, 256, 0, s>>>(a);
-    else conv_gemm_kernel<T, 64, KR, DGRAD, false><<<grid, 256, 0, s>>>(a);
+    if (!s1) {
+      if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
+      else conv_gemm_kernel<T, 64, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+    } else if (vec) {
+      conv_gemm_kernel<T, 64, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
+    } else {
+      conv_gemm_kernel<T, 64, KR, DGRAD, false, true><<<grid, 256, 0, s>>>(a);
+    }
   } else {
-    if (vec) conv_gemm_kernel<T, 128, KR, DGRAD, true><<<grid, 256, 0, s>>>(a);
-    else conv_gemm_kernel<T, 128, KR, DGRAD, false><<<grid, 256, 0, s>>>(a);
+    if (!s1) {
+      if (vec) conv_gemm_kernel<T, 128, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
+      else conv_gemm_kernel<T, 128, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+    } else if (vec) {
+      conv_gemm_kernel<T, 128, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
+    } else {
+      conv_gemm_kernel<T, 128, KR, DGRAD, false, true><<<grid, 256, 0, s>>>(a);
+    }
   }
   prof::end(pr, s);
   if (splits > 1) {
@@ -657,6 +754,16 @@ int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream) {
   if (dt == DT_F32)
     return dgrad ? conv_dispatch<float, true>(a, s) : conv_dispatch<float, false>(a, s);
   return dgrad ? conv_dispatch<bf16, true>(a, s) : conv_dispatch<bf16, false>(a, s);
+}
+
+// q = p / d, r = p % d for 0 <= p with p / d < 2^22, by a float
+// reciprocal and one correction step (the estimate is off by at most one).
+__device__ __forceinline__ void divmod_rcp(int p, int d, float inv, int &q, int &r) {
+  q = (int)((float)p * inv);
+  r = p - q * d;
+  const bool lo = r < 0, hi = r >= d;
+  q += hi ? 1 : (lo ? -1 : 0);
+  r += hi ? -d : (lo ? d : 0);
 }
 
 // ------------------------------------------------------------ weight grad
@@ -703,6 +810,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
   };
   V16 ra[2], rb[2];
   int k0 = kbeg;
+  const bool ovok = ov < a.Co, nbok = nb0 < N;
+  const float invW = 1.0f / (float)a.Wv, invR = 1.0f / (float)R;
+  // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
@@ -710,27 +820,23 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       const bool pk = p < kend;
       // A: E output channels of pixel p
       if (VEC) {
-        ra[i].u = (pk && ov < a.Co) ? *(const uint4 *)(dc + (long long)p * a.Co + ov)
-                                    : make_uint4(0, 0, 0, 0);
+        ra[i].u = load16z(dc, ((long long)p * a.Co + ov) * (long long)sizeof(T), pk & ovok);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e)
           ra[i].e[e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
       }
       // B: E input values of pixel p under the column's tap
-      int x = 0, y = 0, b = 0;
-      if (pk) {
-        x = p % a.Wv;
-        int t = p / a.Wv;
-        y = a.y0 + t % R;
-        b = t / R;
-      }
+      int t, x, yy, b;
+      divmod_rcp(pk ? p : 0, a.Wv, invW, t, x);
+      divmod_rcp(t, R, invR, b, yy);
+      const int y = a.y0 + yy;
       if (VEC) {
-        int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
-        bool ok = pk && nb0 < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
-        rb[i].u = ok ? *(const uint4 *)(src + b * a.src.bs + (sy - a.src.row0) * srow +
-                                        (long long)sx * a.src.C + cv)
-                     : make_uint4(0, 0, 0, 0);
+        const int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
+        const bool ok = pk & nbok & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+        const long long off =
+            b * a.src.bs + (sy - a.src.row0) * srow + (long long)sx * a.src.C + cv;
+        rb[i].u = load16z(src, off * (long long)sizeof(T), ok);
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e) {
@@ -799,7 +905,24 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
   };
+  constexpr int NDSW = KM ? 4 : 2 * 2 * E;
+  auto step_full = [&](FR &cur, FR &nxt) {
+    nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    store(s2);
+    gload();
+    cur.mma(acc);
+    interleave_step<FR::NMFMA, FR::NDSR, NDSW, 4>();
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
   int t = 0;
+  if (VEC) {
+    for (; t + 4 < n; t += 2) {
+      step_full(f0, f1);
+      step_full(f1, f0);
+    }
+  }
   for (; t + 1 < n; t += 2) {
     step(t, f0, f1);
     step(t + 1, f1, f0);
@@ -849,6 +972,9 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   const int K = a.B * (a.y1 - a.y0) * a.Wv;
   const int N = a.kh * a.kw * a.Ci;
   if (K <= 0) return 0;
+  // the kernel splits pixel indices with float reciprocals (exact below 2^22
+  // quotients)
+  if ((long long)a.B * (a.y1 - a.y0) >= (1LL << 22)) return (int)hipErrorInvalidValue;
   constexpr int BK = Cfg<T>::BK;
   int splits = wgrad_split_count(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
   const int KT = (K + BK - 1) / BK;
