@@ -44,6 +44,9 @@ def parse():
                     help="skip the layer-wise / recompute comparison runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (a "
+                         "known-size reference for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -131,6 +134,14 @@ def main():
         L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, b["ws"])
 
     peak_rc, bufs = measure(rc_alloc, rc_step)
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib << 18  # float32 elements
+        csrc = torch.ones(n, device="cuda")
+        cdst = torch.empty_like(csrc)
+        torch.cuda.synchronize()
+        cdst.copy_(csrc)
+        torch.cuda.synchronize()
+        del csrc, cdst
 
     # --- timed region
     for _ in range(args.warmup):
@@ -225,6 +236,36 @@ def main():
         except (RuntimeError, L.LrcnnError) as ex:
             out["layerwise"] = {"error": str(ex)[:200]}
         torch.cuda.empty_cache()
+        if mode == L.CARRY and args.bp_refine == 1:
+            # the same forward bands with each backward band split in two
+            # (Section III-C): smaller backward windows, more launches
+            fplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy, bp_refine=2)
+            finfo = fplan.info()
+
+            def f_alloc():
+                return dict(ws=dm.workspace(finfo["workspace_bytes"]), y=dm.empty(out_shape))
+
+            def f_step(b):
+                L.lrcnn_forward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, b["y"], b["ws"])
+                L.lrcnn_backward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, b["ws"])
+            peak_f, fb = measure(f_alloc, f_step)
+            for _ in range(args.warmup):
+                f_step(fb)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(args.steps):
+                f_step(fb)
+            e1.record()
+            torch.cuda.synchronize()
+            f_ms = e0.elapsed_time(e1) / args.steps
+            ent = {"bp_bands": finfo["bp_bands"], "images_per_s": round(B * 1000.0 / f_ms, 3),
+                   "ms_per_step": round(f_ms, 3), "peak_act_bytes": int(peak_f)}
+            if "peak_act_bytes" in out.get("layerwise", {}):
+                ent["mem_ratio_layerwise_over_rows"] = round(
+                    out["layerwise"]["peak_act_bytes"] / peak_f, 3)
+            out["finer_backward_bands"] = ent
+            del fb
+            torch.cuda.empty_cache()
         if mode == L.CARRY:
             rplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.RECOMPUTE, nb,
                                  bp_refine=args.bp_refine)

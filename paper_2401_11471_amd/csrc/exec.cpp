@@ -28,6 +28,35 @@ thread_local bool g_dry = false;
                                         hipGetErrorString((hipError_t)e_)); \
   } while (0)
 
+// The weight gradient of a convolution does not depend on the input
+// gradient of the same layer, and a band's launches of either are often too
+// small to fill the GPU, so the backward runs the weight gradients on a side
+// stream beside the caller's stream. Events order them: the side stream
+// waits until the error operand is formed; the caller's stream waits for the
+// last weight gradient before the error-operand buffer is formed again and
+// at the end of every band (the next band's recompute overwrites the
+// windows the weight gradient reads).
+bool ensure_side(Plan &P) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (P.side_stream && P.side_dev == dev) return true;
+  release_side(P);
+  hipStream_t s = nullptr;
+  hipEvent_t a = nullptr, b = nullptr;
+  if (hipStreamCreateWithFlags(&s, hipStreamNonBlocking) != hipSuccess) return false;
+  if (hipEventCreateWithFlags(&a, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&b, hipEventDisableTiming) != hipSuccess) {
+    if (a) (void)hipEventDestroy(a);
+    (void)hipStreamDestroy(s);
+    return false;
+  }
+  P.side_stream = s;
+  P.ev_act = a;
+  P.ev_wg = b;
+  P.side_dev = dev;
+  return true;
+}
+
 struct Run {
   Plan &P;
   const Layout &L;
@@ -42,6 +71,8 @@ struct Run {
   std::vector<View> act;   // current feature-map view of every node
   std::vector<View> dlt;   // current float32 error view of every node
   std::vector<int> first_consumer;
+  hipStream_t side = nullptr;  // weight-gradient stream (backward only)
+  bool wg_pending = false;     // a weight gradient on `side` not yet joined
 
   Run(Plan &p, const Layout &l, Sched s, void *wsp, const void *x_,
       const void *const *w_, const float *const *sc_, const float *const *sf_,
@@ -261,15 +292,15 @@ struct Run {
                                             " not held by its buffers");
     }
     if (d.op == LRCNN_OP_CONV) {
-      void *dc = ws + L.dc;
+      void *dc = ws + L.dc[v];
       LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a, b,
                             sv.w, sv.c, stream),
              "error operand");
       WgradArgs g{};
       g.dc = dc;
       g.src = act[u];
-      g.out = (float *)(ws + L.part);
-      g.part_bytes = L.part_bytes;
+      g.out = (float *)(ws + L.wpart[v]);
+      g.part_bytes = L.wpart_bytes[v];
       g.B = B;
       g.y0 = a;
       g.y1 = b;
@@ -279,7 +310,15 @@ struct Run {
       g.Hs = su.h;
       g.Ws = su.w;
       g.kh = d.kh, g.kw = d.kw, g.sh = d.sh, g.sw = d.sw, g.ph = d.ph, g.pw = d.pw;
-      LAUNCH(launch_wgrad(dt, g, dw[v], stream), "weight gradient");
+      if (side) {
+        LAUNCH(hipEventRecord((hipEvent_t)P.ev_act, (hipStream_t)stream), "event record");
+        LAUNCH(hipStreamWaitEvent(side, (hipEvent_t)P.ev_act, 0), "stream wait");
+        LAUNCH(launch_wgrad(dt, g, dw[v], side), "weight gradient");
+        LAUNCH(hipEventRecord((hipEvent_t)P.ev_wg, side), "event record");
+        wg_pending = true;
+      } else {
+        LAUNCH(launch_wgrad(dt, g, dw[v], stream), "weight gradient");
+      }
       if (u != 0 || want_dx) {
         ConvArgs c{};
         c.src = View{dc, (long long)(b - a) * sv.w * sv.c, a, sv.w, sv.c, b - a};
@@ -339,6 +378,12 @@ struct Run {
     }
     for (int v = n - 1; v >= 1; --v) {
       const lrcnn_node &d = P.nodes[v];
+      // a conv's step starts by joining the previous weight gradient: its
+      // error operand and partial sums live in arena space this step reuses
+      if (side && wg_pending && d.op == LRCNN_OP_CONV) {
+        LAUNCH(hipStreamWaitEvent((hipStream_t)stream, (hipEvent_t)P.ev_wg, 0), "stream join");
+        wg_pending = false;
+      }
       int ins[2] = {d.in0, d.op == LRCNN_OP_ADD ? d.in1 : -1};
       for (int u : ins)
         if (u >= 0 && first_consumer[u] == v) {
@@ -358,6 +403,12 @@ struct Run {
                  "carry store");
         }
       }
+    }
+    // the next band's recompute overwrites the windows the weight
+    // gradients read
+    if (side && wg_pending) {
+      LAUNCH(hipStreamWaitEvent((hipStream_t)stream, (hipEvent_t)P.ev_wg, 0), "stream join");
+      wg_pending = false;
     }
     // input gradient rows
     if (want_dx) {
@@ -431,6 +482,15 @@ int check_dw(const Plan &P, float *const *dw) {
 uint64_t g_epoch = 0;
 
 }  // namespace
+
+void release_side(Plan &P) {
+  if (P.ev_act) (void)hipEventDestroy((hipEvent_t)P.ev_act);
+  if (P.ev_wg) (void)hipEventDestroy((hipEvent_t)P.ev_wg);
+  if (P.side_stream) (void)hipStreamDestroy((hipStream_t)P.side_stream);
+  P.ev_act = P.ev_wg = P.side_stream = nullptr;
+  P.side_dev = -1;
+}
+
 }  // namespace lrcnn
 
 using namespace lrcnn;
@@ -478,6 +538,7 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
     return lrcnn_fail(LRCNN_ESTATE,
                       "CARRY backward needs a preceding lrcnn_forward_rows on this plan and workspace");
   Run run(P, P.rc, carry ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale, aff_shift, stream);
+  if (!g_dry && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
   if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
   float *dxacc = nullptr;
   if (!carry && dx) {
@@ -522,6 +583,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
   if ((st = check_dw(P, dw)) != LRCNN_OK) return st;
   if ((st = check_ws(P.lw, workspace, ws_bytes)) != LRCNN_OK) return st;
   Run run(P, P.lw, S_LAYERWISE, workspace, x, w, aff_scale, aff_shift, stream);
+  if (!g_dry && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
   // FP keeps every node's full map; BP reads them without recomputing.
   // The pool argmax is produced in FP (bp = true selects its buffer).
   if ((st = run.band_fwd(0, y, mask_out, true)) != LRCNN_OK) return st;

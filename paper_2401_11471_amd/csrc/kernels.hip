@@ -307,6 +307,36 @@ __device__ __forceinline__ void interleave_step() {
   }
 }
 
+// XCD-aware tile order. Workgroups are dispatched to the 8 XCDs round-robin
+// (workgroup w runs on XCD w mod 8), and each XCD has its own L2. The
+// workgroup's linear id is remapped so that every XCD receives one
+// contiguous run of the tile order, in which neighbouring tiles share
+// operand rows; without it each XCD would fetch nearly all of both
+// operands into its L2.
+struct TileId {
+  int x, y, z;
+};
+__device__ __forceinline__ TileId xcd_tile(bool y_fastest) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int total = gx * gy * gridDim.z;
+  const int w = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int q = total >> 3, r = total & 7, c = w & 7, k = w >> 3;
+  const int id = c < r ? c * (q + 1) + k : r * (q + 1) + (c - r) * q + k;
+  TileId t;
+  if (y_fastest) {
+    t.y = id % gy;
+    const int rest = id / gy;
+    t.x = rest % gx;
+    t.z = rest / gx;
+  } else {
+    t.x = id % gx;
+    const int rest = id / gx;
+    t.y = rest % gy;
+    t.z = rest / gy;
+  }
+  return t;
+}
+
 // ------------------------------------------------------- shared helpers
 static unsigned grid_for(long long total) {
   long long g = (total + 255) / 256;
@@ -393,7 +423,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  // output-channel tiles fastest: a run of consecutive pixel tiles per XCD
+  const TileId tl = xcd_tile(true);
+  const int m0 = tl.x * BM, n0 = tl.y * BN;
   const int taps = a.kh * a.kw;
   const int CB = (a.KC + BK - 1) / BK;
   const int KT = taps * CB;
@@ -431,9 +463,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   }
   const int bk0 = tid / BV;
 
-  // K iterations of this workgroup (split-K over blockIdx.z), walked as
+  // K iterations of this workgroup (split-K over the tile's z), walked as
   // (tap, channel block) without divisions in the loop
-  const int kbeg = blockIdx.z * a.kts;
+  const int kbeg = tl.z * a.kts;
   const int kend = min(KT, kbeg + a.kts);
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
@@ -589,7 +621,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 
   if (gridDim.z > 1) {
     // split-K: raw partial sums, reduced in split order by the epilogue kernel
-    float *part = a.part + (long long)blockIdx.z * M * a.N;
+    float *part = a.part + (long long)tl.z * M * a.N;
     const int col = lane & 31;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -790,8 +822,10 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
   const int K = a.B * R * a.Wv;
   const int taps = a.kh * a.kw;
   const int N = taps * a.Ci;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  const int kbeg = blockIdx.z * kchunk;
+  // one split's pixel range per run of workgroups on an XCD
+  const TileId tl = xcd_tile(false);
+  const int m0 = tl.x * BM, n0 = tl.y * BN;
+  const int kbeg = tl.z * kchunk;
   const int kend = min(K, kbeg + kchunk);
   const int rv = tid % RV, kk0 = tid / RV;
   const T *dc = (const T *)a.dc;
@@ -930,7 +964,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
   if (t < n) step(t, f0, f1);
 
   const int col = lane & 31;
-  float *out = gridDim.z == 1 ? dw : a.out + (long long)blockIdx.z * a.Co * N;
+  float *out = gridDim.z == 1 ? dw : a.out + (long long)tl.z * a.Co * N;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll

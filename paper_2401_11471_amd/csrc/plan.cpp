@@ -307,6 +307,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   // the convolution forward / input gradient, for every launch the
   // schedule makes, with the launchers' own split rule
   size_t part = 0;
+  std::vector<size_t> wpn(n, 0);  // per conv node: weight-gradient partial bytes
   const size_t pcap = (size_t)24 << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
@@ -322,7 +323,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
         if (q.b <= q.a) continue;
         const long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
         const int sw_ = wgrad_split_count(d.c_out, nw, mf, pcap, P.es);
-        if (sw_ > 1) part = std::max(part, (size_t)sw_ * d.c_out * nw * 4);
+        if (sw_ > 1) wpn[v] = std::max(wpn[v], (size_t)sw_ * d.c_out * nw * 4);
         const int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), pcap, P.es);
         if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
         const int u0 = std::max(0, q.a * d.sh - d.ph);
@@ -351,23 +352,48 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   for (int v = 0; v < n; ++v)
     if (carry[v] > 0) L.carry[v] = A.take(P.elems(v, carry[v]) * 4);
   L.carry_bytes = A.top - k0;
-  // error windows: node v's window is live from the step of its first
-  // consumer in reverse order (the largest consumer id) to its own step
+  // BP arena, packed by lifetime over the backward steps (step s handles
+  // node n-1-s):
+  //  - node v's error window lives from the step of its first consumer in
+  //    reverse order (the largest consumer id) to its own step;
+  //  - a conv's error operand and weight-gradient partial sums are read by
+  //    the weight gradient on the side stream, which the caller's stream
+  //    joins at the start of the next conv's step, so they live from the
+  //    conv's own step up to that one.
   std::vector<LiveBuf> bufs(n);
   for (int v = 0; v < n; ++v) {
     int first = v;
     for (int c : P.cons[v]) first = std::max(first, c);
     bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, cap[v]) * 4, 0};
   }
+  std::vector<int> dc_i(n, -1), wp_i(n, -1);
+  for (int v = 1; v < n; ++v) {
+    if (P.nodes[v].op != LRCNN_OP_CONV) continue;
+    int nxt = 0;  // next conv in backward order
+    for (int u = v - 1; u >= 1 && !nxt; --u)
+      if (P.nodes[u].op == LRCNN_OP_CONV) nxt = u;
+    const int s0 = n - 1 - v, s1 = nxt ? n - 2 - nxt : n - 1;
+    dc_i[v] = (int)bufs.size();
+    bufs.push_back(LiveBuf{s0, s1, P.elems(v, own[v]) * P.es, 0});
+    if (wpn[v] > 0) {
+      wp_i[v] = (int)bufs.size();
+      bufs.push_back(LiveBuf{s0, s1, wpn[v], 0});
+    }
+  }
   size_t dpeak = pack(bufs);
   size_t d0 = A.take(dpeak);
   for (int v = 0; v < n; ++v) L.delta[v] = d0 + bufs[v].off;
+  L.dc.assign(n, 0);
+  L.wpart.assign(n, 0);
+  L.wpart_bytes.assign(n, 0);
+  for (int v = 1; v < n; ++v) {
+    if (dc_i[v] >= 0) L.dc[v] = d0 + bufs[dc_i[v]].off;
+    if (wp_i[v] >= 0) {
+      L.wpart[v] = d0 + bufs[wp_i[v]].off;
+      L.wpart_bytes[v] = wpn[v];
+    }
+  }
   L.delta_bytes = dpeak;
-  size_t dc = 0;
-  for (int v = 1; v < n; ++v)
-    if (P.nodes[v].op == LRCNN_OP_CONV) dc = std::max(dc, P.elems(v, own[v]) * P.es);
-  L.dc_bytes = dc;
-  L.dc = A.take(dc);
   if (dxacc) {
     L.dxacc_bytes = P.elems(0, P.shp[0].h) * 4;
     L.dxacc = A.take(L.dxacc_bytes);
@@ -597,5 +623,8 @@ extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int
 }
 
 extern "C" void lrcnn_plan_destroy(lrcnn_plan_t *plan) {
-  delete reinterpret_cast<Plan *>(plan);
+  if (!plan) return;
+  Plan *p = reinterpret_cast<Plan *>(plan);
+  release_side(*p);
+  delete p;
 }

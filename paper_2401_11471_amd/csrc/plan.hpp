@@ -32,8 +32,10 @@ struct Layout {
   std::vector<size_t> carry;     // per node: float32 error carried to band r-1
   std::vector<int> carry_cap;
   std::vector<std::vector<size_t>> strip;  // [band][node]: shared rows kept
-  size_t dc = 0, dc_bytes = 0;   // error operand of one conv (storage dtype)
-  size_t part = 0, part_bytes = 0;  // weight-gradient partial sums
+  size_t part = 0, part_bytes = 0;  // split-K partial sums (forward, input gradient)
+  // per conv node, in the BP arena: error operand (storage dtype) and
+  // weight-gradient partial sums
+  std::vector<size_t> dc, wpart, wpart_bytes;
   size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
   size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;
   // forward windows packed by lifetime (when the forward partition is
@@ -65,14 +67,18 @@ struct Plan {
   const void *fwd_workspace = nullptr;
   uint64_t fwd_epoch = 0;
   bool last_band_kept = false;  // FP left the last band's maps in place
+  // side stream and two events of the backward, created by the executor on
+  // first use for the device current at that call (opaque HIP handles)
+  void *side_stream = nullptr, *ev_act = nullptr, *ev_wg = nullptr;
+  int side_dev = -1;
 
   size_t elems(int v, int rows_) const {
     return (size_t)cfg.batch * rows_ * shp[v].w * shp[v].c;
   }
 };
 
-// Weight-gradient split count for a conv with the given GEMM sizes: enough
-// workgroups to fill the chip, at least `min_k` reduction steps each.
+// Releases the executor's side stream and events of a plan (exec.cpp).
+void release_side(Plan &P);
 
 }  // namespace lrcnn
 
