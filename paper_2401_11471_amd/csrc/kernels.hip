@@ -203,26 +203,61 @@ struct Frag<float, BN, KR, AKM, BKM> {
   }
 };
 
-template <int BN, int KR>
-struct Frag<bf16, BN, KR, 0, 0> {
+// bfloat16: one MFMA slice s (16 K values) gives lane half g = l >> 5 the
+// K values 16*g + 8*s + [0, 8) of row / column l & 31 of its 32x32 block.
+// [row][k] operands are read as one 16-byte vector per slice. k-major
+// operands ([k][row], pitch rows + 8) are read with two transposing LDS
+// reads (ds_read_b64_tr_b16): within each 16-lane group, lane i receives
+// element i mod 4 of the 8-byte runs addressed by lanes 4*k' + i/4,
+// k' = 0..3, so lane 16*G + 4*k' + q addresses K row
+// 16*(G >> 1) + 8*s + 4*t + k' at column 16*(G & 1) + 4*q (t = 0, 1 for the
+// two reads), which hands every lane the same K values as the [row][k]
+// read. Both layouts therefore sum K in the same order.
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int pitch, int base, int s, int lane) {
+  const int G = lane >> 4, sl = lane & 15;
+  const int k = 16 * (G >> 1) + 8 * s + (sl >> 2);
+  const int col = base + 16 * (G & 1) + 4 * (sl & 3);
+  const bf16 *p0 = T + k * pitch + col, *p1 = T + (k + 4) * pitch + col;
+  const bf16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4 *)((__attribute__((address_space(3))) char *)(char *)p0));
+  const bf16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+      (lds_bf16x4 *)((__attribute__((address_space(3))) char *)(char *)p1));
+  return __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+template <int BN, int KR, int AKM, int BKM>
+struct Frag<bf16, BN, KR, AKM, BKM> {
   static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
+  static constexpr int PA = BM + 8, PB = BN + 8;
   static constexpr int NMFMA = NV * 2 * NB;
-  static constexpr int NDSR = 2 * NV + NB * NV;
+  static constexpr int NDSR = (AKM ? 4 * NV : 2 * NV) + (BKM ? 2 * NB * NV : NB * NV);
   bf16x8 a[2][NV], b[NB][NV];
   __device__ __forceinline__ void load(const bf16 *As, const bf16 *Bs, int wm, int wn,
                                        int lane) {
     const int r = lane & 31, g = lane >> 5;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 8 * NV * g);
+      if (AKM) {
 #pragma unroll
-      for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+        for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8(As, PA, wm + 32 * i, q, lane);
+      } else {
+        const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 8 * NV * g);
+#pragma unroll
+        for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+      }
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 8 * NV * g);
+      if (BKM) {
 #pragma unroll
-      for (int q = 0; q < NV; ++q) b[j][q] = p[q];
+        for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8(Bs, PB, wn + 32 * j, q, lane);
+      } else {
+        const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 8 * NV * g);
+#pragma unroll
+        for (int q = 0; q < NV; ++q) b[j][q] = p[q];
+      }
     }
   }
   __device__ __forceinline__ void mma(f32x16 (&acc)[2][NB]) const {
@@ -414,9 +449,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // three LDS stages: while tile t is multiplied, the fragments of t+1 are
   // read, tile t+2 is written and tile t+3 is fetched from global memory
   constexpr int ST = 3;
-  // float32 input gradient: weights staged k-major (16-byte stores)
-  constexpr int BKM = (DGRAD && sizeof(T) == 4) ? 1 : 0;
-  constexpr int PB = BN + 4;
+  // input gradient: weights staged k-major (16-byte stores)
+  constexpr int BKM = DGRAD ? 1 : 0;
+  constexpr int PB = BN + E;
   constexpr int BSZ = BKM ? BK * PB : BN * LDK;
   __shared__ __align__(16) T As[ST][BM * LDK];
   __shared__ __align__(16) T Bs[ST][BSZ];
@@ -802,17 +837,17 @@ __device__ __forceinline__ void divmod_rcp(int p, int d, float inv, int &q, int 
 // A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
 // input pixel under tap; both are K-outer in memory, so tiles are written
 // to LDS transposed into the same [row][k] layout used above.
-template <typename T, bool VEC>
+template <typename T, bool AVEC, bool BVEC>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
                                                     float *dw) {
   constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
   constexpr int BN = 128, NB = 2;
   constexpr int RV = BM / E;        // 16-byte vectors per 128-wide tile row
   constexpr int KS = 256 / RV;      // pixels loaded per pass
-  // float32: both operands staged k-major with 16-byte stores; bfloat16:
-  // transposed element stores into the [row][k] layout
-  constexpr int KM = sizeof(T) == 4 ? 1 : 0;
-  constexpr int PA = BM + 4, PB = BN + 4;
+  // both operands are K-outer in memory and staged k-major with 16-byte
+  // stores
+  constexpr int KM = 1;
+  constexpr int PA = BM + E, PB = BN + E;
   constexpr int ASZ = KM ? BK * PA : BM * LDK, BSZ = KM ? BK * PB : BN * LDK;
   constexpr int ST = 3;
   __shared__ __align__(16) T As[ST][ASZ];
@@ -846,6 +881,22 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
   int k0 = kbeg;
   const bool ovok = ov < a.Co, nbok = nb0 < N;
   const float invW = 1.0f / (float)a.Wv, invR = 1.0f / (float)R;
+  // channel counts that are not a multiple of E (the first layer): the
+  // (tap, channel) of each of this thread's E columns, fixed for the launch
+  int cti[BVEC ? 1 : E], ctj[BVEC ? 1 : E], cc[BVEC ? 1 : E];
+  bool cok[BVEC ? 1 : E];
+  if (!BVEC) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int n = nb0 + e;
+      const int tap = n / a.Ci;
+      cc[e] = n - tap * a.Ci;
+      cti[e] = tap / a.kw;
+      ctj[e] = tap - cti[e] * a.kw;
+      cok[e] = n < N;
+    }
+  }
+  const T *zero_e = (const T *)&g_zero16[0];
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
 #pragma unroll
@@ -853,7 +904,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       const int p = k0 + kk0 + KS * i;
       const bool pk = p < kend;
       // A: E output channels of pixel p
-      if (VEC) {
+      if (AVEC) {
         ra[i].u = load16z(dc, ((long long)p * a.Co + ov) * (long long)sizeof(T), pk & ovok);
       } else {
 #pragma unroll
@@ -865,23 +916,22 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
       divmod_rcp(pk ? p : 0, a.Wv, invW, t, x);
       divmod_rcp(t, R, invR, b, yy);
       const int y = a.y0 + yy;
-      if (VEC) {
+      if (BVEC) {
         const int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
         const bool ok = pk & nbok & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
         const long long off =
             b * a.src.bs + (sy - a.src.row0) * srow + (long long)sx * a.src.C + cv;
         rb[i].u = load16z(src, off * (long long)sizeof(T), ok);
       } else {
+        const long long bbase = b * a.src.bs - a.src.row0 * srow;
+        const int sy0 = y * a.sh - a.ph, sx0 = x * a.sw - a.pw;
 #pragma unroll
         for (int e = 0; e < E; ++e) {
-          const int n = nb0 + e;
-          const int tap = n / a.Ci, c = n - (n / a.Ci) * a.Ci;
-          const int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
-          const int sy = y * a.sh - a.ph + ti, sx = x * a.sw - a.pw + tj;
-          const bool ok = pk && n < N && sy >= 0 && sy < a.Hs && sx >= 0 && sx < a.Ws;
-          rb[i].e[e] = ok ? src[b * a.src.bs + (sy - a.src.row0) * srow +
-                                (long long)sx * a.src.C + c]
-                          : (T)0;
+          const int sy = sy0 + cti[e], sx = sx0 + ctj[e];
+          const bool ok =
+              pk & cok[e] & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+          const T *q = ok ? src + bbase + sy * srow + (long long)sx * a.src.C + cc[e] : zero_e;
+          rb[i].e[e] = *q;
         }
       }
     }
@@ -951,7 +1001,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
     __syncthreads();
   };
   int t = 0;
-  if (VEC) {
+  if (AVEC && BVEC) {
     for (; t + 4 < n; t += 2) {
       step_full(f0, f1);
       step_full(f1, f0);
@@ -1014,15 +1064,16 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   const int KT = (K + BK - 1) / BK;
   const int kchunk = (KT + splits - 1) / splits * BK;
   splits = (K + kchunk - 1) / kchunk;
-  const bool vec = (a.Co % Cfg<T>::E) == 0 && (a.Ci % Cfg<T>::E) == 0;
+  const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
   dim3 grid((a.Co + BM - 1) / BM, (N + 127) / 128, splits);
   int pr = -1;
   if (prof::on)
     pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
-                         (vec ? ", vec>" : ", scalar>"),
+                         (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
-  if (vec) wgrad_kernel<T, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
-  else wgrad_kernel<T, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  if (avec && bvec) wgrad_kernel<T, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  else if (avec) wgrad_kernel<T, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  else wgrad_kernel<T, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
   prof::end(pr, s);
   if (splits > 1) {
     long long mn = (long long)a.Co * N;

@@ -49,9 +49,10 @@ def bench_name(mangled: str) -> str:
         return (f"conv_gemm_kernel<{m.group(1)}, {m.group(2)}, "
                 f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, "
                 f"{'vec' if m.group(4) == 'true' else 'scalar'}>")
-    m = re.match(r"wgrad_kernel<(\w+), (true|false)>", n)
+    m = re.match(r"wgrad_kernel<(\w+), (true|false), (true|false)>", n)
     if m:
-        return f"wgrad_kernel<{m.group(1)}, {'vec' if m.group(2) == 'true' else 'scalar'}>"
+        vec = m.group(2) == "true" and m.group(3) == "true"
+        return f"wgrad_kernel<{m.group(1)}, {'vec' if vec else 'scalar'}>"
     for short in ("conv_split_epilogue", "wgrad_reduce_kernel"):
         if n.startswith(short):
             return short
