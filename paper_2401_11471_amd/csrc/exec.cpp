@@ -299,6 +299,19 @@ struct Run {
       WgradArgs g{};
       g.dc = dc;
       g.src = act[u];
+      float *wdst = dw[v];
+      const bool padded = L.cpad && u == 0;
+      if (padded) {
+        // input rows of the band in channel-padded form
+        const int r0 = std::max(0, a * d.sh - d.ph);
+        const int r1 = std::min(su.h, (b - 1) * d.sh - d.ph + d.kh);
+        if (r1 - r0 > L.xpad_cap) return lrcnn_fail(LRCNN_EINVAL, "internal: padded input rows");
+        g.src = View{ws + L.xpad, (long long)L.xpad_cap * su.w * L.cpad, r0, su.w, L.cpad,
+                     L.xpad_cap};
+        LAUNCH(launch_pad_channels(dt, act[0], g.src, su.c, L.cpad, B, r0, r1, su.w, stream),
+               "pad input channels");
+        wdst = (float *)(ws + L.dwpad[v]);
+      }
       g.out = (float *)(ws + L.wpart[v]);
       g.part_bytes = L.wpart_bytes[v];
       g.B = B;
@@ -306,18 +319,18 @@ struct Run {
       g.y1 = b;
       g.Wv = sv.w;
       g.Co = sv.c;
-      g.Ci = su.c;
+      g.Ci = padded ? L.cpad : su.c;
       g.Hs = su.h;
       g.Ws = su.w;
       g.kh = d.kh, g.kw = d.kw, g.sh = d.sh, g.sw = d.sw, g.ph = d.ph, g.pw = d.pw;
       if (side) {
         LAUNCH(hipEventRecord((hipEvent_t)P.ev_act, (hipStream_t)stream), "event record");
         LAUNCH(hipStreamWaitEvent(side, (hipEvent_t)P.ev_act, 0), "stream wait");
-        LAUNCH(launch_wgrad(dt, g, dw[v], side), "weight gradient");
+        LAUNCH(launch_wgrad(dt, g, wdst, side), "weight gradient");
         LAUNCH(hipEventRecord((hipEvent_t)P.ev_wg, side), "event record");
         wg_pending = true;
       } else {
-        LAUNCH(launch_wgrad(dt, g, dw[v], stream), "weight gradient");
+        LAUNCH(launch_wgrad(dt, g, wdst, stream), "weight gradient");
       }
       if (u != 0 || want_dx) {
         ConvArgs c{};
@@ -437,8 +450,31 @@ struct Run {
     for (int v = 1; v < P.n; ++v)
       if (P.nodes[v].op == LRCNN_OP_CONV) {
         const lrcnn_node &d = P.nodes[v];
+        if (L.cpad && d.in0 == 0) {
+          size_t cnt = (size_t)d.c_out * d.kh * d.kw * L.cpad;
+          LAUNCH(launch_zero_f32((float *)(ws + L.dwpad[v]), cnt, stream), "zero dW");
+          continue;
+        }
         size_t cnt = (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c;
         LAUNCH(launch_zero_f32(dw[v], cnt, stream), "zero dW");
+      }
+    return LRCNN_OK;
+  }
+
+  // first-layer weight gradients accumulated in channel-padded form
+  int finish_dw(float *const *dw) {
+    if (!L.cpad) return LRCNN_OK;
+    if (side && wg_pending) {
+      LAUNCH(hipStreamWaitEvent((hipStream_t)stream, (hipEvent_t)P.ev_wg, 0), "stream join");
+      wg_pending = false;
+    }
+    for (int v = 1; v < P.n; ++v)
+      if (P.nodes[v].op == LRCNN_OP_CONV && P.nodes[v].in0 == 0) {
+        const lrcnn_node &d = P.nodes[v];
+        const long long cnt = (long long)d.c_out * d.kh * d.kw * P.shp[0].c;
+        LAUNCH(launch_compact_dw((const float *)(ws + L.dwpad[v]), dw[v], P.shp[0].c, L.cpad,
+                                 cnt, stream),
+               "first-layer dW");
       }
     return LRCNN_OK;
   }
@@ -557,6 +593,7 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
     if ((st = run.band_fwd(r, nullptr, nullptr, true, false, skip)) != LRCNN_OK) return st;
     if ((st = run.band_bwd(r, dy, dw, dx, dxacc)) != LRCNN_OK) return st;
   }
+  if ((st = run.finish_dw(dw)) != LRCNN_OK) return st;
   if (!carry && dx && P.cfg.dtype == LRCNN_BF16 && !g_dry) {
     const Shape &s = P.shp[0];
     int e = launch_rows_copy(DT_F32, DT_BF16, run.full(dxacc, 0), run.full(dx, 0), 0,
@@ -588,7 +625,8 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
   // The pool argmax is produced in FP (bp = true selects its buffer).
   if ((st = run.band_fwd(0, y, mask_out, true)) != LRCNN_OK) return st;
   if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
-  return run.band_bwd(0, dy, dw, dx, nullptr);
+  if ((st = run.band_bwd(0, dy, dw, dx, nullptr)) != LRCNN_OK) return st;
+  return run.finish_dw(dw);
 }
 
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }

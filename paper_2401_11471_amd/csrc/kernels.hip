@@ -1389,6 +1389,47 @@ int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C, void *stream
   return (int)hipGetLastError();
 }
 
+// Rows [r0, r1) of a map with C channels into a view with Cp > C channels
+// (storage dtype), the extra channels zero. Gives a first layer with few
+// input channels whole 16-byte vectors per pixel for its weight gradient.
+template <typename T>
+__global__ void pad_channels_kernel(View src, View dst, int C, int Cp, RowIter it) {
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, 1, b, y, in);
+    const int x = in / Cp, c = in - x * Cp;
+    T v = (T)0;
+    if (c < C) v = ((const T *)src.p)[view_off(src, b, y, x * C + c)];
+    ((T *)dst.p)[view_off(dst, b, y, in)] = v;
+  }
+}
+
+int launch_pad_channels(int dt, View src, View dst, int C, int Cp, int B, int r0, int r1,
+                        int W, void *stream) {
+  RowIter it = row_iter(B, r0, r1, W, Cp, 1);
+  if (it.total <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == DT_F32)
+    pad_channels_kernel<float><<<grid_for(it.total), 256, 0, s>>>(src, dst, C, Cp, it);
+  else
+    pad_channels_kernel<bf16><<<grid_for(it.total), 256, 0, s>>>(src, dst, C, Cp, it);
+  return (int)hipGetLastError();
+}
+
+// dW [rows][C] from a channel-padded float32 [rows][Cp] (n = rows * C).
+__global__ void compact_dw_kernel(const float *pad, float *dw, int C, int Cp, long long n) {
+  GRID_STRIDE(i, n) {
+    const long long t = i / C;
+    dw[i] = pad[t * Cp + (i - t * C)];
+  }
+}
+
+int launch_compact_dw(const float *pad, float *dw, int C, int Cp, long long n, void *stream) {
+  if (n <= 0) return 0;
+  compact_dw_kernel<<<grid_for(n), 256, 0, (hipStream_t)stream>>>(pad, dw, C, Cp, n);
+  return (int)hipGetLastError();
+}
+
 __global__ void zero_kernel(float *p, long long n) {
   GRID_STRIDE(i, n) p[i] = 0.f;
 }

@@ -161,6 +161,11 @@ int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate,
 int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C,
                      void *stream);
 int launch_zero_f32(float *p, size_t n, void *stream);
+// Rows [r0, r1) of src (C channels) into dst (Cp channels, extra ones zero).
+int launch_pad_channels(int dt, View src, View dst, int C, int Cp, int B, int r0, int r1,
+                        int W, void *stream);
+// dw[t][c] = pad[t][c] for c < C, t over n / C rows of the padded [t][Cp].
+int launch_compact_dw(const float *pad, float *dw, int C, int Cp, long long n, void *stream);
 
 // Launch timing of the matrix-core kernels (test hook).
 void profile_enable(int enable);

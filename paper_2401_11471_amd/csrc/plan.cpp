@@ -308,13 +308,19 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   // schedule makes, with the launchers' own split rule
   size_t part = 0;
   std::vector<size_t> wpn(n, 0);  // per conv node: weight-gradient partial bytes
+  // a first layer whose input channels do not fill 16-byte vectors computes
+  // its weight gradient from a channel-padded copy of the input rows
+  const int vec_e = 16 / P.es;
+  L.cpad = P.shp[0].c % vec_e ? (P.shp[0].c + vec_e - 1) / vec_e * vec_e : 0;
+  int xrows = 0;
   const size_t pcap = (size_t)24 << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
       const Shape &su = P.shp[d.in0], &sv = P.shp[v];
       const int taps = d.kh * d.kw;
-      const int64_t nw = (int64_t)taps * su.c;
+      const bool padded = L.cpad && d.in0 == 0;
+      const int64_t nw = (int64_t)taps * (padded ? L.cpad : su.c);
       std::vector<Rows> qs;
       if (layerwise) qs.push_back(Rows{0, sv.h, 0, sv.h});
       for (auto *tab : bands)
@@ -328,6 +334,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
         if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
         const int u0 = std::max(0, q.a * d.sh - d.ph);
         const int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
+        if (padded) xrows = std::max(xrows, u1 - u0);
         const long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
         const int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), pcap, P.es);
         if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
@@ -343,6 +350,14 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
     L.win[v] = A.take(P.elems(v, cap[v]) * P.es);
   }
   L.cache_bytes = A.top - c0;
+  L.dwpad.assign(n, 0);
+  if (L.cpad) {
+    L.xpad_cap = xrows;
+    L.xpad = A.take((size_t)P.cfg.batch * xrows * P.shp[0].w * L.cpad * P.es);
+    for (int v = 1; v < n; ++v)
+      if (P.nodes[v].op == LRCNN_OP_CONV && P.nodes[v].in0 == 0)
+        L.dwpad[v] = A.take((size_t)P.nodes[v].c_out * P.nodes[v].kh * P.nodes[v].kw * L.cpad * 4);
+  }
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_MAXPOOL) {
       L.argmax_cap[v] = own[v];

@@ -36,6 +36,12 @@ struct Layout {
   // per conv node, in the BP arena: error operand (storage dtype) and
   // weight-gradient partial sums
   std::vector<size_t> dc, wpart, wpart_bytes;
+  // input with a channel count that is not a multiple of one 16-byte vector:
+  // a channel-padded copy of the rows a first-layer weight gradient reads,
+  // and that gradient accumulated in padded form [C_out][taps][cpad]
+  int cpad = 0, xpad_cap = 0;
+  size_t xpad = 0;
+  std::vector<size_t> dwpad;
   size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
   size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;
   // forward windows packed by lifetime (when the forward partition is
