@@ -8,7 +8,8 @@ tensors with the paper's shapes (ImageNet is not available), resident in HBM
 before timing starts. Prints one JSON line.
 
 Default workload: VGG-16 conv trunk, float32, batch 8, 3x224x224, 4 row bands
-of 56 rows, two-phase sharing. Also reported: peak activation bytes of the
+of 56 rows, two-phase sharing. The timed step is captured once in a HIP graph
+and replayed (--eager launches every kernel from the host instead). Also reported: peak activation bytes of the
 row-centric step against the layer-wise baseline (same kernels, every
 feature map kept), the layer-wise step's speed, the overlapping-recompute
 mode's speed (halo overhead), a roofline line for the dominant kernel, and
@@ -44,6 +45,9 @@ def parse():
                     help="skip the layer-wise / recompute comparison runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4)
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every kernel from the host in the timed region "
+                         "(default: the step is captured once in a HIP graph and replayed)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a "
                          "known-size reference for hardware byte counters)")
@@ -80,6 +84,53 @@ def cpu_baseline(cfg_id, n_img):
             "kind": "oracle",
             "sample": f"{n_img} image(s) of the same workload, float64 column FP+BP "
                       f"(numpy/BLAS), {dt:.1f} s"}
+
+
+def timed_steps(torch, step, steps, warmup, eager, profile=None):
+    """ms per step over `steps` steps between two events on the current
+    stream. By default the step is captured once in a HIP graph (after a
+    warm-up run on a side stream, as capture requires) and replayed, so the
+    host's per-launch cost is not in the timed region; the library's
+    per-launch events, when `profile` switches them on, are captured into
+    the graph and hold the last replay's times. Returns (ms, profiled steps,
+    graph)."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if eager:
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        if profile:
+            profile(True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        if profile:
+            profile(False)
+        return e0.elapsed_time(e1) / steps, steps, None
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    if profile:
+        profile(True)
+    with torch.cuda.graph(graph):
+        step()
+    if profile:
+        profile(False)
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps, 1, graph
 
 
 def main():
@@ -144,21 +195,17 @@ def main():
         del csrc, cdst
 
     # --- timed region
-    for _ in range(args.warmup):
-        rc_step(bufs)
-    torch.cuda.synchronize()
-    L.lrcnn_debug_profile(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        rc_step(bufs)
-    e1.record()
-    torch.cuda.synchronize()
-    L.lrcnn_debug_profile(False)
-    ms = e0.elapsed_time(e1) / args.steps
-    kern = L.lrcnn_debug_profile_collect()
+    ms, psteps, graph = timed_steps(torch, lambda: rc_step(bufs), args.steps, args.warmup,
+                                    args.eager, L.lrcnn_debug_profile if args.eager else None)
+    del graph
     value = B * 1000.0 / ms
+    if not args.eager:
+        # HIP cannot time events recorded inside a graph, so the per-kernel
+        # durations come from an eager pass of the same steps with the
+        # library's events around every matrix-core launch
+        _, psteps, _ = timed_steps(torch, lambda: rc_step(bufs), args.steps, 0, True,
+                                   L.lrcnn_debug_profile)
+    kern = L.lrcnn_debug_profile_collect()
 
     # dominant kernel: the largest share of the algorithmic FLOPs (the
     # forward convolution: it runs in FP and in the recompute, where no
@@ -178,10 +225,13 @@ def main():
             traffic = None
     roofline = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
                 "frac": round(achieved / peak, 4), "traffic": traffic,
-                "kernel": dom_name, "launches_per_step": dom_n // args.steps,
+                "kernel": dom_name, "launches_per_step": dom_n // psteps,
+                "timing": ("HIP events around every launch in the timed region" if args.eager
+                           else "HIP events around every launch in an eager pass of the "
+                                "same steps after the timed graph replays"),
                 "avg_launch_ms": round(dom_ms / dom_n, 4)}
-    all_mfma_ms = sum(v[1] for k, v in kern.items() if "reduce" not in k) / args.steps
-    all_mfma_fl = sum(v[2] for v in kern.values()) / args.steps
+    all_mfma_ms = sum(v[1] for k, v in kern.items() if "reduce" not in k) / psteps
+    all_mfma_fl = sum(v[2] for v in kern.values()) / psteps
 
     out = {
         "metric": "training images/sec (FP+BP) + peak activation bytes vs layer-wise, 1 MI355X",
@@ -191,13 +241,14 @@ def main():
         "dtype": dts, "data": "synthetic N(0,1), paper's shapes (ImageNet not available)",
         "config": {"workload": c["name"], "net": c["net"], "batch": B,
                    "input": [Cin, H, W], "bands": nb, "bp_bands": info["bp_bands"],
-                   "mode": args.mode, "dx": False},
+                   "mode": args.mode, "dx": False,
+                   "launch": "host" if args.eager else "hip-graph"},
         "roofline": roofline,
         "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),
         "mfma_kernels": {"ms_per_step": round(all_mfma_ms, 3),
                          "tflops": round(all_mfma_fl / (all_mfma_ms * 1e-3) / 1e12, 2),
-                         "per_kernel": {k: {"launches": v[0] // args.steps,
-                                            "ms": round(v[1] / args.steps, 3),
+                         "per_kernel": {k: {"launches": v[0] // psteps,
+                                            "ms": round(v[1] / psteps, 3),
                                             "tflops": round(v[2] / max(v[1], 1e-9) / 1e9, 2)}
                                         for k, v in sorted(kern.items())}},
         "peak_act_bytes": int(peak_rc),
@@ -222,15 +273,9 @@ def main():
                                             dm.dw, None, b["ws"])
         try:
             peak_lw, lb = measure(lw_alloc, lw_step)
-            for _ in range(args.warmup):
-                lw_step(lb)
-            torch.cuda.synchronize()
-            e0.record()
-            for _ in range(args.steps):
-                lw_step(lb)
-            e1.record()
-            torch.cuda.synchronize()
-            lw_ms = e0.elapsed_time(e1) / args.steps
+            lw_ms, _, g_ = timed_steps(torch, lambda: lw_step(lb), args.steps, args.warmup,
+                                       args.eager)
+            del g_
             out["layerwise"] = {"images_per_s": round(B * 1000.0 / lw_ms, 3),
                                 "ms_per_step": round(lw_ms, 3),
                                 "peak_act_bytes": int(peak_lw)}
@@ -252,15 +297,9 @@ def main():
                 L.lrcnn_forward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, b["y"], b["ws"])
                 L.lrcnn_backward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, b["ws"])
             peak_f, fb = measure(f_alloc, f_step)
-            for _ in range(args.warmup):
-                f_step(fb)
-            torch.cuda.synchronize()
-            e0.record()
-            for _ in range(args.steps):
-                f_step(fb)
-            e1.record()
-            torch.cuda.synchronize()
-            f_ms = e0.elapsed_time(e1) / args.steps
+            f_ms, _, g_ = timed_steps(torch, lambda: f_step(fb), args.steps, args.warmup,
+                                      args.eager)
+            del g_
             ent = {"bp_bands": finfo["bp_bands"], "images_per_s": round(B * 1000.0 / f_ms, 3),
                    "ms_per_step": round(f_ms, 3), "peak_act_bytes": int(peak_f)}
             if "peak_act_bytes" in out.get("layerwise", {}):
@@ -279,15 +318,8 @@ def main():
             def rstep():
                 L.lrcnn_forward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, ry, rws)
                 L.lrcnn_backward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, rws)
-            for _ in range(args.warmup):
-                rstep()
-            torch.cuda.synchronize()
-            e0.record()
-            for _ in range(args.steps):
-                rstep()
-            e1.record()
-            torch.cuda.synchronize()
-            r_ms = e0.elapsed_time(e1) / args.steps
+            r_ms, _, g_ = timed_steps(torch, rstep, args.steps, args.warmup, args.eager)
+            del g_
             out["recompute"] = {"images_per_s": round(B * 1000.0 / r_ms, 3),
                                 "ms_per_step": round(r_ms, 3),
                                 "time_over_carry": round(r_ms / ms, 3),
