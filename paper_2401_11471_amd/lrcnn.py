@@ -10,6 +10,12 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+# torch first: it brings its own HIP runtime, and liblrcnn.so must bind to
+# that same runtime (one HIP/HSA runtime per process). Loading the library
+# first would load the system runtime and leave torch and the library on
+# different ones.
+import torch  # noqa: F401
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblrcnn.so")
 
