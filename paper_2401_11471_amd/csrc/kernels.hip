@@ -453,8 +453,14 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   constexpr int BKM = DGRAD ? 1 : 0;
   constexpr int PB = BN + E;
   constexpr int BSZ = BKM ? BK * PB : BN * LDK;
-  __shared__ __align__(16) T As[ST][BM * LDK];
-  __shared__ __align__(16) T Bs[ST][BSZ];
+  // LDS: the operand ring during the K loop; the forward epilogue then
+  // reuses it to stage the output tile ([BM][BN + E] in the storage dtype)
+  constexpr int CP = BN + E;
+  constexpr size_t RING = sizeof(T) * ST * ((size_t)BM * LDK + BSZ);
+  constexpr size_t CTILE = DGRAD ? 0 : sizeof(T) * (size_t)BM * CP;
+  __shared__ __align__(16) char smem[RING > CTILE ? RING : CTILE];
+  T (*As)[BM * LDK] = reinterpret_cast<T (*)[BM * LDK]>(smem);
+  T (*Bs)[BSZ] = reinterpret_cast<T (*)[BSZ]>(smem + sizeof(T) * ST * BM * LDK);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
@@ -676,6 +682,55 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // epilogue
   const int col = lane & 31;
   const long long drow = (long long)a.Wd * a.N;
+  if (!DGRAD && (a.N % E) == 0) {
+    // forward: affine, ReLU (and the optional mask) in registers, the tile
+    // staged in LDS, then whole 16-byte row chunks stored per thread
+    T *Ct = reinterpret_cast<T *>(smem);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = wm + 32 * i + acc_row(v, lane);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int cl = wn + 32 * j + col;
+          const int n = n0 + cl;
+          float val = acc[i][j][v];
+          if (n < a.N) {
+            if (a.scale) val = val * a.scale[n] + a.shift[n];
+            if (a.relu) val = val > 0.f ? val : 0.f;
+          }
+          stf(&Ct[r * CP + cl], val);
+        }
+      }
+    __syncthreads();
+    constexpr int CPR = BN / E;     // 16-byte chunks per tile row
+    constexpr int RPP = 256 / CPR;  // tile rows per pass
+    const int cc = tid % CPR;
+    const int n = n0 + cc * E;
+    for (int r = tid / CPR; r < BM; r += RPP) {
+      const int m = m0 + r;
+      if (m >= M || n >= a.N) continue;
+      const int x = m % a.Wd;
+      const int t = m / a.Wd;
+      const int y = a.y0 + t % R;
+      const int b = t / R;
+      const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
+      const uint4 q = *(const uint4 *)&Ct[r * CP + cc * E];
+      *(uint4 *)((T *)a.dst.p + off) = q;
+      if (a.mask) {
+        union {
+          uint4 u;
+          T e[E];
+        } w;
+        w.u = q;
+        uint8_t *mk = a.mask + (((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n;
+#pragma unroll
+        for (int e = 0; e < E; ++e) mk[e] = ldf(&w.e[e]) > 0.f ? 1 : 0;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
 #pragma unroll
