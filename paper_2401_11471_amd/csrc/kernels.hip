@@ -457,7 +457,9 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // reuses it to stage the output tile ([BM][BN + E] in the storage dtype)
   constexpr int CP = BN + E;
   constexpr size_t RING = sizeof(T) * ST * ((size_t)BM * LDK + BSZ);
-  constexpr size_t CTILE = DGRAD ? 0 : sizeof(T) * (size_t)BM * CP;
+  // (input gradient: float32 tile [BM][BN + 4], added to the error window)
+  constexpr size_t CTILE = DGRAD ? sizeof(float) * (size_t)BM * (BN + 4)
+                                 : sizeof(T) * (size_t)BM * CP;
   __shared__ __align__(16) char smem[RING > CTILE ? RING : CTILE];
   T (*As)[BM * LDK] = reinterpret_cast<T (*)[BM * LDK]>(smem);
   T (*Bs)[BSZ] = reinterpret_cast<T (*)[BSZ]>(smem + sizeof(T) * ST * BM * LDK);
@@ -728,6 +730,40 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 #pragma unroll
         for (int e = 0; e < E; ++e) mk[e] = ldf(&w.e[e]) > 0.f ? 1 : 0;
       }
+    }
+    return;
+  }
+  if (DGRAD && (a.N % 4) == 0) {
+    // input gradient: the float32 tile staged in LDS, then 16-byte
+    // read-add-write of the error window
+    constexpr int FP = BN + 4;
+    float *Ct = reinterpret_cast<float *>(smem);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = wm + 32 * i + acc_row(v, lane);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) Ct[r * FP + wn + 32 * j + col] = acc[i][j][v];
+      }
+    __syncthreads();
+    constexpr int CPR = BN / 4;
+    constexpr int RPP = 256 / CPR;
+    const int cc = tid % CPR;
+    const int n = n0 + cc * 4;
+    for (int r = tid / CPR; r < BM; r += RPP) {
+      const int m = m0 + r;
+      if (m >= M || n >= a.N) continue;
+      const int x = m % a.Wd;
+      const int t = m / a.Wd;
+      const int y = a.y0 + t % R;
+      const int b = t / R;
+      float4 *d = (float4 *)((float *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow +
+                             (long long)x * a.N + n);
+      const float4 q = *(const float4 *)&Ct[r * FP + cc * 4];
+      float4 o = *d;
+      o.x += q.x, o.y += q.y, o.z += q.z, o.w += q.w;
+      *d = o;
     }
     return;
   }
@@ -1087,21 +1123,35 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
     }
 }
 
-// dW += sum over splits, in split order (deterministic).
+// dW += sum over the split partial sums in a fixed order (deterministic):
+// eight groups of threads each add the splits z = g, g + 8, ... of 32
+// vectors of V elements, then the eight group sums are added in order.
 template <int V>
-__global__ void wgrad_reduce_kernel(const float *part, float *dw, long long mn,
-                                    int splits) {
-  GRID_STRIDE(i4, mn / V) {
-    const long long i = i4 * V;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f}, q[4];
-    for (int z = 0; z < splits; ++z) {
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, float *dw,
+                                                           long long mn, int splits) {
+  __shared__ float red[8][32 * 4];
+  const int g = threadIdx.x >> 5, e = threadIdx.x & 31;
+  const long long i = ((long long)blockIdx.x * 32 + e) * V;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f}, q[4];
+  if (i < mn) {
+    for (int z = g; z < splits; z += 8) {
       ldv<float, V>(part + z * mn + i, q);
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[e] += q[e];
+      for (int k = 0; k < V; ++k) acc[k] += q[k];
     }
+  }
+#pragma unroll
+  for (int k = 0; k < V; ++k) red[g][e * 4 + k] = acc[k];
+  __syncthreads();
+  if (g == 0 && i < mn) {
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int gg = 0; gg < 8; ++gg)
+#pragma unroll
+      for (int k = 0; k < V; ++k) sum[k] += red[gg][e * 4 + k];
     ldv<float, V>(dw + i, q);
 #pragma unroll
-    for (int e = 0; e < V; ++e) q[e] += acc[e];
+    for (int k = 0; k < V; ++k) q[k] += sum[k];
     stv<float, V>(dw + i, q);
   }
 }
@@ -1134,9 +1184,10 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
     long long mn = (long long)a.Co * N;
     int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
     if (mn % 4 == 0)
-      wgrad_reduce_kernel<4><<<grid_for(mn / 4), 256, 0, s>>>(a.out, dw, mn, splits);
+      wgrad_reduce_kernel<4><<<(unsigned)((mn / 4 + 31) / 32), 256, 0, s>>>(a.out, dw, mn,
+                                                                            splits);
     else
-      wgrad_reduce_kernel<1><<<grid_for(mn), 256, 0, s>>>(a.out, dw, mn, splits);
+      wgrad_reduce_kernel<1><<<(unsigned)((mn + 31) / 32), 256, 0, s>>>(a.out, dw, mn, splits);
     prof::end(p2, s);
   }
   return (int)hipGetLastError();
