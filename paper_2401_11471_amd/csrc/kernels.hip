@@ -802,45 +802,61 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
 // Sum the split-K partials of every output element in split order, then
 // apply the forward epilogue (affine, ReLU, store, mask) or add the input
 // gradient into the error window.
+// Sum the split-K partials of every output element in a fixed order
+// (G groups of threads each add the splits z = g, g + G, ...; the G group
+// sums are then added in order), then apply the forward epilogue (affine,
+// ReLU, store, mask) or add the input gradient into the error window.
 template <typename T, bool DGRAD, int V>
-__global__ void conv_split_epilogue(ConvArgs a, int splits) {
+__global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int splits, int G) {
+  __shared__ float red[256 * 4];
   const int R = a.y1 - a.y0;
   const long long M = (long long)a.B * R * a.Wd;
   const long long MN = M * a.N;
   const long long drow = (long long)a.Wd * a.N;
-  GRID_STRIDE(i4, MN / V) {
-    const long long idx = i4 * V;
-    float val[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int z = 0; z < splits; ++z) {
+  const int epb = 256 / G;  // vectors per block
+  const int g = threadIdx.x / epb, e = threadIdx.x - g * epb;
+  const long long idx = ((long long)blockIdx.x * epb + e) * V;
+  float val[4] = {0.f, 0.f, 0.f, 0.f};
+  if (idx < MN) {
+    for (int z = g; z < splits; z += G) {
       float q[4];
       ldv<float, V>(a.part + z * MN + idx, q);
 #pragma unroll
-      for (int e = 0; e < V; ++e) val[e] += q[e];
+      for (int k = 0; k < V; ++k) val[k] += q[k];
     }
-    const int n = (int)(idx % a.N);
-    const long long m = idx / a.N;
-    const int x = (int)(m % a.Wd);
-    const long long t = m / a.Wd;
-    const int y = a.y0 + (int)(t % R);
-    const int b = (int)(t / R);
-    const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
-    if (DGRAD) {
-      float *d = (float *)a.dst.p + off;
-      float q[4];
-      ldv<float, V>(d, q);
+  }
 #pragma unroll
-      for (int e = 0; e < V; ++e) q[e] += val[e];
-      stv<float, V>(d, q);
-    } else {
+  for (int k = 0; k < V; ++k) red[(g * epb + e) * 4 + k] = val[k];
+  __syncthreads();
+  if (g != 0 || idx >= MN) return;
 #pragma unroll
-      for (int e = 0; e < V; ++e) {
-        if (a.scale) val[e] = val[e] * a.scale[n + e] + a.shift[n + e];
-        if (a.relu) val[e] = val[e] > 0.f ? val[e] : 0.f;
-        if (a.mask)
-          a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n + e] = val[e] > 0.f ? 1 : 0;
-      }
-      stv<T, V>((T *)a.dst.p + off, val);
+  for (int k = 0; k < V; ++k) val[k] = 0.f;
+  for (int gg = 0; gg < G; ++gg)
+#pragma unroll
+    for (int k = 0; k < V; ++k) val[k] += red[(gg * epb + e) * 4 + k];
+  const int n = (int)(idx % a.N);
+  const long long m = idx / a.N;
+  const int x = (int)(m % a.Wd);
+  const long long t = m / a.Wd;
+  const int y = a.y0 + (int)(t % R);
+  const int b = (int)(t / R);
+  const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
+  if (DGRAD) {
+    float *d = (float *)a.dst.p + off;
+    float q[4];
+    ldv<float, V>(d, q);
+#pragma unroll
+    for (int k = 0; k < V; ++k) q[k] += val[k];
+    stv<float, V>(d, q);
+  } else {
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      if (a.scale) val[k] = val[k] * a.scale[n + k] + a.shift[n + k];
+      if (a.relu) val[k] = val[k] > 0.f ? val[k] : 0.f;
+      if (a.mask)
+        a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n + k] = val[k] > 0.f ? 1 : 0;
     }
+    stv<T, V>((T *)a.dst.p + off, val);
   }
 }
 
@@ -898,10 +914,13 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   prof::end(pr, s);
   if (splits > 1) {
     int p2 = prof::begin("conv_split_epilogue", 0.0, s);
+    const int G = splits >= 8 ? 8 : splits >= 4 ? 4 : 2;
+    const long long vecs = a.N % 4 == 0 ? (long long)M * a.N / 4 : (long long)M * a.N;
+    const unsigned blocks = (unsigned)((vecs + 256 / G - 1) / (256 / G));
     if (a.N % 4 == 0)
-      conv_split_epilogue<T, DGRAD, 4><<<grid_for((long long)M * a.N / 4), 256, 0, s>>>(a, splits);
+      conv_split_epilogue<T, DGRAD, 4><<<blocks, 256, 0, s>>>(a, splits, G);
     else
-      conv_split_epilogue<T, DGRAD, 1><<<grid_for((long long)M * a.N), 256, 0, s>>>(a, splits);
+      conv_split_epilogue<T, DGRAD, 1><<<blocks, 256, 0, s>>>(a, splits, G);
     prof::end(p2, s);
   }
   return (int)hipGetLastError();
