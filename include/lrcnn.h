@@ -106,6 +106,13 @@ typedef struct {
                              /* every forward band evenly into bp_refine      */
                              /* bands, N_BP = N * bp_refine (the paper's finer */
                              /* BP granularity, Section III-C)                */
+  int32_t hybrid_from;       /* 0: every node row-centric. k in [2, n-1]: the  */
+                             /* hybrid variants (2PS-H / OverL-H, checkpoints  */
+                             /* integrated with row partitioning, Sections     */
+                             /* IV-A and IV-B): nodes 0..k-1 are row-centric,  */
+                             /* node k-1 is a checkpoint kept at full size,   */
+                             /* nodes k..n-1 run layer-wise over whole maps.  */
+                             /* No node >= k may read a node below k-1.        */
 } lrcnn_config;
 
 /* Opaque plan handle (host memory only). */
@@ -141,8 +148,9 @@ typedef struct {
  * Section IV-B). Pure host code; needs no GPU. `nodes`, `cfg` and
  * `cfg->bounds` are read during the call only. On success *out owns a plan
  * that the caller releases with lrcnn_plan_destroy.
- * Errors: EINVAL (null pointer, bad enum), ESHAPE (bad ids, channel or size
- * mismatch, a layer with empty output), EPARTITION (bad bounds). */
+ * Errors: EINVAL (null pointer, bad enum, a hybrid checkpoint that an edge
+ * crosses), ESHAPE (bad ids, channel or size mismatch, a layer with empty
+ * output), EPARTITION (bad bounds). */
 int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
                const lrcnn_config *cfg, lrcnn_plan_t **out);
 

@@ -73,6 +73,7 @@ struct Run {
   std::vector<int> first_consumer;
   hipStream_t side = nullptr;  // weight-gradient stream (backward only)
   bool wg_pending = false;     // a weight gradient on `side` not yet joined
+  bool dx_f32 = false;         // store dL/dx as float32 (a checkpoint's error)
 
   Run(Plan &p, const Layout &l, Sched s, void *wsp, const void *x_,
       const void *const *w_, const float *const *sc_, const float *const *sf_,
@@ -385,8 +386,8 @@ struct Run {
       int st = init_delta(r, n - 1);
       if (st != LRCNN_OK) return st;
       const Shape &s = P.shp[n - 1];
-      LAUNCH(launch_rows_copy(dt, DT_F32, full(const_cast<void *>(dy), n - 1), dlt[n - 1], 0, B,
-                              q.a, q.b, s.w, s.c, stream),
+      LAUNCH(launch_rows_copy(P.dy_f32 ? DT_F32 : dt, DT_F32, full(const_cast<void *>(dy), n - 1),
+                              dlt[n - 1], 0, B, q.a, q.b, s.w, s.c, stream),
              "seed error");
     }
     for (int v = n - 1; v >= 1; --v) {
@@ -432,7 +433,8 @@ struct Run {
         LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[0], acc, 1, B, q.lo, q.hi, s.w, s.c, stream),
                "input gradient accumulate");
       } else {
-        LAUNCH(launch_rows_copy(DT_F32, dt, dlt[0], full(dx, 0), 0, B, q.a, q.b, s.w, s.c, stream),
+        LAUNCH(launch_rows_copy(DT_F32, dx_f32 ? DT_F32 : dt, dlt[0], full(dx, 0), 0, B, q.a, q.b,
+                                s.w, s.c, stream),
                "input gradient store");
         if (sched == S_CARRY && r > 0 && q.a > q.lo) {
           View cv{ws + L.carry[0], (long long)L.carry_cap[0] * s.w * s.c, q.lo, s.w, s.c,
@@ -498,14 +500,16 @@ int check_params(const Plan &P, const void *x, const void *const *w, const float
   return LRCNN_OK;
 }
 
-int check_ws(const Layout &L, void *ws, size_t bytes) {
+int check_ws_bytes(size_t need, void *ws, size_t bytes) {
   if (!ws) return lrcnn_fail(LRCNN_EINVAL, "workspace is null");
   if (misaligned(ws)) return lrcnn_fail(LRCNN_EINVAL, "workspace is not 16-byte aligned");
-  if (bytes < L.total)
-    return lrcnn_fail(LRCNN_EWORKSPACE, "workspace needs " + std::to_string(L.total) +
+  if (bytes < need)
+    return lrcnn_fail(LRCNN_EWORKSPACE, "workspace needs " + std::to_string(need) +
                                             " bytes, got " + std::to_string(bytes));
   return LRCNN_OK;
 }
+
+int check_ws(const Layout &L, void *ws, size_t bytes) { return check_ws_bytes(L.total, ws, bytes); }
 
 int check_dw(const Plan &P, float *const *dw) {
   if (!dw) return lrcnn_fail(LRCNN_EINVAL, "dw array is null");
@@ -527,6 +531,53 @@ void release_side(Plan &P) {
   P.side_dev = -1;
 }
 
+namespace {
+
+// Hybrid depth (2PS-H / OverL-H): the row-centric part writes the
+// checkpoint map at full size; the layer-wise part reads it as its input.
+int hybrid_forward(Plan &P, const void *x, const void *const *w, const float *const *sc,
+                   const float *const *sf, void *y, char *ws, void *const *mask_out,
+                   void *stream) {
+  const int c = P.hyb - 1;
+  P.fwd_workspace = nullptr;
+  int st = lrcnn_forward_rows(reinterpret_cast<lrcnn_plan_t *>(P.row), x, w, sc, sf,
+                              ws + P.h_ck, ws, P.h_ck, mask_out, stream);
+  if (st != LRCNN_OK) return st;
+  Plan &C = *P.col;
+  Run run(C, C.lw, S_LAYERWISE, ws + P.h_col, ws + P.h_ck, w + c, sc ? sc + c : nullptr,
+          sf ? sf + c : nullptr, stream);
+  // the output map stays in the layer-wise part's window for the backward
+  if ((st = run.band_fwd(0, y, mask_out ? mask_out + c : nullptr, true, true)) != LRCNN_OK)
+    return st;
+  P.fwd_workspace = ws;
+  return LRCNN_OK;
+}
+
+// The layer-wise part's backward (its maps are still in place) gives the
+// checkpoint's float32 error, which seeds the row-centric part's backward.
+int hybrid_backward(Plan &P, const void *x, const void *const *w, const float *const *sc,
+                    const float *const *sf, const void *dy, float *const *dw, void *dx,
+                    char *ws, void *stream) {
+  const int c = P.hyb - 1;
+  if (P.fwd_workspace != ws)
+    return lrcnn_fail(LRCNN_ESTATE,
+                      "hybrid backward needs a preceding lrcnn_forward_rows on this plan and "
+                      "workspace");
+  Plan &C = *P.col;
+  Run run(C, C.lw, S_LAYERWISE, ws + P.h_col, ws + P.h_ck, w + c, sc ? sc + c : nullptr,
+          sf ? sf + c : nullptr, stream);
+  run.dx_f32 = true;
+  if (!g_dry && ensure_side(C)) run.side = (hipStream_t)C.side_stream;
+  int st;
+  if ((st = run.band_fwd(0, nullptr, nullptr, true, false, true)) != LRCNN_OK) return st;
+  if ((st = run.zero_dw(dw + c)) != LRCNN_OK) return st;
+  if ((st = run.band_bwd(0, dy, dw + c, ws + P.h_dck, nullptr)) != LRCNN_OK) return st;
+  if ((st = run.finish_dw(dw + c)) != LRCNN_OK) return st;
+  return lrcnn_backward_rows(reinterpret_cast<lrcnn_plan_t *>(P.row), x, w, sc, sf,
+                             ws + P.h_dck, dw, dx, ws, P.h_ck, stream);
+}
+
+}  // namespace
 }  // namespace lrcnn
 
 using namespace lrcnn;
@@ -540,6 +591,10 @@ extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void 
   int st = check_params(P, x, w, aff_scale, aff_shift);
   if (st != LRCNN_OK) return st;
   if (!y || misaligned(y)) return lrcnn_fail(LRCNN_EINVAL, "y null or misaligned");
+  if (P.hyb) {
+    if ((st = check_ws_bytes(P.h_total, workspace, ws_bytes)) != LRCNN_OK) return st;
+    return hybrid_forward(P, x, w, aff_scale, aff_shift, y, (char *)workspace, mask_out, stream);
+  }
   if ((st = check_ws(P.rc, workspace, ws_bytes)) != LRCNN_OK) return st;
   Run run(P, P.rc, P.cfg.mode == LRCNN_CARRY ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale,
           aff_shift, stream);
@@ -547,7 +602,7 @@ extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void 
   P.last_band_kept = false;
   // the last band's maps can serve the BP only when both passes use the
   // same partition
-  const bool keep = P.refine == 1;
+  const bool keep = P.refine == 1 && !P.no_keep;
   for (int r = 0; r < P.nb_fp; ++r)
     if ((st = run.band_fwd(r, y, mask_out, false, keep && r == P.nb_fp - 1)) != LRCNN_OK)
       return st;
@@ -568,6 +623,10 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
   if (!dy || misaligned(dy)) return lrcnn_fail(LRCNN_EINVAL, "dy null or misaligned");
   if (dx && misaligned(dx)) return lrcnn_fail(LRCNN_EINVAL, "dx misaligned");
   if ((st = check_dw(P, dw)) != LRCNN_OK) return st;
+  if (P.hyb) {
+    if ((st = check_ws_bytes(P.h_total, workspace, ws_bytes)) != LRCNN_OK) return st;
+    return hybrid_backward(P, x, w, aff_scale, aff_shift, dy, dw, dx, (char *)workspace, stream);
+  }
   if ((st = check_ws(P.rc, workspace, ws_bytes)) != LRCNN_OK) return st;
   const bool carry = P.cfg.mode == LRCNN_CARRY;
   if (carry && P.fwd_workspace != workspace)

@@ -208,6 +208,9 @@ static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
     return lrcnn_fail(LRCNN_EINVAL, "EXPLICIT policy needs bounds");
   if (cfg->bp_refine < 0 || cfg->bp_refine > 64)
     return lrcnn_fail(LRCNN_EINVAL, "bp_refine must be in [0, 64]");
+  if (cfg->hybrid_from < 0 || cfg->hybrid_from == 1 ||
+      (cfg->hybrid_from > 0 && cfg->hybrid_from > n - 1))
+    return lrcnn_fail(LRCNN_EINVAL, "hybrid_from must be 0 or in [2, n_nodes - 1]");
   for (int v = 1; v < n; ++v) {
     const lrcnn_node &d = nodes[v];
     std::string at = "node " + std::to_string(v) + ": ";
@@ -343,10 +346,11 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   L.part_bytes = part;
   L.part = A.take(part);
   const size_t ubase = A.top;
+  L.ubase = ubase;
   // --- backward region (also the forward windows unless packed)
   size_t c0 = A.top;
   for (int v = 1; v < n; ++v) {
-    if (layerwise && v == n - 1) continue;  // the output node lives in y
+    if (layerwise && v == n - 1 && !P.lw_keep_out) continue;  // the output lives in y
     L.win[v] = A.take(P.elems(v, cap[v]) * P.es);
   }
   L.cache_bytes = A.top - c0;
@@ -549,6 +553,71 @@ static int build(Plan &P) {
 
 using lrcnn::Plan;
 
+namespace lrcnn {
+
+// Hybrid depth (2PS-H / OverL-H): a checkpoint at node c = hyb - 1 splits
+// the network into a row-centric part (nodes 0..c) and a layer-wise part
+// (nodes hyb..n-1, which read c as their input). Built as two sub-plans.
+static int build_hybrid(Plan &P) {
+  const int k = P.cfg.hybrid_from, c = k - 1, n = P.n;
+  for (int v = k; v < n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.in0 < c || (d.op == LRCNN_OP_ADD && d.in1 < c))
+      return lrcnn_fail(LRCNN_EINVAL, "hybrid checkpoint at node " + std::to_string(c) +
+                                          " is crossed by an edge into node " +
+                                          std::to_string(v));
+  }
+  auto sub = [&](std::vector<lrcnn_node> nodes, const lrcnn_config &cfg, Plan *&out) -> int {
+    Plan *Q = new (std::nothrow) Plan();
+    if (!Q) return lrcnn_fail(LRCNN_EINVAL, "out of host memory");
+    Q->nodes = std::move(nodes);
+    Q->cfg = cfg;
+    Q->n = (int)Q->nodes.size();
+    Q->es = P.es;
+    out = Q;
+    return LRCNN_OK;
+  };
+  lrcnn_config rc = P.cfg;
+  rc.hybrid_from = 0;
+  std::vector<lrcnn_node> rn(P.nodes.begin(), P.nodes.begin() + k);
+  int st = sub(rn, rc, P.row);
+  if (st != LRCNN_OK) return st;
+  P.row->no_keep = true;
+  P.row->dy_f32 = true;
+  st = build(*P.row);
+  P.row->cfg.bounds = nullptr;
+  if (st != LRCNN_OK) return st;
+  lrcnn_config cc = P.cfg;
+  cc.hybrid_from = 0;
+  cc.in_c = P.shp[c].c, cc.in_h = P.shp[c].h, cc.in_w = P.shp[c].w;
+  cc.mode = LRCNN_CARRY;
+  cc.n_bands = 1;
+  cc.policy = LRCNN_EVEN;
+  cc.bounds = nullptr;
+  cc.bp_refine = 1;
+  std::vector<lrcnn_node> cn(1 + n - k);
+  cn[0] = P.nodes[0];
+  for (int v = k; v < n; ++v) {
+    lrcnn_node d = P.nodes[v];
+    d.in0 -= c;
+    if (d.op == LRCNN_OP_ADD) d.in1 -= c;
+    cn[v - c] = d;
+  }
+  if ((st = sub(cn, cc, P.col)) != LRCNN_OK) return st;
+  P.col->lw_keep_out = true;
+  if ((st = build(*P.col)) != LRCNN_OK) return st;
+  P.hyb = k;
+  P.h_col = P.row->rc.ubase;
+  const size_t top = std::max(P.row->rc.total, P.h_col + P.col->lw.total);
+  P.h_ck = align256(top);
+  P.h_dck = align256(P.h_ck + P.elems(c, P.shp[c].h) * P.es);
+  P.h_total = align256(P.h_dck + P.elems(c, P.shp[c].h) * 4);
+  P.flops_rows = P.row->flops_rows + 3.0 * P.col->tau;
+  return LRCNN_OK;
+}
+
+}  // namespace lrcnn
+
 extern "C" int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
                           const lrcnn_config *cfg, lrcnn_plan_t **out) {
   if (!out) return lrcnn_fail(LRCNN_EINVAL, "null output pointer");
@@ -567,6 +636,7 @@ extern "C" int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
     P->cfg.bounds = cfg->bounds;
   }
   st = lrcnn::build(*P);
+  if (st == LRCNN_OK && cfg->hybrid_from > 0) st = lrcnn::build_hybrid(*P);
   P->cfg.bounds = nullptr;
   if (st != LRCNN_OK) {
     delete P;
@@ -581,15 +651,15 @@ extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info)
   const Plan &P = *reinterpret_cast<const Plan *>(plan);
   std::memset(info, 0, sizeof(*info));
   info->n_nodes = P.n;
-  info->n_bands = P.nb_fp;
-  info->bp_bands = P.nb;
+  info->n_bands = P.hyb ? P.row->nb_fp : P.nb_fp;
+  info->bp_bands = P.hyb ? P.row->nb : P.nb;
   info->fp_window_bytes = P.rc.fp_packed ? P.rc.fwin_bytes : P.rc.cache_bytes;
   info->mode = P.cfg.mode;
   info->dtype = P.cfg.dtype;
   info->out_h = P.shp[P.n - 1].h;
   info->out_w = P.shp[P.n - 1].w;
   info->out_c = P.shp[P.n - 1].c;
-  info->workspace_bytes = P.rc.total;
+  info->workspace_bytes = P.hyb ? P.h_total : P.rc.total;
   info->layerwise_workspace_bytes = P.lw.total;
   info->strip_bytes = P.rc.strip_bytes;
   info->band_cache_bytes = P.rc.cache_bytes;
@@ -602,7 +672,18 @@ extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info)
   info->omega_bytes = omega;
   info->omega_fp_bytes = (double)P.rc.strip_bytes + P.rc.part_bytes +
                          (P.rc.fp_packed ? P.rc.fwin_bytes : P.rc.cache_bytes) + ybytes;
-  info->omega_bp_bytes = (double)P.rc.total + ybytes;
+  info->omega_bp_bytes = (double)(P.hyb ? P.h_total : P.rc.total) + ybytes;
+  if (P.hyb) {
+    // the row part's figures; the layer-wise part keeps whole maps
+    const Plan &R = *P.row;
+    info->strip_bytes = R.rc.strip_bytes;
+    info->band_cache_bytes = R.rc.cache_bytes;
+    info->delta_bytes = R.rc.delta_bytes;
+    info->carry_bytes = R.rc.carry_bytes;
+    info->partial_bytes = R.rc.part_bytes;
+    info->fp_window_bytes = R.rc.fp_packed ? R.rc.fwin_bytes : R.rc.cache_bytes;
+    info->omega_fp_bytes = (double)P.h_total + ybytes;
+  }
   info->flops_tau = P.tau;
   info->flops_rows = P.flops_rows;
   info->flops_layerwise = 3.0 * P.tau;
@@ -629,7 +710,19 @@ extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int
   const int nbands = phase == 0 ? P.nb_fp : P.nb;
   if (node < 0 || node >= P.n || band < 0 || band >= nbands || (phase != 0 && phase != 1))
     return lrcnn_fail(LRCNN_EINVAL, "phase, band or node out of range");
-  const lrcnn::Rows &q = phase == 0 ? P.rows_fp[band][node] : P.rows[band][node];
+  lrcnn::Rows q = phase == 0 ? P.rows_fp[band][node] : P.rows[band][node];
+  if (P.hyb) {
+    // hybrid: the row part's bands; layer-wise nodes are whole in band 0
+    if (node < P.hyb) {
+      const Plan &R = *P.row;
+      const int rb = phase == 0 ? R.nb_fp : R.nb;
+      if (band >= rb) return lrcnn_fail(LRCNN_EINVAL, "band out of range");
+      q = phase == 0 ? R.rows_fp[band][node] : R.rows[band][node];
+    } else {
+      const int h = band == 0 ? P.shp[node].h : 0;
+      q = lrcnn::Rows{0, h, 0, h};
+    }
+  }
   rows[0] = q.a;
   rows[1] = q.b;
   rows[2] = q.lo;
@@ -640,6 +733,8 @@ extern "C" int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int
 extern "C" void lrcnn_plan_destroy(lrcnn_plan_t *plan) {
   if (!plan) return;
   Plan *p = reinterpret_cast<Plan *>(plan);
+  if (p->row) release_side(*p->row);
+  if (p->col) release_side(*p->col);
   release_side(*p);
   delete p;
 }

@@ -24,6 +24,7 @@ struct Rows {
 // Byte offsets of every buffer inside one workspace.
 struct Layout {
   size_t total = 0;
+  size_t ubase = 0;              // start of the region FP and BP share
   std::vector<size_t> win;       // per node: feature-map window ([B][cap][W][C])
   std::vector<int> win_cap;      // rows of each window
   std::vector<size_t> argmax;    // per MAXPOOL node: uint8 argmax of own rows
@@ -77,6 +78,22 @@ struct Plan {
   // first use for the device current at that call (opaque HIP handles)
   void *side_stream = nullptr, *ev_act = nullptr, *ev_wg = nullptr;
   int side_dev = -1;
+  // hybrid depth: nodes < hyb row-centric (sub-plan `row`, nodes 0..hyb-1),
+  // nodes >= hyb layer-wise (sub-plan `col`, re-indexed from the checkpoint
+  // node hyb-1 as its input). Workspace: the row part's layout; the column
+  // part's layer-wise layout overlays the row part's shared FP/BP region
+  // (idle between the two parts); then the checkpoint map (storage dtype)
+  // and its float32 error.
+  int hyb = 0;
+  Plan *row = nullptr, *col = nullptr;
+  size_t h_col = 0, h_ck = 0, h_dck = 0, h_total = 0;
+  bool no_keep = false;      // FP must not leave its last band for BP
+  bool dy_f32 = false;       // dL/dy is float32 (a checkpoint's error)
+  bool lw_keep_out = false;  // layer-wise layout keeps the output node's map
+  ~Plan() {
+    delete row;
+    delete col;
+  }
 
   size_t elems(int v, int rows_) const {
     return (size_t)cfg.batch * rows_ * shp[v].w * shp[v].c;

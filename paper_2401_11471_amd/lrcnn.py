@@ -44,7 +44,8 @@ class Config(C.Structure):
     _fields_ = [("batch", C.c_int32), ("in_c", C.c_int32), ("in_h", C.c_int32),
                 ("in_w", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
                 ("n_bands", C.c_int32), ("policy", C.c_int32),
-                ("bounds", C.POINTER(C.c_int32)), ("bp_refine", C.c_int32)]
+                ("bounds", C.POINTER(C.c_int32)), ("bp_refine", C.c_int32),
+                ("hybrid_from", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
@@ -147,9 +148,10 @@ class Plan:
 
 
 def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
-               policy=EVEN, bounds=None, bp_refine=1):
+               policy=EVEN, bounds=None, bp_refine=1, hybrid_from=0):
     arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
-    cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None, bp_refine)
+    cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None, bp_refine,
+                 hybrid_from)
     keep = None
     if bounds is not None:
         keep = (C.c_int32 * len(bounds))(*bounds)

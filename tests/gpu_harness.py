@@ -22,14 +22,24 @@ def has_mask(nd):
     return (nd[0] in (L.OP_CONV, L.OP_ADD) and nd[11]) or nd[0] == L.OP_MAXPOOL
 
 
+def hybrid_cuts(nodes):
+    """hybrid_from values whose checkpoint (node k - 1) no edge crosses."""
+    n = len(nodes)
+    return [k for k in range(2, n)
+            if all(nodes[v][1] >= k - 1 and (nodes[v][0] != L.OP_ADD or nodes[v][2] >= k - 1)
+                   for v in range(k, n))]
+
+
 def rel(a, b):
     return float(np.max(np.abs(a - b)) / max(float(np.max(np.abs(b))), 1e-30))
 
 
 def gpu_run(nodes, inp, mode=L.CARRY, nb=1, policy=L.EVEN, bounds=None,
-            layerwise=False, want_dx=True, masks=True, repeat_bwd=1, bp_refine=1):
+            layerwise=False, want_dx=True, masks=True, repeat_bwd=1, bp_refine=1,
+            hybrid_from=0):
     b, h, w, c = inp.x.shape
-    plan = L.lrcnn_plan(nodes, b, c, h, w, inp.dtype, mode, nb, policy, bounds, bp_refine)
+    plan = L.lrcnn_plan(nodes, b, c, h, w, inp.dtype, mode, nb, policy, bounds, bp_refine,
+                        hybrid_from)
     info = plan.info()
     dm = DeviceModel.from_inputs(nodes, inp)
     out_shape = (b,) + plan.node_shape(len(nodes) - 1)

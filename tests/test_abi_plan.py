@@ -251,8 +251,9 @@ class _Fake:
 
 
 def dry_run(nodes, batch, h, w, dtype, mode, nb, policy=L.EVEN, bounds=None,
-            dx=True, bp_refine=1):
-    p = L.lrcnn_plan(nodes, batch, 3, h, w, dtype, mode, nb, policy, bounds, bp_refine)
+            dx=True, bp_refine=1, hybrid_from=0):
+    p = L.lrcnn_plan(nodes, batch, 3, h, w, dtype, mode, nb, policy, bounds, bp_refine,
+                     hybrid_from)
     f = _Fake(1 << 30)
     per = [None] + [f if nd[0] == L.OP_CONV else None for nd in nodes[1:]]
     aff = [None] + [f if (nd[0] == L.OP_CONV and nd[10]) else None for nd in nodes[1:]]
@@ -329,3 +330,58 @@ def test_finer_backward_bands_cut_memory_on_vgg():
     assert two["workspace_bytes"] < one["workspace_bytes"]
     assert two["band_cache_bytes"] < one["band_cache_bytes"]
     assert two["layerwise_workspace_bytes"] > 3 * two["workspace_bytes"]
+
+
+def _cuts(nodes):
+    n = len(nodes)
+    return [k for k in range(2, n)
+            if all(nodes[v][1] >= k - 1 and (nodes[v][0] != L.OP_ADD or nodes[v][2] >= k - 1)
+                   for v in range(k, n))]
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("mode", ["carry", "recompute"])
+def test_hybrid_depth_dry_run(cid, mode):
+    # every valid checkpoint of every workload plans and runs through the
+    # executor's host checks; the workspace is at most the row part's plus
+    # the layer-wise part's and the checkpoint's
+    c = CONFIGS[cid]
+    nodes = net_nodes(c["net"])
+    m = L.RECOMPUTE if mode == "recompute" else L.CARRY
+    cuts = _cuts(nodes)
+    assert cuts
+    for k in cuts[:: max(1, len(cuts) // 4)]:
+        p = dry_run(nodes, c["batch"], c["h"], c["w"], c["dtype"], m, c["bands"], hybrid_from=k)
+        info = p.info()
+        rp = L.lrcnn_plan(nodes[:k], c["batch"], 3, c["h"], c["w"], c["dtype"], m, c["bands"])
+        assert info["workspace_bytes"] >= rp.info()["workspace_bytes"]
+        # layer-wise nodes are whole in band 0 and empty after it
+        a, b, lo, hi = p.band_rows(0, len(nodes) - 1)
+        assert (a, b) == (0, p.node_shape(len(nodes) - 1)[0])
+        if info["n_bands"] > 1:
+            assert p.band_rows(1, len(nodes) - 1)[:2] == (0, 0)
+        # the row part's nodes keep the row part's bands
+        assert p.band_rows(0, k - 1) == rp.band_rows(0, k - 1)
+
+
+def test_hybrid_depth_errors():
+    nodes = resnet50_net()
+    good = set(_cuts(nodes))
+    bad = next(k for k in range(2, len(nodes)) if k not in good)
+    for k in (1, -1, len(nodes), bad):
+        with pytest.raises(L.LrcnnError) as e:
+            L.lrcnn_plan(nodes, 2, 3, 64, 64, L.F32, L.CARRY, 2, hybrid_from=k)
+        assert "EINVAL" in str(e.value)
+
+
+def test_hybrid_cuts_vgg_flops_and_memory():
+    # a checkpoint after pool3 runs conv4/conv5 layer-wise: less recompute
+    # than the all-row-centric plan, and a smaller workspace at 4 bands
+    c = CONFIGS[2]
+    nodes = vgg16_net()
+    full = L.lrcnn_plan(nodes, c["batch"], 3, c["h"], c["w"], c["dtype"], L.CARRY, 4).info()
+    hy = L.lrcnn_plan(nodes, c["batch"], 3, c["h"], c["w"], c["dtype"], L.CARRY, 4,
+                      hybrid_from=11).info()
+    assert hy["flops_rows"] < full["flops_rows"]
+    assert hy["workspace_bytes"] < full["workspace_bytes"]
+    assert hy["flops_layerwise"] == full["flops_layerwise"]

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import assert_parity, gpu_run, rel
+from gpu_harness import assert_parity, gpu_run, hybrid_cuts, rel
 from paper_2401_11471_amd import lrcnn as L
 from workloads import NetBuilder, Inputs, config_inputs, tiny_net, F32, BF16
 
@@ -114,6 +114,35 @@ def test_finer_backward_partition_parity(name, dtype, mode):
     nodes, inp = _inputs(name, dtype, seed=15)
     gpu = gpu_run(nodes, inp, mode, 3, bp_refine=3)
     assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", ["vgg_like", "odd", "resnet_like"])
+@pytest.mark.parametrize("mode", [L.CARRY, L.RECOMPUTE])
+@pytest.mark.parametrize("where", ["early", "late"])
+def test_hybrid_depth_parity(name, dtype, mode, where):
+    # 2PS-H / OverL-H: row-centric up to a checkpoint, layer-wise after it
+    nodes, inp = _inputs(name, dtype, seed=17)
+    cuts = hybrid_cuts(nodes)
+    k = cuts[0] if where == "early" else cuts[-1]
+    print(f"hybrid {name} dtype={dtype} mode={mode} hybrid_from={k}", flush=True)
+    gpu = gpu_run(nodes, inp, mode, 3, hybrid_from=k)
+    assert_parity(nodes, inp, gpu)
+
+
+@pytest.mark.parametrize("name", ["vgg_like", "resnet_like"])
+def test_hybrid_matches_row_centric_float32(name):
+    # the checkpoint's error enters the row part in float32, so the hybrid
+    # step equals the all-row-centric step to rounding
+    nodes, inp = _inputs(name, F32, seed=19)
+    ref = gpu_run(nodes, inp, L.CARRY, 4)
+    for k in hybrid_cuts(nodes):
+        hy = gpu_run(nodes, inp, L.CARRY, 4, hybrid_from=k)
+        assert rel(hy["y"], ref["y"]) < 1e-5, k
+        assert rel(hy["dx"], ref["dx"]) < 1e-4, k
+        for v, (a, b) in enumerate(zip(hy["dw"], ref["dw"])):
+            if b is not None:
+                assert rel(a, b) < 1e-4, (k, v)
 
 
 @pytest.mark.parametrize("dtype", [F32, BF16])
