@@ -41,6 +41,9 @@ def parse():
     ap.add_argument("--bp-refine", type=int, default=1,
                     help="backward bands per forward band (finer BP partition)")
     ap.add_argument("--batch", type=int, default=0, help="override the batch")
+    ap.add_argument("--hybrid-from", type=int, default=0,
+                    help="hybrid depth: first node run layer-wise (-1: the planner's "
+                         "smallest-workspace checkpoint; 0: all row-centric)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the layer-wise / recompute comparison runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -158,7 +161,7 @@ def main():
     dts = "bf16" if inp.dtype == BF16 else "f32"
 
     plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy,
-                        bp_refine=args.bp_refine)
+                        bp_refine=args.bp_refine, hybrid_from=args.hybrid_from)
     info = plan.info()
     dm = DeviceModel.from_inputs(nodes, inp)
     out_shape = (B,) + plan.node_shape(len(nodes) - 1)
@@ -241,7 +244,7 @@ def main():
         "dtype": dts, "data": "synthetic N(0,1), paper's shapes (ImageNet not available)",
         "config": {"workload": c["name"], "net": c["net"], "batch": B,
                    "input": [Cin, H, W], "bands": nb, "bp_bands": info["bp_bands"],
-                   "mode": args.mode, "dx": False,
+                   "mode": args.mode, "dx": False, "hybrid_from": info["hybrid_from"],
                    "launch": "host" if args.eager else "hip-graph"},
         "roofline": roofline,
         "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),
@@ -308,6 +311,34 @@ def main():
             out["finer_backward_bands"] = ent
             del fb
             torch.cuda.empty_cache()
+        if args.hybrid_from == 0:
+            # hybrid depth (2PS-H / OverL-H) at the planner's checkpoint
+            hplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy,
+                                 bp_refine=args.bp_refine, hybrid_from=L.HYBRID_AUTO)
+            hinfo = hplan.info()
+            if hinfo["hybrid_from"]:
+                def h_alloc():
+                    return dict(ws=dm.workspace(hinfo["workspace_bytes"]), y=dm.empty(out_shape))
+
+                def h_step(b):
+                    L.lrcnn_forward_rows(hplan, dm.x, dm.w, dm.sc, dm.sf, b["y"], b["ws"])
+                    L.lrcnn_backward_rows(hplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None,
+                                          b["ws"])
+                peak_h, hb = measure(h_alloc, h_step)
+                h_ms, _, g_ = timed_steps(torch, lambda: h_step(hb), args.steps, args.warmup,
+                                          args.eager)
+                del g_
+                ent = {"hybrid_from": hinfo["hybrid_from"],
+                       "images_per_s": round(B * 1000.0 / h_ms, 3),
+                       "ms_per_step": round(h_ms, 3), "peak_act_bytes": int(peak_h),
+                       "flops_over_layerwise": round(hinfo["flops_rows"] /
+                                                     hinfo["flops_layerwise"], 3)}
+                if "peak_act_bytes" in out.get("layerwise", {}):
+                    ent["mem_ratio_layerwise_over_rows"] = round(
+                        out["layerwise"]["peak_act_bytes"] / peak_h, 3)
+                out["hybrid_depth"] = ent
+                del hb
+                torch.cuda.empty_cache()
         if mode == L.CARRY:
             rplan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.RECOMPUTE, nb,
                                  bp_refine=args.bp_refine)

@@ -94,6 +94,7 @@ enum { LRCNN_CARRY = 0, LRCNN_RECOMPUTE = 1 };
  *   EXPLICIT  the caller's `bounds` (n_bands + 1 non-decreasing values from
  *             0 to the partitioned height; empty bands are allowed)       */
 enum { LRCNN_EVEN = 0, LRCNN_BALANCED = 1, LRCNN_EXPLICIT = 2 };
+enum { LRCNN_HYBRID_AUTO = -1 };
 
 typedef struct {
   int32_t batch, in_c, in_h, in_w;
@@ -113,6 +114,9 @@ typedef struct {
                              /* node k-1 is a checkpoint kept at full size,   */
                              /* nodes k..n-1 run layer-wise over whole maps.  */
                              /* No node >= k may read a node below k-1.        */
+                             /* LRCNN_HYBRID_AUTO (-1): the planner takes the  */
+                             /* valid k with the smallest workspace (0 if no   */
+                             /* checkpoint beats the all-row-centric plan).    */
 } lrcnn_config;
 
 /* Opaque plan handle (host memory only). */
@@ -141,6 +145,8 @@ typedef struct {
   int32_t bp_bands;                /* backward bands (n_bands * bp_refine)  */
   size_t fp_window_bytes;          /* forward windows (lifetime-packed when */
                                    /* bp_refine > 1, else the band cache)   */
+  int32_t hybrid_from;             /* the checkpoint in use (0: none); the  */
+                                   /* planner's choice for LRCNN_HYBRID_AUTO */
 } lrcnn_plan_info;
 
 /* Build a plan: shapes of every node, per-band row intervals, workspace

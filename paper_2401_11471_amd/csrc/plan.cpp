@@ -208,7 +208,7 @@ static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
     return lrcnn_fail(LRCNN_EINVAL, "EXPLICIT policy needs bounds");
   if (cfg->bp_refine < 0 || cfg->bp_refine > 64)
     return lrcnn_fail(LRCNN_EINVAL, "bp_refine must be in [0, 64]");
-  if (cfg->hybrid_from < 0 || cfg->hybrid_from == 1 ||
+  if (cfg->hybrid_from < LRCNN_HYBRID_AUTO || cfg->hybrid_from == 1 ||
       (cfg->hybrid_from > 0 && cfg->hybrid_from > n - 1))
     return lrcnn_fail(LRCNN_EINVAL, "hybrid_from must be 0 or in [2, n_nodes - 1]");
   for (int v = 1; v < n; ++v) {
@@ -558,14 +558,16 @@ namespace lrcnn {
 // Hybrid depth (2PS-H / OverL-H): a checkpoint at node c = hyb - 1 splits
 // the network into a row-centric part (nodes 0..c) and a layer-wise part
 // (nodes hyb..n-1, which read c as their input). Built as two sub-plans.
-static int build_hybrid(Plan &P) {
+static int build_hybrid(Plan &P, bool quiet = false) {
   const int k = P.cfg.hybrid_from, c = k - 1, n = P.n;
   for (int v = k; v < n; ++v) {
     const lrcnn_node &d = P.nodes[v];
-    if (d.in0 < c || (d.op == LRCNN_OP_ADD && d.in1 < c))
+    if (d.in0 < c || (d.op == LRCNN_OP_ADD && d.in1 < c)) {
+      if (quiet) return LRCNN_EINVAL;
       return lrcnn_fail(LRCNN_EINVAL, "hybrid checkpoint at node " + std::to_string(c) +
                                           " is crossed by an edge into node " +
                                           std::to_string(v));
+    }
   }
   auto sub = [&](std::vector<lrcnn_node> nodes, const lrcnn_config &cfg, Plan *&out) -> int {
     Plan *Q = new (std::nothrow) Plan();
@@ -636,7 +638,28 @@ extern "C" int lrcnn_plan(const lrcnn_node *nodes, int32_t n_nodes,
     P->cfg.bounds = cfg->bounds;
   }
   st = lrcnn::build(*P);
-  if (st == LRCNN_OK && cfg->hybrid_from > 0) st = lrcnn::build_hybrid(*P);
+  if (st == LRCNN_OK && cfg->hybrid_from == LRCNN_HYBRID_AUTO) {
+    // budget-driven choice of the checkpoint: the smallest workspace over
+    // every valid cut (each is planned on a scratch copy), none if no cut
+    // beats the all-row-centric plan
+    int best = 0;
+    size_t best_ws = P->rc.total;
+    for (int k = 2; k < n_nodes; ++k) {
+      Plan Q;
+      Q.nodes = P->nodes;
+      Q.cfg = P->cfg;
+      Q.cfg.hybrid_from = k;
+      Q.n = P->n;
+      Q.es = P->es;
+      if (lrcnn::build(Q) != LRCNN_OK || lrcnn::build_hybrid(Q, true) != LRCNN_OK) continue;
+      if (Q.h_total < best_ws) {
+        best_ws = Q.h_total;
+        best = k;
+      }
+    }
+    P->cfg.hybrid_from = best;
+  }
+  if (st == LRCNN_OK && P->cfg.hybrid_from > 0) st = lrcnn::build_hybrid(*P);
   P->cfg.bounds = nullptr;
   if (st != LRCNN_OK) {
     delete P;
@@ -651,6 +674,7 @@ extern "C" int lrcnn_plan_query(const lrcnn_plan_t *plan, lrcnn_plan_info *info)
   const Plan &P = *reinterpret_cast<const Plan *>(plan);
   std::memset(info, 0, sizeof(*info));
   info->n_nodes = P.n;
+  info->hybrid_from = P.hyb;
   info->n_bands = P.hyb ? P.row->nb_fp : P.nb_fp;
   info->bp_bands = P.hyb ? P.row->nb : P.nb;
   info->fp_window_bytes = P.rc.fp_packed ? P.rc.fwin_bytes : P.rc.cache_bytes;

@@ -23,6 +23,7 @@ OP_INPUT, OP_CONV, OP_MAXPOOL, OP_ADD = 0, 1, 2, 3
 F32, BF16 = 0, 1
 CARRY, RECOMPUTE = 0, 1
 EVEN, BALANCED, EXPLICIT = 0, 1, 2
+HYBRID_AUTO = -1
 
 STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EPARTITION",
           -4: "EWORKSPACE", -5: "ESTATE", -6: "EDTYPE", -7: "EHIP",
@@ -60,7 +61,8 @@ class PlanInfo(C.Structure):
                 ("omega_bp_bytes", C.c_double), ("flops_tau", C.c_double),
                 ("flops_rows", C.c_double), ("flops_layerwise", C.c_double),
                 ("shared_rows", C.c_int64), ("halo_rows", C.c_int64),
-                ("bp_bands", C.c_int32), ("fp_window_bytes", C.c_size_t)]
+                ("bp_bands", C.c_int32), ("fp_window_bytes", C.c_size_t),
+                ("hybrid_from", C.c_int32)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

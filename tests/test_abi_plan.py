@@ -368,7 +368,7 @@ def test_hybrid_depth_errors():
     nodes = resnet50_net()
     good = set(_cuts(nodes))
     bad = next(k for k in range(2, len(nodes)) if k not in good)
-    for k in (1, -1, len(nodes), bad):
+    for k in (1, -2, len(nodes), bad):
         with pytest.raises(L.LrcnnError) as e:
             L.lrcnn_plan(nodes, 2, 3, 64, 64, L.F32, L.CARRY, 2, hybrid_from=k)
         assert "EINVAL" in str(e.value)
@@ -385,3 +385,19 @@ def test_hybrid_cuts_vgg_flops_and_memory():
     assert hy["flops_rows"] < full["flops_rows"]
     assert hy["workspace_bytes"] < full["workspace_bytes"]
     assert hy["flops_layerwise"] == full["flops_layerwise"]
+
+
+@pytest.mark.parametrize("cid", [2, 3, 5])
+def test_hybrid_auto_picks_the_smallest_workspace(cid):
+    # budget-driven placement: the planner's checkpoint is a valid cut whose
+    # workspace is the minimum over every cut and the all-row-centric plan
+    c = CONFIGS[cid]
+    nodes = net_nodes(c["net"])
+    args = (nodes, c["batch"], 3, c["h"], c["w"], c["dtype"], L.CARRY, c["bands"])
+    auto = L.lrcnn_plan(*args, hybrid_from=L.HYBRID_AUTO).info()
+    sizes = {0: L.lrcnn_plan(*args).info()["workspace_bytes"]}
+    for k in _cuts(nodes):
+        sizes[k] = L.lrcnn_plan(*args, hybrid_from=k).info()["workspace_bytes"]
+    assert auto["hybrid_from"] in sizes
+    assert auto["workspace_bytes"] == min(sizes.values())
+    assert auto["workspace_bytes"] == sizes[auto["hybrid_from"]]
