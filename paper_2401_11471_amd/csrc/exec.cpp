@@ -4,6 +4,7 @@
 // lrcnn_layerwise_reference_gpu (Algorithm 1 and its column baseline).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -185,11 +186,39 @@ struct Run {
   // pool argmax bytes are recorded), so BP can skip recomputing this band.
   // `views_only`: set the band's views without launching anything (the
   // maps are already in place).
+  // Copies of one band's strips. Unless the forward windows are packed by
+  // lifetime, every node has a window of its own, so all strip loads of a
+  // band can run in one launch before its first node and all strip stores
+  // in one launch after its last; otherwise each copy runs at its node.
+  int flush_copies(std::vector<CopySeg> &segs, const char *what) {
+    for (size_t i = 0; i < segs.size(); i += kMaxCopySegs) {
+      const int cnt = (int)std::min<size_t>(kMaxCopySegs, segs.size() - i);
+      LAUNCH(launch_rows_copy_batch(dt, segs.data() + i, cnt, stream), what);
+    }
+    segs.clear();
+    return LRCNN_OK;
+  }
+  int strip_copy(bool batch, std::vector<CopySeg> &segs, View src, View dst, int r0, int r1,
+                 int v, const char *what) {
+    if (batch) {
+      segs.push_back(CopySeg{src, dst, P.cfg.batch, r0, r1, P.shp[v].w, P.shp[v].c});
+      return LRCNN_OK;
+    }
+    LAUNCH(launch_rows_copy(dt, dt, src, dst, 0, P.cfg.batch, r0, r1, P.shp[v].w, P.shp[v].c,
+                            stream),
+           what);
+    return LRCNN_OK;
+  }
+
   int band_fwd(int r, void *y, void *const *mask_out, bool bp, bool keep = false,
                bool views_only = false) {
     const int n = P.n;
     const bool fp = !bp && sched != S_LAYERWISE;
     const bool packed = fp && L.fp_packed;
+    const bool batch = !packed;
+    std::vector<CopySeg> segs;
+    int st;
+    // views of every node's rows, and the strip loads
     for (int v = 1; v < n; ++v) {
       const Rows q = fp ? P.rows_fp[r][v] : band_rows(r, v);
       View dst;
@@ -202,7 +231,7 @@ struct Run {
       }
       act[v] = dst;
       if (views_only) continue;
-      if (sched == S_CARRY && r > 0 && q.a > q.lo) {
+      if (sched == S_CARRY && r > 0 && q.a > q.lo && batch) {
         // rows shared from earlier bands (two-phase sharing): kept at the
         // backward boundary that ends where this band starts
         const int sidx = fp ? r * P.refine - 1 : r - 1;
@@ -210,15 +239,28 @@ struct Run {
         if (!holds(strip, P.tail[sidx][v], P.rows[sidx][v].b) || P.tail[sidx][v] != q.lo ||
             P.rows[sidx][v].b != q.a)
           return lrcnn_fail(LRCNN_EINVAL, "internal: strip rows do not match the band");
-        LAUNCH(launch_rows_copy(dt, dt, strip, dst, 0, P.cfg.batch, q.lo, q.a,
-                                P.shp[v].w, P.shp[v].c, stream),
-               "strip load");
+        if ((st = strip_copy(true, segs, strip, dst, q.lo, q.a, v, "strip load")) != LRCNN_OK)
+          return st;
+      }
+    }
+    if (views_only) return LRCNN_OK;
+    if ((st = flush_copies(segs, "strip load")) != LRCNN_OK) return st;
+    for (int v = 1; v < n; ++v) {
+      const Rows q = fp ? P.rows_fp[r][v] : band_rows(r, v);
+      const View dst = act[v];
+      if (sched == S_CARRY && r > 0 && q.a > q.lo && !batch) {
+        const int sidx = fp ? r * P.refine - 1 : r - 1;
+        View strip = win(L.strip[sidx][v], v, q.a - q.lo, q.lo);
+        if (!holds(strip, P.tail[sidx][v], P.rows[sidx][v].b) || P.tail[sidx][v] != q.lo ||
+            P.rows[sidx][v].b != q.a)
+          return lrcnn_fail(LRCNN_EINVAL, "internal: strip rows do not match the band");
+        if ((st = strip_copy(false, segs, strip, dst, q.lo, q.a, v, "strip load")) != LRCNN_OK)
+          return st;
       }
       uint8_t *am = ((bp || keep) && P.nodes[v].op == LRCNN_OP_MAXPOOL)
                         ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
       uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
-      int st = node_fwd(v, q.a, q.b, dst, am, mk);
-      if (st != LRCNN_OK) return st;
+      if ((st = node_fwd(v, q.a, q.b, dst, am, mk)) != LRCNN_OK) return st;
       if (v == n - 1 && y && keep)
         LAUNCH(launch_rows_copy(dt, dt, dst, full(y, v), 0, P.cfg.batch, q.a, q.b,
                                 P.shp[v].w, P.shp[v].c, stream),
@@ -233,13 +275,12 @@ struct Run {
           View strip = win(L.strip[sidx][v], v, e - t, t);
           if (!holds(dst, t, e))
             return lrcnn_fail(LRCNN_EINVAL, "internal: strip rows not in the band window");
-          LAUNCH(launch_rows_copy(dt, dt, dst, strip, 0, P.cfg.batch, t, e,
-                                  P.shp[v].w, P.shp[v].c, stream),
-                 "strip store");
+          if ((st = strip_copy(batch, segs, dst, strip, t, e, v, "strip store")) != LRCNN_OK)
+            return st;
         }
       }
     }
-    return LRCNN_OK;
+    return flush_copies(segs, "strip store");
   }
 
   Rows band_rows(int r, int v) const {

@@ -1494,6 +1494,54 @@ int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate, int B,
   return (int)hipGetLastError();
 }
 
+struct CopyBatch {
+  int n;
+  CopySeg seg[kMaxCopySegs];
+  RowIter it[kMaxCopySegs];
+  long long start[kMaxCopySegs + 1];  // first flat vector index of each segment
+};
+
+template <typename T, int V>
+__global__ void rows_copy_batch_kernel(CopyBatch cb) {
+  GRID_STRIDE(idx, cb.start[cb.n]) {
+    int s = 0;
+    while (s + 1 < cb.n && idx >= cb.start[s + 1]) ++s;
+    const CopySeg &g = cb.seg[s];
+    int b, y, in;
+    cb.it[s].at(idx - cb.start[s], V, b, y, in);
+    float v[4];
+    ldv<T, V>((const T *)g.src.p + view_off(g.src, b, y, in), v);
+    stv<T, V>((T *)g.dst.p + view_off(g.dst, b, y, in), v);
+  }
+}
+
+int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream) {
+  if (n <= 0) return 0;
+  if (n > kMaxCopySegs) return (int)hipErrorInvalidValue;
+  CopyBatch cb{};
+  int V = 4;
+  for (int i = 0; i < n; ++i)
+    if (((long long)segs[i].W * segs[i].C) % 4 != 0) V = 1;
+  cb.n = n;
+  cb.start[0] = 0;
+  for (int i = 0; i < n; ++i) {
+    cb.seg[i] = segs[i];
+    cb.it[i] = row_iter(segs[i].B, segs[i].r0, segs[i].r1, segs[i].W, segs[i].C, V);
+    cb.start[i + 1] = cb.start[i] + (cb.it[i].total > 0 ? cb.it[i].total : 0);
+  }
+  if (cb.start[n] <= 0) return 0;
+  hipStream_t s = (hipStream_t)stream;
+  const unsigned g = grid_for(cb.start[n]);
+  if (dt == DT_F32) {
+    if (V == 4) rows_copy_batch_kernel<float, 4><<<g, 256, 0, s>>>(cb);
+    else rows_copy_batch_kernel<float, 1><<<g, 256, 0, s>>>(cb);
+  } else {
+    if (V == 4) rows_copy_batch_kernel<bf16, 4><<<g, 256, 0, s>>>(cb);
+    else rows_copy_batch_kernel<bf16, 1><<<g, 256, 0, s>>>(cb);
+  }
+  return (int)hipGetLastError();
+}
+
 template <int V>
 __global__ void rows_zero_kernel(View dst, RowIter it) {
   const float z[4] = {0.f, 0.f, 0.f, 0.f};

@@ -157,6 +157,15 @@ int launch_act_bwd(int dt, View dz, View z, const float *scale, int relu,
 // accumulate adds into dst.
 int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate,
                      int B, int r0, int r1, int W, int C, void *stream);
+// Several same-dtype row copies in one launch (strips of every node of a
+// band). Segments are copied independently; the caller guarantees that no
+// segment's destination overlaps another segment's source or destination.
+struct CopySeg {
+  View src, dst;
+  int B, r0, r1, W, C;
+};
+constexpr int kMaxCopySegs = 24;
+int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream);
 // Zero rows [r0, r1) of a float32 view.
 int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C,
                      void *stream);
