@@ -294,21 +294,20 @@ struct Run {
     const Rows q = band_rows(r, u);
     const Shape &s = P.shp[u];
     dlt[u] = win(L.delta[u], u, L.win_cap[u], q.lo);
-    int zhi = q.hi;
     if (sched == S_CARRY && r + 1 < P.nb) {
       const int t = P.tail[r][u];
       if (q.b > t) {
+        // zero rows [lo, t), carried rows [t, b): one launch
         View cv = View{ws + L.carry[u], (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
                        L.carry_cap[u]};
-        if (!holds(cv, t, q.b) || !holds(dlt[u], t, q.b))
+        if (!holds(cv, t, q.b) || !holds(dlt[u], q.lo, q.b) || q.b != q.hi)
           return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
-        LAUNCH(launch_rows_copy(DT_F32, DT_F32, cv, dlt[u], 0, P.cfg.batch, t, q.b, s.w,
-                                s.c, stream),
-               "carry load");
-        zhi = t;
+        LAUNCH(launch_rows_init(dlt[u], &cv, t, P.cfg.batch, q.lo, q.b, s.w, s.c, stream),
+               "error window with carry");
+        return LRCNN_OK;
       }
     }
-    LAUNCH(launch_rows_zero(dlt[u], P.cfg.batch, q.lo, zhi, s.w, s.c, stream), "zero error");
+    LAUNCH(launch_rows_zero(dlt[u], P.cfg.batch, q.lo, q.hi, s.w, s.c, stream), "zero error");
     return LRCNN_OK;
   }
 
@@ -335,8 +334,16 @@ struct Run {
     }
     if (d.op == LRCNN_OP_CONV) {
       void *dc = ws + L.dc[v];
+      // the rows carried to the previous band leave in the same launch
+      View cv{};
+      const bool carries = sched == S_CARRY && r > 0 && q.a > q.lo;
+      if (carries) {
+        cv = View{ws + L.carry[v], (long long)L.carry_cap[v] * sv.w * sv.c, q.lo, sv.w, sv.c,
+                  L.carry_cap[v]};
+        if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+      }
       LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a, b,
-                            sv.w, sv.c, stream),
+                            sv.w, sv.c, stream, carries ? &cv : nullptr, q.lo, q.a),
              "error operand");
       WgradArgs g{};
       g.dc = dc;
@@ -447,7 +454,10 @@ struct Run {
         }
       int st = node_bwd(r, v, dw, want_dx);
       if (st != LRCNN_OK) return st;
-      if (sched == S_CARRY && r > 0) {
+      // a conv's carried rows left with its error operand, unless the band
+      // owns none of its rows (node_bwd then launches nothing)
+      const Rows qv = band_rows(r, v);
+      if (sched == S_CARRY && r > 0 && (d.op != LRCNN_OP_CONV || qv.b <= qv.a)) {
         const Rows q = band_rows(r, v);
         if (q.a > q.lo) {
           const Shape &s = P.shp[v];

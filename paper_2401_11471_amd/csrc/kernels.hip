@@ -1418,13 +1418,22 @@ int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
   return (int)hipGetLastError();
 }
 
+// Error operand of a conv (dc = rnd(scale[c] * dz * [z > 0]) over the
+// band's own rows, contiguous) and, in the same launch, the float32 copy of
+// the rows [lo, a) of dz that are carried to the previous band.
 template <typename T, int V>
 __global__ void act_bwd_kernel(View dz, View z, const float *scale, int relu, T *dc,
-                               int C, RowIter it) {
-  GRID_STRIDE(idx, it.total) {
+                               int C, RowIter it, View cdst, RowIter cit) {
+  GRID_STRIDE(idx, it.total + cit.total) {
     int b, y, in;
-    it.at(idx, V, b, y, in);
     float d[4], zz[4];
+    if (idx >= it.total) {
+      cit.at(idx - it.total, V, b, y, in);
+      ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
+      stv<float, V>((float *)cdst.p + view_off(cdst, b, y, in), d);
+      continue;
+    }
+    it.at(idx, V, b, y, in);
     ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
     if (relu) {
       ldv<T, V>((const T *)z.p + view_off(z, b, y, in), zz);
@@ -1441,18 +1450,25 @@ __global__ void act_bwd_kernel(View dz, View z, const float *scale, int relu, T 
 }
 
 int launch_act_bwd(int dt, View dz, View z, const float *scale, int relu,
-                   void *dc, int B, int y0, int y1, int W, int C, void *stream) {
+                   void *dc, int B, int y0, int y1, int W, int C, void *stream,
+                   const View *carry, int c0, int c1) {
   const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
   RowIter it = row_iter(B, y0, y1, W, C, V);
-  if (it.total <= 0) return 0;
+  RowIter cit = row_iter(B, c0, carry ? c1 : c0, W, C, V);
+  const View cd = carry ? *carry : View{};
+  if (it.total + cit.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  const unsigned g = grid_for(it.total);
+  const unsigned g = grid_for(it.total + cit.total);
   if (dt == DT_F32) {
-    if (V == 4) act_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it);
-    else act_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it);
+    if (V == 4)
+      act_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it, cd, cit);
+    else
+      act_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (float *)dc, C, it, cd, cit);
   } else {
-    if (V == 4) act_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it);
-    else act_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it);
+    if (V == 4)
+      act_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it, cd, cit);
+    else
+      act_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, scale, relu, (bf16 *)dc, C, it, cd, cit);
   }
   return (int)hipGetLastError();
 }
@@ -1539,6 +1555,32 @@ int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream) {
     if (V == 4) rows_copy_batch_kernel<bf16, 4><<<g, 256, 0, s>>>(cb);
     else rows_copy_batch_kernel<bf16, 1><<<g, 256, 0, s>>>(cb);
   }
+  return (int)hipGetLastError();
+}
+
+// Rows of a float32 error window at the start of a band: rows below t are
+// zero, rows from t on are the error carried from the next band.
+template <int V>
+__global__ void rows_init_kernel(View dst, View carry, int t, RowIter it) {
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, V, b, y, in);
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (y >= t) ldv<float, V>((const float *)carry.p + view_off(carry, b, y, in), v);
+    stv<float, V>((float *)dst.p + view_off(dst, b, y, in), v);
+  }
+}
+
+int launch_rows_init(View dst, const View *carry, int t, int B, int r0, int r1, int W, int C,
+                     void *stream) {
+  const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
+  RowIter it = row_iter(B, r0, r1, W, C, V);
+  if (it.total <= 0) return 0;
+  const View cv = carry ? *carry : View{};
+  if (!carry) t = r1;
+  hipStream_t s = (hipStream_t)stream;
+  if (V == 4) rows_init_kernel<4><<<grid_for(it.total), 256, 0, s>>>(dst, cv, t, it);
+  else rows_init_kernel<1><<<grid_for(it.total), 256, 0, s>>>(dst, cv, t, it);
   return (int)hipGetLastError();
 }
 

@@ -151,8 +151,10 @@ int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
                    int y0, int y1, int W, int C, void *stream);
 // Error operand of a conv: dc = rnd(scale[c] * dz * [z > 0]) over rows
 // [y0, y1), written contiguously (storage dtype).
+// `carry` (nullable): also copy rows [c0, c1) of dz (float32) into it.
 int launch_act_bwd(int dt, View dz, View z, const float *scale, int relu,
-                   void *dc, int B, int y0, int y1, int W, int C, void *stream);
+                   void *dc, int B, int y0, int y1, int W, int C, void *stream,
+                   const View *carry = nullptr, int c0 = 0, int c1 = 0);
 // Rows [r0, r1) from src to dst with conversion (types 0 = f32, 1 = bf16);
 // accumulate adds into dst.
 int launch_rows_copy(int st, int dtt, View src, View dst, int accumulate,
@@ -166,6 +168,10 @@ struct CopySeg {
 };
 constexpr int kMaxCopySegs = 24;
 int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream);
+// Rows [r0, r1) of a float32 view: zero below t, rows [t, r1) copied from
+// `carry` (nullable: all zero).
+int launch_rows_init(View dst, const View *carry, int t, int B, int r0, int r1, int W, int C,
+                     void *stream);
 // Zero rows [r0, r1) of a float32 view.
 int launch_rows_zero(View dst, int B, int r0, int r1, int W, int C,
                      void *stream);
