@@ -126,12 +126,22 @@ __device__ __forceinline__ int fdiv(int a, int b) {
 
 // Tile geometry: a K tile row is KR 16-byte vectors (64 or 128 bytes) of one
 // pixel or one weight row, staged in LDS with one extra vector of pitch.
+#ifndef LRCNN_SWZ
+#define LRCNN_SWZ 1
+#endif
 template <typename T, int KR = 4>
 struct Cfg {
   static constexpr int E = 16 / (int)sizeof(T);  // elements per 16 bytes
   static constexpr int BK = KR * E;               // K elements per tile row
-  static constexpr int LDK = BK + E;              // LDS pitch in elements
+  static constexpr int LDK = LRCNN_SWZ ? BK : BK + E;  // LDS pitch in elements
 };
+// Row-major LDS tiles with LRCNN_SWZ: no padding; the 16-byte vector v of
+// row r is stored at slot v ^ ((r >> 2) & 3), which keeps the 16-lane
+// phases of 16-byte reads (16 consecutive rows, one vector) and writes (4
+// rows x 4 vectors) on distinct banks. Needs 4 vectors per row.
+__device__ __forceinline__ int swz(int row, int vec) {
+  return LRCNN_SWZ ? (vec ^ ((row >> 2) & 3)) : vec;
+}
 
 constexpr int BM = 128;
 
@@ -169,10 +179,11 @@ struct Frag<float, BN, KR, AKM, BKM> {
 #pragma unroll
         for (int s = 0; s < S; ++s) a[i][s] = As[(S * g + s) * PA + wm + 32 * i + r];
       } else {
-        const float4 *p = (const float4 *)(As + (wm + 32 * i + r) * LDK + S * g);
+        const int row = wm + 32 * i + r;
+        const float4 *p = (const float4 *)(As + row * LDK);
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
-          const float4 t = p[q];
+          const float4 t = p[swz(row, NV * g + q)];
           a[i][4 * q] = t.x, a[i][4 * q + 1] = t.y, a[i][4 * q + 2] = t.z, a[i][4 * q + 3] = t.w;
         }
       }
@@ -183,10 +194,11 @@ struct Frag<float, BN, KR, AKM, BKM> {
 #pragma unroll
         for (int s = 0; s < S; ++s) b[j][s] = Bs[(S * g + s) * PB + wn + 32 * j + r];
       } else {
-        const float4 *p = (const float4 *)(Bs + (wn + 32 * j + r) * LDK + S * g);
+        const int row = wn + 32 * j + r;
+        const float4 *p = (const float4 *)(Bs + row * LDK);
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
-          const float4 t = p[q];
+          const float4 t = p[swz(row, NV * g + q)];
           b[j][4 * q] = t.x, b[j][4 * q + 1] = t.y, b[j][4 * q + 2] = t.z, b[j][4 * q + 3] = t.w;
         }
       }
@@ -243,9 +255,10 @@ struct Frag<bf16, BN, KR, AKM, BKM> {
 #pragma unroll
         for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8(As, PA, wm + 32 * i, q, lane);
       } else {
-        const bf16x8 *p = (const bf16x8 *)(As + (wm + 32 * i + r) * LDK + 8 * NV * g);
+        const int row = wm + 32 * i + r;
+        const bf16x8 *p = (const bf16x8 *)(As + row * LDK);
 #pragma unroll
-        for (int q = 0; q < NV; ++q) a[i][q] = p[q];
+        for (int q = 0; q < NV; ++q) a[i][q] = p[swz(row, NV * g + q)];
       }
     }
 #pragma unroll
@@ -254,9 +267,10 @@ struct Frag<bf16, BN, KR, AKM, BKM> {
 #pragma unroll
         for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8(Bs, PB, wn + 32 * j, q, lane);
       } else {
-        const bf16x8 *p = (const bf16x8 *)(Bs + (wn + 32 * j + r) * LDK + 8 * NV * g);
+        const int row = wn + 32 * j + r;
+        const bf16x8 *p = (const bf16x8 *)(Bs + row * LDK);
 #pragma unroll
-        for (int q = 0; q < NV; ++q) b[j][q] = p[q];
+        for (int q = 0; q < NV; ++q) b[j][q] = p[swz(row, NV * g + q)];
       }
     }
   }
@@ -439,7 +453,9 @@ static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
 
 // ------------------------------------------- conv forward / input grad
 template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1>
-__global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
+// bfloat16: three workgroups per CU (the register budget is set for it;
+// the swizzled LDS tiles fit three); float32 keeps the registers of two
+__global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(ConvArgs a) {
   using CF = Cfg<T, KR>;
   constexpr int E = CF::E, BK = CF::BK, LDK = CF::LDK;
   constexpr int NB = BN / 64;
@@ -457,9 +473,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   // reuses it to stage the output tile ([BM][BN + E] in the storage dtype)
   constexpr int CP = BN + E;
   constexpr size_t RING = sizeof(T) * ST * ((size_t)BM * LDK + BSZ);
-  // (input gradient: float32 tile [BM][BN + 4], added to the error window)
-  constexpr size_t CTILE = DGRAD ? sizeof(float) * (size_t)BM * (BN + 4)
-                                 : sizeof(T) * (size_t)BM * CP;
+  // (input gradient: float32 tile [BM][BN + 4], added to the error window);
+  // a tile larger than the ring is staged in two halves of 64 rows
+  constexpr size_t CROW = DGRAD ? sizeof(float) * (BN + 4) : sizeof(T) * CP;
+  constexpr int HR = CROW * BM > RING ? BM / 2 : BM;
+  constexpr size_t CTILE = CROW * HR;
   __shared__ __align__(16) char smem[RING > CTILE ? RING : CTILE];
   T (*As)[BM * LDK] = reinterpret_cast<T (*)[BM * LDK]>(smem);
   T (*Bs)[BSZ] = reinterpret_cast<T (*)[BSZ]>(smem + sizeof(T) * ST * BM * LDK);
@@ -593,7 +611,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
   auto store = [&](int st) {
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + kv * E]) = ra[i];
+      *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + swz(tid / KR + RS * i, kv) * E]) = ra[i];
 #pragma unroll
     for (int j = 0; j < NBL; ++j) {
       if (BKM) {
@@ -608,7 +626,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         for (int e = 0; e < E; ++e)
           Bs[st][((tid % BV) * E + e) * LDK + bk0 + BKS * j] = t.e[e];
       } else {
-        *(uint4 *)(&Bs[st][(tid / KR + RS * j) * LDK + kv * E]) = rb[j];
+        *(uint4 *)(&Bs[st][(tid / KR + RS * j) * LDK + swz(tid / KR + RS * j, kv) * E]) = rb[j];
       }
     }
   };
@@ -688,29 +706,33 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     // forward: affine, ReLU (and the optional mask) in registers, the tile
     // staged in LDS, then whole 16-byte row chunks stored per thread
     T *Ct = reinterpret_cast<T *>(smem);
+    constexpr int CPR = BN / E;     // 16-byte chunks per tile row
+    constexpr int RPP = 256 / CPR;  // tile rows per pass
+    const int cc = tid % CPR;
+    const int n = n0 + cc * E;
+    for (int h0 = 0; h0 < BM; h0 += HR) {
+    if (h0) __syncthreads();
+    if (wm >= h0 && wm < h0 + HR) {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int r = wm + 32 * i + acc_row(v, lane);
+        const int r = wm - h0 + 32 * i + acc_row(v, lane);
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
           const int cl = wn + 32 * j + col;
-          const int n = n0 + cl;
+          const int nn = n0 + cl;
           float val = acc[i][j][v];
-          if (n < a.N) {
-            if (a.scale) val = val * a.scale[n] + a.shift[n];
+          if (nn < a.N) {
+            if (a.scale) val = val * a.scale[nn] + a.shift[nn];
             if (a.relu) val = val > 0.f ? val : 0.f;
           }
           stf(&Ct[r * CP + cl], val);
         }
       }
+    }
     __syncthreads();
-    constexpr int CPR = BN / E;     // 16-byte chunks per tile row
-    constexpr int RPP = 256 / CPR;  // tile rows per pass
-    const int cc = tid % CPR;
-    const int n = n0 + cc * E;
-    for (int r = tid / CPR; r < BM; r += RPP) {
+    for (int r = h0 + tid / CPR; r < h0 + HR; r += RPP) {
       const int m = m0 + r;
       if (m >= M || n >= a.N) continue;
       const int x = m % a.Wd;
@@ -718,7 +740,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       const int y = a.y0 + t % R;
       const int b = t / R;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
-      const uint4 q = *(const uint4 *)&Ct[r * CP + cc * E];
+      const uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
       *(uint4 *)((T *)a.dst.p + off) = q;
       if (a.mask) {
         union {
@@ -731,6 +753,7 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
         for (int e = 0; e < E; ++e) mk[e] = ldf(&w.e[e]) > 0.f ? 1 : 0;
       }
     }
+    }
     return;
   }
   if (DGRAD && (a.N % 4) == 0) {
@@ -738,20 +761,24 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
     // read-add-write of the error window
     constexpr int FP = BN + 4;
     float *Ct = reinterpret_cast<float *>(smem);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = wm + 32 * i + acc_row(v, lane);
-#pragma unroll
-        for (int j = 0; j < NB; ++j) Ct[r * FP + wn + 32 * j + col] = acc[i][j][v];
-      }
-    __syncthreads();
     constexpr int CPR = BN / 4;
     constexpr int RPP = 256 / CPR;
     const int cc = tid % CPR;
     const int n = n0 + cc * 4;
-    for (int r = tid / CPR; r < BM; r += RPP) {
+    for (int h0 = 0; h0 < BM; h0 += HR) {
+    if (h0) __syncthreads();
+    if (wm >= h0 && wm < h0 + HR) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = wm - h0 + 32 * i + acc_row(v, lane);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) Ct[r * FP + wn + 32 * j + col] = acc[i][j][v];
+      }
+    }
+    __syncthreads();
+    for (int r = h0 + tid / CPR; r < h0 + HR; r += RPP) {
       const int m = m0 + r;
       if (m >= M || n >= a.N) continue;
       const int x = m % a.Wd;
@@ -760,10 +787,11 @@ __global__ __launch_bounds__(256) void conv_gemm_kernel(ConvArgs a) {
       const int b = t / R;
       float4 *d = (float4 *)((float *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow +
                              (long long)x * a.N + n);
-      const float4 q = *(const float4 *)&Ct[r * FP + cc * 4];
+      const float4 q = *(const float4 *)&Ct[(r - h0) * FP + cc * 4];
       float4 o = *d;
       o.x += q.x, o.y += q.y, o.z += q.z, o.w += q.w;
       *d = o;
+    }
     }
     return;
   }
