@@ -509,6 +509,17 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     ay[i] = a.y0 + t % R;
     abase[i] = (long long)(t / R) * a.src.bs - (long long)a.src.row0 * srow;
   }
+  // source row / column of each A row before the tap offset, and its
+  // address there: a K step then adds one uniform offset per tap and
+  // channel block (input gradient: subtracts the tap)
+  int by[NA], bx[NA];
+  long long rbase[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i) {
+    by[i] = DGRAD ? ay[i] + a.ph : ay[i] * a.sh - a.ph;
+    bx[i] = DGRAD ? ax[i] + a.pw : ax[i] * a.sw - a.pw;
+    rbase[i] = abase[i] + (long long)by[i] * srow + (long long)bx[i] * a.src.C;
+  }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
   // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output
   // channel of the consumer), contiguous along n, so each 16-byte load
@@ -523,6 +534,11 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     bvld[j] = bn[j] < a.N;
   }
   const int bk0 = tid / BV;
+  long long bbase[NBL];
+#pragma unroll
+  for (int j = 0; j < NBL; ++j)
+    bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * taps * a.N + bn[j]
+                     : (long long)bn[j] * taps * a.KC + kv * E;
 
   // K iterations of this workgroup (split-K over the tile's z), walked as
   // (tap, channel block) without divisions in the loop
@@ -538,27 +554,25 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     const int c0 = cb + kv * E;
     const bool cok = c0 < a.KC;
     const int lim = a.KC - c0;
+    const long long tofs = (long long)ti * srow + (long long)tj * a.src.C;  // uniform
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       int sy, sx;
       bool ok;
-      if (DGRAD) {
-        const int ty = ay[i] + a.ph - ti, tx = ax[i] + a.pw - tj;
-        ok = (ty >= 0) & (tx >= 0);
-        if (S1) {
-          sy = ty, sx = tx;
-        } else {
-          sy = ty / a.sh;
-          sx = tx / a.sw;
-          ok = ok & (sy * a.sh == ty) & (sx * a.sw == tx);
-        }
+      long long off;
+      if (DGRAD && !S1) {
+        const int ty = by[i] - ti, tx = bx[i] - tj;
+        sy = ty / a.sh;
+        sx = tx / a.sw;
+        ok = (ty >= 0) & (tx >= 0) & (sy * a.sh == ty) & (sx * a.sw == tx);
+        off = abase[i] + sy * srow + (long long)sx * a.src.C + c0;
       } else {
-        sy = ay[i] * a.sh - a.ph + ti;
-        sx = ax[i] * a.sw - a.pw + tj;
+        sy = DGRAD ? by[i] - ti : by[i] + ti;
+        sx = DGRAD ? bx[i] - tj : bx[i] + tj;
         ok = sx >= 0;
+        off = (DGRAD ? rbase[i] - tofs : rbase[i] + tofs) + c0;
       }
       ok = ok & am[i] & cok & (sy >= a.sy0) & (sy < a.sy1) & (sx < a.Ws);
-      const long long off = abase[i] + sy * srow + (long long)sx * a.src.C + c0;
       if (VEC) {
         ra[i] = load16z(src, off * (long long)sizeof(T), ok);
       } else {
@@ -575,11 +589,11 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       if (DGRAD) {
         const int o = cb + bk0 + BKS * j;
         ok = bvld[j] & (o < a.KC);
-        off = ((long long)o * taps + tap) * a.N + bn[j];
+        off = bbase[j] + ((long long)cb * taps + tap) * a.N;
         blim = a.N - bn[j];
       } else {
         ok = bvld[j] & cok;
-        off = ((long long)bn[j] * taps + tap) * a.KC + c0;
+        off = bbase[j] + (long long)tap * a.KC + cb;
         blim = lim;
       }
       if (VEC) {
@@ -975,8 +989,11 @@ __device__ __forceinline__ void divmod_rcp(int p, int d, float inv, int &q, int 
 // A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
 // input pixel under tap; both are K-outer in memory, so tiles are written
 // to LDS transposed into the same [row][k] layout used above.
+#ifndef LRCNN_WG_OCC
+#define LRCNN_WG_OCC 2
+#endif
 template <typename T, bool AVEC, bool BVEC>
-__global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a, int kchunk,
+__global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, int kchunk,
                                                     float *dw) {
   constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
   constexpr int BN = 128, NB = 2;
