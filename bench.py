@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from the host in the timed region "
                          "(default: the step is captured once in a HIP graph and replayed)")
+    ap.add_argument("--max-batch", action="store_true",
+                    help="largest-batch study instead of the throughput line: the "
+                         "largest layer-wise and row-centric batches that fit the free "
+                         "device memory (planner search), each confirmed by one step")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a "
                          "known-size reference for hardware byte counters)")
@@ -136,6 +140,85 @@ def timed_steps(torch, step, steps, warmup, eager, profile=None):
     return e0.elapsed_time(e1) / steps, 1, graph
 
 
+def max_batch_study(args):
+    """Largest batch of the layer-wise baseline and of the row-centric step
+    that fit in the device's free memory: found by the planner's search
+    (lrcnn_max_batch over the exact workspace plus every other buffer of the
+    step), then confirmed by allocating every buffer and running one step.
+    Inputs are N(0, 1) drawn on the device (the confirmation measures
+    capacity and time, not values)."""
+    import torch
+    from paper_2401_11471_amd import lrcnn as L
+    from workloads import CONFIGS, config_inputs, BF16
+
+    c = dict(CONFIGS[args.config])
+    nb = args.bands or c["bands"]
+    mode = L.RECOMPUTE if args.mode == "recompute" else L.CARRY
+    policy = L.BALANCED if args.mode == "balanced" else L.EVEN
+    nodes, inp = config_inputs(args.config, batch=1)
+    _, H, W, Cin = inp.x.shape
+    tdt = torch.bfloat16 if inp.dtype == BF16 else torch.float32
+    free, total = torch.cuda.mem_get_info()
+    # the allocator rounds every buffer up to whole 2 MiB blocks: leave a
+    # margin for that and for the runtime's own allocations
+    budget = free - (2 << 30)
+    out = {"metric": "largest training batch that fits one MI355X (FP+BP)",
+           "unit": "images", "n_gpus": 1, "config": {"workload": c["name"], "bands": nb,
+           "mode": args.mode}, "device_total_bytes": total, "device_free_bytes": free,
+           "budget_bytes": budget}
+    gen = torch.Generator(device="cuda")
+    for label, lw in (("layerwise", True), ("row_centric", False)):
+        B = L.lrcnn_max_batch(nodes, Cin, H, W, budget, inp.dtype, mode, nb, policy,
+                              bp_refine=args.bp_refine, layerwise=lw)
+        plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb, policy,
+                            bp_refine=args.bp_refine)
+        info = plan.info()
+        print(f"max-batch {label}: B={B}, planned step bytes {plan.step_bytes(lw)}; "
+              "allocating and running one step", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        gen.manual_seed(args.config)
+        x = torch.empty((B, H, W, Cin), device="cuda", dtype=tdt)
+        for i in range(B):
+            x[i].normal_(generator=gen)
+        w = [None] + [None if wv is None else torch.from_numpy(wv).to("cuda", tdt)
+                      for wv in inp.weights]
+        sc = [None] + [None if v is None else torch.from_numpy(v).cuda() for v in inp.scales]
+        sf = [None] + [None if v is None else torch.from_numpy(v).cuda() for v in inp.shifts]
+        dw = [None if t is None else torch.empty(t.shape, device="cuda") for t in w]
+        oshape = (B,) + plan.node_shape(len(nodes) - 1)
+        dy = torch.empty(oshape, device="cuda", dtype=tdt).normal_(generator=gen)
+        y = torch.empty(oshape, device="cuda", dtype=tdt)
+        ws = torch.empty(info["layerwise_workspace_bytes" if lw else "workspace_bytes"],
+                         device="cuda", dtype=torch.uint8)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        if lw:
+            L.lrcnn_layerwise_reference_gpu(plan, x, w, sc, sf, dy, y, dw, None, ws)
+        else:
+            L.lrcnn_forward_rows(plan, x, w, sc, sf, y, ws)
+            L.lrcnn_backward_rows(plan, x, w, sc, sf, dy, dw, None, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        # per image: a float32 copy of the whole output would not fit
+        finite = all(bool(torch.isfinite(y[i].float().sum()).item()) for i in range(B)) and \
+            all(t is None or bool(torch.isfinite(t.sum()).item()) for t in dw)
+        out[label] = {"batch": B, "planned_step_bytes": plan.step_bytes(lw),
+                      "peak_allocated_bytes": int(torch.cuda.max_memory_allocated() - base),
+                      "step_ms": round(ms, 1), "images_per_s": round(B * 1000.0 / ms, 3),
+                      "outputs_finite": finite}
+        print(f"max-batch {label}: step {ms:.0f} ms", file=sys.stderr, flush=True)
+        del x, w, sc, sf, dw, dy, y, ws, plan
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    out["batch_ratio_rows_over_layerwise"] = round(
+        out["row_centric"]["batch"] / out["layerwise"]["batch"], 3)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -144,6 +227,10 @@ def main():
               f"(WORLD_SIZE={world}) is not supported. Multi-GPU sharding is a "
               "design note, not an implemented path.", file=sys.stderr)
         sys.exit(2)
+
+    if args.max_batch:
+        max_batch_study(args)
+        return
 
     import torch
     from paper_2401_11471_amd import lrcnn as L
@@ -261,6 +348,16 @@ def main():
                                           "partial_bytes", "omega_bytes", "flops_tau",
                                           "flops_rows", "shared_rows", "halo_rows")},
     }
+    # largest batch the planner fits in the whole device memory (host-side
+    # search; `--max-batch` confirms it by running)
+    total = torch.cuda.mem_get_info()[1]
+    out["planned_max_batch"] = {
+        "budget_bytes": int(total),
+        "layerwise": L.lrcnn_max_batch(nodes, Cin, H, W, total, inp.dtype, mode, nb, policy,
+                                       bp_refine=args.bp_refine, layerwise=True),
+        "row_centric": L.lrcnn_max_batch(nodes, Cin, H, W, total, inp.dtype, mode, nb,
+                                         policy, bp_refine=args.bp_refine,
+                                         hybrid_from=args.hybrid_from)}
     del bufs
     torch.cuda.synchronize()
     torch.cuda.empty_cache()

@@ -177,6 +177,57 @@ int lrcnn_plan_band_rows(const lrcnn_plan_t *plan, int32_t phase, int32_t band,
 
 void lrcnn_plan_destroy(lrcnn_plan_t *plan);
 
+/* Device bytes of one training step under `plan`: the workspace
+ * (row-centric, or layer-wise when layerwise != 0) plus the xi of
+ * Eqs. (9)-(10) -- every other buffer the step touches: x, y, dy (storage
+ * dtype), the weights (storage dtype), their float32 gradients, the float32
+ * affine scale and shift, and dx when want_dx != 0. Each buffer is counted
+ * at the 256-byte granularity the library uses; a caller's allocator may
+ * round further. Errors: EINVAL on null. */
+int lrcnn_plan_step_bytes(const lrcnn_plan_t *plan, int32_t layerwise,
+                          int32_t want_dx, size_t *bytes);
+
+/* Memory budget of the budget-driven planner and the batch search. */
+typedef struct {
+  size_t budget_bytes;  /* M: device bytes the step may use               */
+  int32_t max_bands;    /* largest N_BP tried; 0: min(256, partitioned   */
+                        /* height: input rows in CARRY, output rows in    */
+                        /* RECOMPUTE)                                     */
+  int32_t max_refine;   /* largest N_BP / N_FP tried (0 reads as 1)       */
+  int32_t want_dx;      /* count dx in xi                                 */
+} lrcnn_budget;
+
+/* Budget-driven row granularity (Section III-C, Eqs. (9)-(10); the memory
+ * bound of 2PS, Eq. (12), and of OverL, Section IV-B): the plan with the
+ * smallest backward band count N_BP = N whose step fits the budget
+ * (lrcnn_plan_step_bytes(plan, 0, want_dx) <= budget_bytes), and for that
+ * N_BP the smallest forward band count N_FP (a divisor of N_BP with
+ * N_BP / N_FP <= max_refine). Small N is preferred because it gives the
+ * kernels the most parallel work (the paper's second principle). The exact
+ * workspace of each candidate plan stands in for the paper's analytic
+ * Omega, so the strips, error windows and split-K buffers are counted too.
+ * cfg->n_bands and cfg->bp_refine are ignored; cfg->policy must be EVEN or
+ * BALANCED. Candidates are tried in increasing (N_BP, N_FP) order, each a
+ * full host-side plan (milliseconds).
+ * Errors: EINVAL (null, EXPLICIT policy, bad budget), the errors of
+ * lrcnn_plan, EINFEASIBLE (no candidate up to max_bands fits). */
+int lrcnn_plan_for_budget(const lrcnn_node *nodes, int32_t n_nodes,
+                          const lrcnn_config *cfg, const lrcnn_budget *budget,
+                          lrcnn_plan_t **out);
+
+/* Largest batch whose step fits the budget: the largest B with
+ * lrcnn_plan_step_bytes(plan(B), layerwise, want_dx) <= budget_bytes, for
+ * the row-centric step of cfg (layerwise == 0) or the layer-wise baseline
+ * (layerwise != 0) -- the paper's largest-batch comparison (Section V).
+ * cfg->batch is ignored; budget->max_bands and max_refine are unused. The
+ * search doubles B until the step no longer fits (at most 2^24), then
+ * bisects; step bytes grow with B. On success *batch >= 1.
+ * Errors: EINVAL (null), the errors of lrcnn_plan, EINFEASIBLE (B = 1 does
+ * not fit). */
+int lrcnn_max_batch(const lrcnn_node *nodes, int32_t n_nodes,
+                    const lrcnn_config *cfg, int32_t layerwise,
+                    const lrcnn_budget *budget, int32_t *batch);
+
 /* Row-centric FP (Algorithm 1, FP loop): writes y. In CARRY mode the rows
  * shared between bands are left in `workspace` for lrcnn_backward_rows.
  * mask_out (nullable host array; entries nullable): per node a device

@@ -762,3 +762,131 @@ extern "C" void lrcnn_plan_destroy(lrcnn_plan_t *plan) {
   release_side(*p);
   delete p;
 }
+
+namespace lrcnn {
+
+// The xi of Eqs. (9)-(10): device bytes of a step outside the workspace.
+static size_t other_bytes(const Plan &P, bool want_dx) {
+  const size_t es = (size_t)P.es;
+  size_t t = 0;
+  const size_t xb = P.elems(0, P.shp[0].h) * es;
+  const size_t yb = P.elems(P.n - 1, P.shp[P.n - 1].h) * es;
+  t += align256(xb) + 2 * align256(yb);  // x, y, dy
+  if (want_dx) t += align256(xb);
+  for (int v = 1; v < P.n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV) continue;
+    const size_t wn = (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c;
+    t += align256(wn * es) + align256(wn * 4);  // weights, float32 dW
+    if (d.affine) t += 2 * align256((size_t)d.c_out * 4);
+  }
+  return t;
+}
+
+static size_t step_bytes(const Plan &P, bool layerwise, bool want_dx) {
+  return (layerwise ? P.lw.total : (P.hyb ? P.h_total : P.rc.total)) + other_bytes(P, want_dx);
+}
+
+}  // namespace lrcnn
+
+extern "C" int lrcnn_plan_step_bytes(const lrcnn_plan_t *plan, int32_t layerwise,
+                                     int32_t want_dx, size_t *bytes) {
+  if (!plan || !bytes) return lrcnn_fail(LRCNN_EINVAL, "null plan or output");
+  *bytes = lrcnn::step_bytes(*reinterpret_cast<const Plan *>(plan), layerwise != 0,
+                             want_dx != 0);
+  return LRCNN_OK;
+}
+
+extern "C" int lrcnn_plan_for_budget(const lrcnn_node *nodes, int32_t n_nodes,
+                                     const lrcnn_config *cfg, const lrcnn_budget *budget,
+                                     lrcnn_plan_t **out) {
+  if (!out) return lrcnn_fail(LRCNN_EINVAL, "null output pointer");
+  *out = nullptr;
+  if (!nodes || !cfg || !budget) return lrcnn_fail(LRCNN_EINVAL, "null argument");
+  if (cfg->policy != LRCNN_EVEN && cfg->policy != LRCNN_BALANCED)
+    return lrcnn_fail(LRCNN_EINVAL, "the budget search takes the EVEN or BALANCED policy");
+  if (budget->max_bands < 0 || budget->max_refine < 0 || budget->max_refine > 64)
+    return lrcnn_fail(LRCNN_EINVAL, "max_bands must be >= 0 and max_refine in [0, 64]");
+  lrcnn_config c = *cfg;
+  c.n_bands = 1;
+  c.bp_refine = 1;
+  c.bounds = nullptr;
+  // shapes from a one-band plan give the partitioned height
+  lrcnn_plan_t *probe = nullptr;
+  int st = lrcnn_plan(nodes, n_nodes, &c, &probe);
+  if (st != LRCNN_OK) return st;
+  const Plan &P1 = *reinterpret_cast<const Plan *>(probe);
+  const int H = c.mode == LRCNN_CARRY ? P1.shp[0].h : P1.shp[P1.n - 1].h;
+  const bool fits1 = lrcnn::step_bytes(P1, false, budget->want_dx != 0) <= budget->budget_bytes;
+  if (fits1) {
+    *out = probe;
+    return LRCNN_OK;
+  }
+  lrcnn_plan_destroy(probe);
+  const int maxb = budget->max_bands > 0 ? std::min(budget->max_bands, H) : std::min(256, H);
+  const int maxr = budget->max_refine > 1 ? budget->max_refine : 1;
+  for (int nbp = 2; nbp <= maxb; ++nbp) {
+    for (int nfp = 1; nfp <= nbp; ++nfp) {
+      if (nbp % nfp != 0 || nbp / nfp > maxr) continue;
+      c.n_bands = nfp;
+      c.bp_refine = nbp / nfp;
+      lrcnn_plan_t *p = nullptr;
+      st = lrcnn_plan(nodes, n_nodes, &c, &p);
+      if (st != LRCNN_OK) return st;
+      if (lrcnn::step_bytes(*reinterpret_cast<const Plan *>(p), false, budget->want_dx != 0) <=
+          budget->budget_bytes) {
+        *out = p;
+        return LRCNN_OK;
+      }
+      lrcnn_plan_destroy(p);
+    }
+  }
+  return lrcnn_fail(LRCNN_EINFEASIBLE, "no plan with at most " + std::to_string(maxb) +
+                                           " backward bands fits " +
+                                           std::to_string(budget->budget_bytes) + " bytes");
+}
+
+extern "C" int lrcnn_max_batch(const lrcnn_node *nodes, int32_t n_nodes,
+                               const lrcnn_config *cfg, int32_t layerwise,
+                               const lrcnn_budget *budget, int32_t *batch) {
+  if (!nodes || !cfg || !budget || !batch) return lrcnn_fail(LRCNN_EINVAL, "null argument");
+  *batch = 0;
+  lrcnn_config c = *cfg;
+  // 1: fits, 0: does not fit, < 0: planner error
+  auto fits = [&](int b) -> int {
+    c.batch = b;
+    lrcnn_plan_t *p = nullptr;
+    const int st = lrcnn_plan(nodes, n_nodes, &c, &p);
+    if (st != LRCNN_OK) return st;
+    const bool ok = lrcnn::step_bytes(*reinterpret_cast<const Plan *>(p), layerwise != 0,
+                                      budget->want_dx != 0) <= budget->budget_bytes;
+    lrcnn_plan_destroy(p);
+    return ok ? 1 : 0;
+  };
+  int f = fits(1);
+  if (f < 0) return f;
+  if (f == 0)
+    return lrcnn_fail(LRCNN_EINFEASIBLE, "a batch of one does not fit " +
+                                             std::to_string(budget->budget_bytes) + " bytes");
+  int lo = 1, hi = 2;  // lo fits; hi is the next candidate above it
+  const int cap = 1 << 24;
+  for (;;) {
+    if (hi > cap) {
+      *batch = lo;
+      return LRCNN_OK;
+    }
+    f = fits(hi);
+    if (f < 0) return f;
+    if (f == 0) break;
+    lo = hi;
+    hi *= 2;
+  }
+  while (hi - lo > 1) {  // fits(lo) == 1, fits(hi) == 0
+    const int mid = lo + (hi - lo) / 2;
+    f = fits(mid);
+    if (f < 0) return f;
+    (f ? lo : hi) = mid;
+  }
+  *batch = lo;
+  return LRCNN_OK;
+}

@@ -68,6 +68,11 @@ class PlanInfo(C.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+class Budget(C.Structure):
+    _fields_ = [("budget_bytes", C.c_size_t), ("max_bands", C.c_int32),
+                ("max_refine", C.c_int32), ("want_dx", C.c_int32)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
@@ -81,6 +86,11 @@ def _load():
     lib.lrcnn_plan_node_shape.argtypes = [vp, i32, C.POINTER(i32)]
     lib.lrcnn_plan_band_rows.argtypes = [vp, i32, i32, i32, C.POINTER(i32)]
     lib.lrcnn_plan_destroy.argtypes = [vp]
+    lib.lrcnn_plan_step_bytes.argtypes = [vp, i32, i32, C.POINTER(sz)]
+    lib.lrcnn_plan_for_budget.argtypes = [C.POINTER(Node), i32, C.POINTER(Config),
+                                          C.POINTER(Budget), C.POINTER(vp)]
+    lib.lrcnn_max_batch.argtypes = [C.POINTER(Node), i32, C.POINTER(Config), i32,
+                                    C.POINTER(Budget), C.POINTER(i32)]
     lib.lrcnn_plan_destroy.restype = None
     lib.lrcnn_forward_rows.argtypes = [vp, vp, pp, pp, pp, vp, vp, sz, pp, vp]
     lib.lrcnn_backward_rows.argtypes = [vp, vp, pp, pp, pp, vp, pp, vp, vp, sz, vp]
@@ -98,7 +108,8 @@ def _load():
     lib.lrcnn_debug_profile_entry.restype = C.c_int
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
               "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
-              "lrcnn_layerwise_reference_gpu"):
+              "lrcnn_layerwise_reference_gpu", "lrcnn_plan_step_bytes",
+              "lrcnn_plan_for_budget", "lrcnn_max_batch"):
         getattr(lib, f).restype = C.c_int
     return lib
 
@@ -107,7 +118,8 @@ LIB = _load()
 
 # Names the header declares (checked by the tests against the shared object).
 EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
-           "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_forward_rows",
+           "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_plan_step_bytes",
+           "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_forward_rows",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
            "lrcnn_debug_dry_run", "lrcnn_debug_profile", "lrcnn_debug_profile_collect",
            "lrcnn_debug_profile_entry")
@@ -141,6 +153,14 @@ class Plan:
         _check(LIB.lrcnn_plan_node_shape(self.handle, v, out))
         return tuple(out)
 
+    def step_bytes(self, layerwise=False, want_dx=False):
+        """Workspace plus every other buffer of one step (the xi of
+        Eqs. (9)-(10)), in bytes."""
+        out = C.c_size_t()
+        _check(LIB.lrcnn_plan_step_bytes(self.handle, 1 if layerwise else 0,
+                                         1 if want_dx else 0, C.byref(out)))
+        return out.value
+
     def band_rows(self, band, v, phase=1):
         """Rows (a, b, lo, hi) of node v in a backward (phase 1) or forward
         (phase 0) band."""
@@ -161,6 +181,39 @@ def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
     h = C.c_void_p()
     _check(LIB.lrcnn_plan(arr, len(nodes), C.byref(cfg), C.byref(h)))
     return Plan(h, nodes)
+
+
+def _node_cfg(nodes, batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, bp_refine,
+              hybrid_from):
+    arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
+    return arr, Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None,
+                       bp_refine, hybrid_from)
+
+
+def lrcnn_plan_for_budget(nodes, batch, in_c, in_h, in_w, budget_bytes, dtype=F32,
+                          mode=CARRY, policy=EVEN, max_bands=0, max_refine=1,
+                          want_dx=False, hybrid_from=0):
+    """Smallest (N_BP, N_FP) whose step fits budget_bytes (Eqs. (9)-(10))."""
+    arr, cfg = _node_cfg(nodes, batch, in_c, in_h, in_w, dtype, mode, 1, policy, 1,
+                         hybrid_from)
+    bud = Budget(int(budget_bytes), max_bands, max_refine, 1 if want_dx else 0)
+    h = C.c_void_p()
+    _check(LIB.lrcnn_plan_for_budget(arr, len(nodes), C.byref(cfg), C.byref(bud),
+                                     C.byref(h)))
+    return Plan(h, nodes)
+
+
+def lrcnn_max_batch(nodes, in_c, in_h, in_w, budget_bytes, dtype=F32, mode=CARRY,
+                    n_bands=1, policy=EVEN, bp_refine=1, hybrid_from=0, layerwise=False,
+                    want_dx=False):
+    """Largest batch whose row-centric (or layer-wise) step fits budget_bytes."""
+    arr, cfg = _node_cfg(nodes, 1, in_c, in_h, in_w, dtype, mode, n_bands, policy,
+                         bp_refine, hybrid_from)
+    bud = Budget(int(budget_bytes), 0, 1, 1 if want_dx else 0)
+    out = C.c_int32()
+    _check(LIB.lrcnn_max_batch(arr, len(nodes), C.byref(cfg), 1 if layerwise else 0,
+                               C.byref(bud), C.byref(out)))
+    return out.value
 
 
 def _ptr(t):
