@@ -158,14 +158,16 @@ constexpr int BM = 128;
 // layout is K-outer (the input gradient's weights, both weight-gradient
 // operands) be stored with 16-byte writes; it is used for float32, where
 // one element feeds one MFMA.
-template <typename T, int BN, int KR, int AKM = 0, int BKM = 0>
+// TA / TB: rows of the A tile and columns of the B tile in LDS (the pitch
+// of a k-major operand); NB = BN / 64 column blocks per wave.
+template <typename T, int BN, int KR, int AKM = 0, int BKM = 0, int TA = BM, int TB = BN>
 struct Frag;
 
-template <int BN, int KR, int AKM, int BKM>
-struct Frag<float, BN, KR, AKM, BKM> {
+template <int BN, int KR, int AKM, int BKM, int TA, int TB>
+struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
   static constexpr int LDK = Cfg<float, KR>::LDK, NB = BN / 64, NV = KR / 2;
   static constexpr int S = 4 * NV;            // K elements per lane group
-  static constexpr int PA = BM + 4, PB = BN + 4;
+  static constexpr int PA = TA + 4, PB = TB + 4;
   // instructions per tile step: MFMAs and LDS reads of one fragment load
   static constexpr int NMFMA = S * 2 * NB;
   static constexpr int NDSR = (AKM ? 2 * S : 2 * NV) + (BKM ? NB * S : NB * NV);
@@ -239,10 +241,10 @@ __device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int pitch, int base, int
   return __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
-template <int BN, int KR, int AKM, int BKM>
-struct Frag<bf16, BN, KR, AKM, BKM> {
+template <int BN, int KR, int AKM, int BKM, int TA, int TB>
+struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
   static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
-  static constexpr int PA = BM + 8, PB = BN + 8;
+  static constexpr int PA = TA + 8, PB = TB + 8;
   static constexpr int NMFMA = NV * 2 * NB;
   static constexpr int NDSR = (AKM ? 4 * NV : 2 * NV) + (BKM ? 2 * NB * NV : NB * NV);
   bf16x8 a[2][NV], b[NB][NV];
@@ -547,6 +549,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
 
+  // two register buffers: the global loads of tile t+4 are issued in step t
+  // and written to LDS in step t+2, so a load has two steps to arrive
   uint4 ra[NA], rb[NBL];
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
@@ -987,23 +991,28 @@ __device__ __forceinline__ void divmod_rcp(int p, int d, float inv, int &q, int 
 
 // ------------------------------------------------------------ weight grad
 // A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
-// input pixel under tap; both are K-outer in memory, so tiles are written
-// to LDS transposed into the same [row][k] layout used above.
+// input pixel under tap. Both are K-outer in memory, so both tiles are
+// staged k-major ([k][row], 16-byte stores). The tile is WBM x 128: WBM =
+// 128 (four waves of 64 x 64) or, for 64 output channels or fewer, WBM = 64
+// (four waves of 64 x 32), so a narrow layer does not compute a half-empty
+// tile.
 #ifndef LRCNN_WG_OCC
 #define LRCNN_WG_OCC 2
 #endif
-template <typename T, bool AVEC, bool BVEC>
+template <typename T, int WBM, bool AVEC, bool BVEC>
 __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, int kchunk,
                                                     float *dw) {
-  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK, LDK = Cfg<T>::LDK;
-  constexpr int BN = 128, NB = 2;
-  constexpr int RV = BM / E;        // 16-byte vectors per 128-wide tile row
-  constexpr int KS = 256 / RV;      // pixels loaded per pass
-  // both operands are K-outer in memory and staged k-major with 16-byte
-  // stores
-  constexpr int KM = 1;
-  constexpr int PA = BM + E, PB = BN + E;
-  constexpr int ASZ = KM ? BK * PA : BM * LDK, BSZ = KM ? BK * PB : BN * LDK;
+  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK;
+  constexpr int BN = 128;
+  constexpr int FBN = WBM == 128 ? 128 : 64;  // columns per wave: FBN / 2
+  constexpr int NB = FBN / 64;
+  constexpr int RV = BN / E;        // 16-byte vectors per B tile row
+  constexpr int KS = 256 / RV;      // pixels of B loaded per pass
+  constexpr int RVA = WBM / E;      // 16-byte vectors per A tile row
+  constexpr int KSA = 256 / RVA;    // pixels of A loaded per pass
+  constexpr int NPA = BK / KSA;     // A passes per tile
+  constexpr int PA = WBM + E, PB = BN + E;
+  constexpr int ASZ = BK * PA, BSZ = BK * PB;
   constexpr int ST = 3;
   __shared__ __align__(16) T As[ST][ASZ];
   __shared__ __align__(16) T Bs[ST][BSZ];
@@ -1014,10 +1023,11 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   const int N = taps * a.Ci;
   // one split's pixel range per run of workgroups on an XCD
   const TileId tl = xcd_tile(false);
-  const int m0 = tl.x * BM, n0 = tl.y * BN;
+  const int m0 = tl.x * WBM, n0 = tl.y * BN;
   const int kbeg = tl.z * kchunk;
   const int kend = min(K, kbeg + kchunk);
   const int rv = tid % RV, kk0 = tid / RV;
+  const int rva = tid % RVA, kka0 = tid / RVA;
   const T *dc = (const T *)a.dc;
   const T *src = (const T *)a.src.p;
   const long long srow = (long long)a.src.W * a.src.C;
@@ -1026,13 +1036,13 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   const int nb0 = n0 + rv * E;
   const int tapv = nb0 / a.Ci, cv = nb0 - (nb0 / a.Ci) * a.Ci;
   const int tiv = tapv / a.kw, tjv = tapv - (tapv / a.kw) * a.kw;
-  const int ov = m0 + rv * E;
+  const int ov = m0 + rva * E;
 
   union V16 {
     uint4 u;
     T e[E];
   };
-  V16 ra[2], rb[2];
+  V16 ra[NPA], rb[2];
   int k0 = kbeg;
   const bool ovok = ov < a.Co, nbok = nb0 < N;
   const float invW = 1.0f / (float)a.Wv, invR = 1.0f / (float)R;
@@ -1055,10 +1065,10 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int p = k0 + kk0 + KS * i;
-      const bool pk = p < kend;
+    for (int i = 0; i < NPA; ++i) {
       // A: E output channels of pixel p
+      const int p = k0 + kka0 + KSA * i;
+      const bool pk = p < kend;
       if (AVEC) {
         ra[i].u = load16z(dc, ((long long)p * a.Co + ov) * (long long)sizeof(T), pk & ovok);
       } else {
@@ -1066,7 +1076,12 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
         for (int e = 0; e < E; ++e)
           ra[i].e[e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
       }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
       // B: E input values of pixel p under the column's tap
+      const int p = k0 + kk0 + KS * i;
+      const bool pk = p < kend;
       int t, x, yy, b;
       divmod_rcp(pk ? p : 0, a.Wv, invW, t, x);
       divmod_rcp(t, R, invR, b, yy);
@@ -1094,19 +1109,11 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   };
   auto store = [&](int st) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int kk = kk0 + KS * i;
-      if (KM) {
-        *(uint4 *)(&As[st][kk * PA + rv * E]) = ra[i].u;
-        *(uint4 *)(&Bs[st][kk * PB + rv * E]) = rb[i].u;
-      } else {
+    for (int i = 0; i < NPA; ++i)
+      *(uint4 *)(&As[st][(kka0 + KSA * i) * PA + rva * E]) = ra[i].u;
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-          As[st][(rv * E + e) * LDK + kk] = ra[i].e[e];
-          Bs[st][(rv * E + e) * LDK + kk] = rb[i].e[e];
-        }
-      }
-    }
+    for (int i = 0; i < 2; ++i)
+      *(uint4 *)(&Bs[st][(kk0 + KS * i) * PB + rv * E]) = rb[i].u;
   };
 
   f32x16 acc[2][NB];
@@ -1117,7 +1124,8 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int wm = (wave & 1) * 64, wn = (wave >> 1) * (BN / 2);
+  const int wm = WBM == 128 ? (wave & 1) * 64 : 0;
+  const int wn = WBM == 128 ? (wave >> 1) * 64 : wave * 32;
   const int n = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   if (n > 0) {
     gload();
@@ -1129,7 +1137,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   }
   if (n > 2) gload();
   __syncthreads();
-  using FR = Frag<T, BN, 4, KM, KM>;
+  using FR = Frag<T, FBN, 4, 1, 1, WBM, BN>;
   FR f0, f1;
   if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
   int s1 = 1, s2 = 2;
@@ -1144,13 +1152,12 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
   };
-  constexpr int NDSW = KM ? 4 : 2 * 2 * E;
   auto step_full = [&](FR &cur, FR &nxt) {
     nxt.load(As[s1], Bs[s1], wm, wn, lane);
     store(s2);
     gload();
     cur.mma(acc);
-    interleave_step<FR::NMFMA, FR::NDSR, NDSW, 4>();
+    interleave_step<FR::NMFMA, FR::NDSR, NPA + 2, NPA + 2>();
     s1 = s2;
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
@@ -1234,15 +1241,22 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   const int kchunk = (KT + splits - 1) / splits * BK;
   splits = (K + kchunk - 1) / kchunk;
   const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
-  dim3 grid((a.Co + BM - 1) / BM, (N + 127) / 128, splits);
+  const int wbm = wgrad_tile_rows(a.Co);
+  dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
   int pr = -1;
   if (prof::on)
     pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                          (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
-  if (avec && bvec) wgrad_kernel<T, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
-  else if (avec) wgrad_kernel<T, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
-  else wgrad_kernel<T, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  if (wbm == 64) {
+    if (avec && bvec) wgrad_kernel<T, 64, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else if (avec) wgrad_kernel<T, 64, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else wgrad_kernel<T, 64, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  } else {
+    if (avec && bvec) wgrad_kernel<T, 128, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else if (avec) wgrad_kernel<T, 128, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else wgrad_kernel<T, 128, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  }
   prof::end(pr, s);
   if (splits > 1) {
     long long mn = (long long)a.Co * N;

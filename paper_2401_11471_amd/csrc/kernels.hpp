@@ -114,10 +114,13 @@ struct WgradArgs {
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels
 inline int wgrad_k_iters(long long K, int es) { return (int)((K + 64 / es - 1) / (64 / es)); }
+// rows of a weight-gradient tile (output channels): 64 for narrow layers
+inline int wgrad_tile_rows(int Co) { return Co <= 64 ? 64 : 128; }
 // weight gradient: Co x N outputs (N = taps * C_in) over K pixels
 inline int wgrad_split_count(int Co, long long N, long long K, size_t cap, int es) {
-  const long long tiles = ((Co + 127) / 128) * ((N + 127) / 128);
-  SplitCost c{es == 2 ? 1.1 : 1.5, 3, 12.0};
+  const int tr = wgrad_tile_rows(Co);
+  const long long tiles = ((Co + tr - 1) / tr) * ((N + 127) / 128);
+  SplitCost c{(es == 2 ? 1.1 : 1.5) * (tr == 64 ? 0.55 : 1.0), 3, 12.0};
   return split_count(tiles, wgrad_k_iters(K, es), (long long)Co * N, cap, c);
 }
 
