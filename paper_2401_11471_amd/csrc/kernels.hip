@@ -549,8 +549,6 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
 
-  // two register buffers: the global loads of tile t+4 are issued in step t
-  // and written to LDS in step t+2, so a load has two steps to arrive
   uint4 ra[NA], rb[NBL];
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
