@@ -55,6 +55,10 @@ def parse():
                     help="largest-batch study instead of the throughput line: the "
                          "largest layer-wise and row-centric batches that fit the free "
                          "device memory (planner search), each confirmed by one step")
+    ap.add_argument("--sweep-bands", default="",
+                    help="band-count study instead of the throughput line: comma-separated "
+                         "N values; for each, the CARRY and RECOMPUTE steps' speed, peak "
+                         "activation bytes, shared rows and halo rows (use with --batch)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a "
                          "known-size reference for hardware byte counters)")
@@ -219,6 +223,83 @@ def max_batch_study(args):
     print(json.dumps(out), flush=True)
 
 
+def band_sweep(args):
+    """Row granularity study (the paper's N sweep, Section V): for every band
+    count N, the row-centric step in both modes -- images/s, peak activation
+    bytes (allocator peak of workspace + y), the rows kept between bands
+    (two-phase sharing) and the rows computed twice (overlapping partition)
+    -- against the layer-wise step of the same batch."""
+    import torch
+    from paper_2401_11471_amd import lrcnn as L
+    from paper_2401_11471_amd.device import DeviceModel
+    from workloads import CONFIGS, config_inputs, BF16
+
+    c = dict(CONFIGS[args.config])
+    if args.batch:
+        c["batch"] = args.batch
+    nodes, inp = config_inputs(args.config, batch=c["batch"])
+    B, H, W, Cin = inp.x.shape
+    dm = DeviceModel.from_inputs(nodes, inp)
+    p1 = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, 1)
+    out_shape = (B,) + p1.node_shape(len(nodes) - 1)
+    dy = dm.to_device(inp.grad(out_shape))
+
+    def run(make_step, ws_bytes):
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        ws = dm.workspace(ws_bytes)
+        y = dm.empty(out_shape)
+        step = make_step(ws, y)
+        step()
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - base
+        ms, _, g = timed_steps(torch, step, args.steps, args.warmup, args.eager)
+        del g, ws, y
+        return ms, int(peak)
+
+    def rc_step(plan):
+        return lambda ws, y: (lambda: (
+            L.lrcnn_forward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, y, ws),
+            L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, ws)))
+
+    lw_ms, lw_peak = run(lambda ws, y: (lambda: L.lrcnn_layerwise_reference_gpu(
+        p1, dm.x, dm.w, dm.sc, dm.sf, dy, y, dm.dw, None, ws)),
+        p1.info()["layerwise_workspace_bytes"])
+    res = []
+    for nb in [int(v) for v in args.sweep_bands.split(",") if v.strip()]:
+        ent = {"n_bands": nb}
+        for mode, key in ((L.CARRY, "carry"), (L.RECOMPUTE, "recompute")):
+            try:
+                plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, mode, nb)
+            except L.LrcnnError as ex:
+                ent[key] = {"error": str(ex)[:120]}
+                continue
+            info = plan.info()
+            ms, peak = run(rc_step(plan), info["workspace_bytes"])
+            ent[key] = {"images_per_s": round(B * 1000.0 / ms, 3), "ms_per_step": round(ms, 3),
+                        "peak_act_bytes": peak,
+                        "mem_ratio_layerwise_over_rows": round(lw_peak / peak, 3),
+                        "flops_over_layerwise": round(info["flops_rows"] /
+                                                      info["flops_layerwise"], 3),
+                        "shared_rows": info["shared_rows"], "halo_rows": info["halo_rows"],
+                        "strip_bytes": info["strip_bytes"]}
+        print(f"sweep N={nb}: " + ", ".join(
+            f"{k} {v.get('images_per_s')} img/s {v.get('peak_act_bytes')} B"
+            for k, v in ent.items() if isinstance(v, dict)), file=sys.stderr, flush=True)
+        res.append(ent)
+    out = {"metric": "row granularity study: training images/s and peak activation bytes vs N",
+           "n_gpus": 1, "dtype": "bf16" if inp.dtype == BF16 else "f32",
+           "config": {"workload": c["name"], "net": c["net"], "batch": B,
+                      "input": [Cin, H, W]},
+           "steps": args.steps, "warmup": args.warmup,
+           "layerwise": {"images_per_s": round(B * 1000.0 / lw_ms, 3),
+                         "ms_per_step": round(lw_ms, 3), "peak_act_bytes": lw_peak},
+           "sweep": res}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -230,6 +311,9 @@ def main():
 
     if args.max_batch:
         max_batch_study(args)
+        return
+    if args.sweep_bands:
+        band_sweep(args)
         return
 
     import torch
