@@ -72,6 +72,7 @@ struct Run {
   std::vector<View> act;   // current feature-map view of every node
   std::vector<View> dlt;   // current float32 error view of every node
   std::vector<int> first_consumer;
+  std::vector<char> dw_set;  // per conv: a band has written its weight gradient
   hipStream_t side = nullptr;  // weight-gradient stream (backward only)
   bool wg_pending = false;     // a weight gradient on `side` not yet joined
   bool dx_f32 = false;         // store dL/dx as float32 (a checkpoint's error)
@@ -372,6 +373,8 @@ struct Run {
       g.Hs = su.h;
       g.Ws = su.w;
       g.kh = d.kh, g.kw = d.kw, g.sh = d.sh, g.sw = d.sw, g.ph = d.ph, g.pw = d.pw;
+      g.overwrite = dw_set[v] ? 0 : 1;
+      dw_set[v] = 1;
       if (side) {
         LAUNCH(hipEventRecord((hipEvent_t)P.ev_act, (hipStream_t)stream), "event record");
         LAUNCH(hipStreamWaitEvent(side, (hipEvent_t)P.ev_act, 0), "stream wait");
@@ -499,18 +502,11 @@ struct Run {
     return LRCNN_OK;
   }
 
-  int zero_dw(float *const *dw) {
-    for (int v = 1; v < P.n; ++v)
-      if (P.nodes[v].op == LRCNN_OP_CONV) {
-        const lrcnn_node &d = P.nodes[v];
-        if (L.cpad && d.in0 == 0) {
-          size_t cnt = (size_t)d.c_out * d.kh * d.kw * L.cpad;
-          LAUNCH(launch_zero_f32((float *)(ws + L.dwpad[v]), cnt, stream), "zero dW");
-          continue;
-        }
-        size_t cnt = (size_t)d.c_out * d.kh * d.kw * P.shp[d.in0].c;
-        LAUNCH(launch_zero_f32(dw[v], cnt, stream), "zero dW");
-      }
+  // The first band that computes a conv's weight gradient writes it, later
+  // bands add to it (Algorithm 1 resets g before the BP loop), so no
+  // separate zeroing pass is needed.
+  int begin_dw() {
+    dw_set.assign(P.n, 0);
     return LRCNN_OK;
   }
 
@@ -621,7 +617,7 @@ int hybrid_backward(Plan &P, const void *x, const void *const *w, const float *c
   if (!g_dry && ensure_side(C)) run.side = (hipStream_t)C.side_stream;
   int st;
   if ((st = run.band_fwd(0, nullptr, nullptr, true, false, true)) != LRCNN_OK) return st;
-  if ((st = run.zero_dw(dw + c)) != LRCNN_OK) return st;
+  if ((st = run.begin_dw()) != LRCNN_OK) return st;
   if ((st = run.band_bwd(0, dy, dw + c, ws + P.h_dck, nullptr)) != LRCNN_OK) return st;
   if ((st = run.finish_dw(dw + c)) != LRCNN_OK) return st;
   return lrcnn_backward_rows(reinterpret_cast<lrcnn_plan_t *>(P.row), x, w, sc, sf,
@@ -685,7 +681,7 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
                       "CARRY backward needs a preceding lrcnn_forward_rows on this plan and workspace");
   Run run(P, P.rc, carry ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale, aff_shift, stream);
   if (!g_dry && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
-  if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
+  if ((st = run.begin_dw()) != LRCNN_OK) return st;
   float *dxacc = nullptr;
   if (!carry && dx) {
     const Shape &s = P.shp[0];
@@ -734,7 +730,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
   // FP keeps every node's full map; BP reads them without recomputing.
   // The pool argmax is produced in FP (bp = true selects its buffer).
   if ((st = run.band_fwd(0, y, mask_out, true)) != LRCNN_OK) return st;
-  if ((st = run.zero_dw(dw)) != LRCNN_OK) return st;
+  if ((st = run.begin_dw()) != LRCNN_OK) return st;
   if ((st = run.band_bwd(0, dy, dw, dx, nullptr)) != LRCNN_OK) return st;
   return run.finish_dw(dw);
 }

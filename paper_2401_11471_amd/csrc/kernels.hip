@@ -1186,18 +1186,20 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
         const int nn = n0 + wn + 32 * j + col;
         if (nn >= N) continue;
         float *d = out + (long long)m * N + nn;
-        if (gridDim.z == 1) *d += acc[i][j][v];
+        if (gridDim.z == 1) *d = a.overwrite ? acc[i][j][v] : *d + acc[i][j][v];
         else *d = acc[i][j][v];
       }
     }
 }
 
-// dW += sum over the split partial sums in a fixed order (deterministic):
+// dW += (first band: dW =) sum over the split partial sums in a fixed order
+// (deterministic):
 // eight groups of threads each add the splits z = g, g + 8, ... of 32
 // vectors of V elements, then the eight group sums are added in order.
 template <int V>
 __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, float *dw,
-                                                           long long mn, int splits) {
+                                                           long long mn, int splits,
+                                                           int overwrite) {
   __shared__ float red[8][32 * 4];
   const int g = threadIdx.x >> 5, e = threadIdx.x & 31;
   const long long i = ((long long)blockIdx.x * 32 + e) * V;
@@ -1218,9 +1220,14 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, fl
     for (int gg = 0; gg < 8; ++gg)
 #pragma unroll
       for (int k = 0; k < V; ++k) sum[k] += red[gg][e * 4 + k];
-    ldv<float, V>(dw + i, q);
+    if (overwrite) {
 #pragma unroll
-    for (int k = 0; k < V; ++k) q[k] += sum[k];
+      for (int k = 0; k < V; ++k) q[k] = sum[k];
+    } else {
+      ldv<float, V>(dw + i, q);
+#pragma unroll
+      for (int k = 0; k < V; ++k) q[k] += sum[k];
+    }
     stv<float, V>(dw + i, q);
   }
 }
@@ -1261,9 +1268,10 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
     int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
     if (mn % 4 == 0)
       wgrad_reduce_kernel<4><<<(unsigned)((mn / 4 + 31) / 32), 256, 0, s>>>(a.out, dw, mn,
-                                                                            splits);
+                                                                            splits, a.overwrite);
     else
-      wgrad_reduce_kernel<1><<<(unsigned)((mn + 31) / 32), 256, 0, s>>>(a.out, dw, mn, splits);
+      wgrad_reduce_kernel<1><<<(unsigned)((mn + 31) / 32), 256, 0, s>>>(a.out, dw, mn, splits,
+                                                                        a.overwrite);
     prof::end(p2, s);
   }
   return (int)hipGetLastError();

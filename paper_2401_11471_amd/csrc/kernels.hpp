@@ -110,6 +110,7 @@ struct WgradArgs {
   size_t part_bytes;  // capacity of `out`
   int B, y0, y1, Wv, Co, Ci, Hs, Ws;
   int kh, kw, sh, sw, ph, pw;
+  int overwrite;  // 1: dw = this launch's sum (the first band); 0: dw += it
 };
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels
