@@ -49,7 +49,7 @@ def bench_name(mangled: str) -> str:
         return (f"conv_gemm_kernel<{m.group(1)}, {m.group(2)}, "
                 f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, "
                 f"{'vec' if m.group(4) == 'true' else 'scalar'}>")
-    m = re.match(r"wgrad_kernel<(\w+), (true|false), (true|false)>", n)
+    m = re.match(r"wgrad_kernel<(\w+), (?:\d+, )?(true|false), (true|false)>", n)
     if m:
         vec = m.group(2) == "true" and m.group(3) == "true"
         return f"wgrad_kernel<{m.group(1)}, {'vec' if vec else 'scalar'}>"
