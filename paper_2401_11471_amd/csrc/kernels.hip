@@ -917,9 +917,10 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
   const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0);
-  const int bn = a.N <= 64 ? 64 : 128;
   const int KT = a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
-  const int splits = conv_split_count(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
+  const ConvTiles ct = conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
+  const int bn = ct.bn;
+  const int splits = ct.splits;
   a.kts = (KT + splits - 1) / splits;
   dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
   int pr = -1;

@@ -59,9 +59,12 @@ struct SplitCost {
   int occ;          // workgroups one CU holds (LDS bound)
   double fixed_us;  // per-launch fixed cost
 };
-inline int split_count(long long tiles, int KT, long long part_elems, size_t cap,
-                       const SplitCost &c) {
-  if (tiles <= 0 || KT <= 1) return 1;
+struct SplitChoice {
+  int s;
+  double us;  // estimated duration
+};
+inline SplitChoice split_choice(long long tiles, int KT, long long part_elems, size_t cap,
+                                const SplitCost &c) {
   auto cost = [&](long long s) {
     const long long wg = tiles * s;
     const long long per_cu = (wg + 255) / 256;
@@ -71,27 +74,43 @@ inline int split_count(long long tiles, int KT, long long part_elems, size_t cap
     if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
     return t;
   };
-  long long best = 1;
-  double bt = cost(1);
+  SplitChoice best{1, cost(1)};
+  if (tiles <= 0 || KT <= 1) return best;
   for (long long s = 2; s <= 128 && s <= KT / 2; ++s) {
     if ((size_t)s * (size_t)part_elems * 4 > cap) break;
     const long long kts = (KT + s - 1) / s;
     if ((KT + kts - 1) / kts != s) continue;  // same work as a smaller s
     const double t = cost(s);
-    if (t < bt * 0.98) {
-      bt = t;
-      best = s;
-    }
+    if (t < best.us * 0.98) best = SplitChoice{(int)s, t};
   }
-  return (int)best;
+  return best;
 }
-// conv forward / input gradient: M x N outputs, KT K iterations
+inline int split_count(long long tiles, int KT, long long part_elems, size_t cap,
+                       const SplitCost &c) {
+  return split_choice(tiles, KT, part_elems, cap, c).s;
+}
+// Tile width and split count of a convolution launch (forward or input
+// gradient, M x N outputs, KT K iterations): 128-row tiles, 64 or 128
+// columns wide. Narrow tiles double the workgroup count of a launch, which
+// fills the CUs better when a band gives only a few hundred 128 x 128
+// tiles; the cheaper of the two estimates is taken (wide unless narrow
+// saves at least 5%).
+struct ConvTiles {
+  int bn, splits;
+};
+inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es) {
+  const double f = es == 2 ? 0.75 : 1.0;
+  const long long mt = (M + 127) / 128;
+  SplitChoice n64 = split_choice(mt * ((N + 63) / 64), KT, M * (long long)N, cap,
+                                 SplitCost{0.75 * f, 3, 5.0});
+  if (N <= 64) return ConvTiles{64, n64.s};
+  SplitChoice n128 = split_choice(mt * ((N + 127) / 128), KT, M * (long long)N, cap,
+                                  SplitCost{1.35 * f, 2, 5.0});
+  return n64.us < n128.us * 0.95 ? ConvTiles{64, n64.s} : ConvTiles{128, n128.s};
+}
+// split count of a convolution launch (the planner sizes partial sums with it)
 inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
-  const bool wide = N > 64;
-  const long long tiles = ((M + 127) / 128) * ((N + (wide ? 127 : 63)) / (wide ? 128 : 64));
-  SplitCost c{wide ? 1.35 : 0.75, wide ? 2 : 3, 5.0};
-  if (es == 2) c.step_us *= 0.75;
-  return split_count(tiles, KT, M * (long long)N, cap, c);
+  return conv_tiles(M, N, KT, cap, es).splits;
 }
 // K iterations of a conv for storage element size es (bytes); one
 // iteration covers LRCNN_CONV_KR 16-byte vectors of a tile row.
