@@ -54,6 +54,20 @@ int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 // kernels in kernels.hip. The count is the cheapest estimate whose partial
 // sums fit in `cap` bytes; it is shared by the launchers and the planner's
 // workspace sizing, so both always agree.
+// Constants of the launch-duration estimates (microseconds; measured on
+// gfx950 with the kernels of kernels.hip).
+#ifndef LRCNN_SHARE2
+#define LRCNN_SHARE2 0.8   // time factor of a workgroup sharing its CU with another
+#endif
+#ifndef LRCNN_STEP_N64
+#define LRCNN_STEP_N64 0.75  // one K iteration of a lone 128 x 64 tile (fp32)
+#endif
+#ifndef LRCNN_STEP_N128
+#define LRCNN_STEP_N128 1.35  // one K iteration of a lone 128 x 128 tile (fp32)
+#endif
+#ifndef LRCNN_NARROW_GAIN
+#define LRCNN_NARROW_GAIN 1.0  // narrow tiles must beat wide ones by this factor
+#endif
 struct SplitCost {
   double step_us;   // one K iteration of a lone workgroup
   int occ;          // workgroups one CU holds (LDS bound)
@@ -69,7 +83,7 @@ inline SplitChoice split_choice(long long tiles, int KT, long long part_elems, s
     const long long wg = tiles * s;
     const long long per_cu = (wg + 255) / 256;
     const long long kts = (KT + s - 1) / s;
-    const double share = per_cu >= 2 && c.occ >= 2 ? 0.8 : 1.0;
+    const double share = per_cu >= 2 && c.occ >= 2 ? LRCNN_SHARE2 : 1.0;
     double t = (double)kts * (double)per_cu * c.step_us * share + c.fixed_us;
     if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
     return t;
@@ -93,8 +107,7 @@ inline int split_count(long long tiles, int KT, long long part_elems, size_t cap
 // gradient, M x N outputs, KT K iterations): 128-row tiles, 64 or 128
 // columns wide. Narrow tiles double the workgroup count of a launch, which
 // fills the CUs better when a band gives only a few hundred 128 x 128
-// tiles; the cheaper of the two estimates is taken (wide unless narrow
-// saves at least 5%).
+// tiles; the cheaper of the two estimates is taken.
 struct ConvTiles {
   int bn, splits;
 };
@@ -102,11 +115,11 @@ inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es) {
   const double f = es == 2 ? 0.75 : 1.0;
   const long long mt = (M + 127) / 128;
   SplitChoice n64 = split_choice(mt * ((N + 63) / 64), KT, M * (long long)N, cap,
-                                 SplitCost{0.75 * f, 3, 5.0});
+                                 SplitCost{LRCNN_STEP_N64 * f, 3, 5.0});
   if (N <= 64) return ConvTiles{64, n64.s};
   SplitChoice n128 = split_choice(mt * ((N + 127) / 128), KT, M * (long long)N, cap,
-                                  SplitCost{1.35 * f, 2, 5.0});
-  return n64.us < n128.us * 0.95 ? ConvTiles{64, n64.s} : ConvTiles{128, n128.s};
+                                  SplitCost{LRCNN_STEP_N128 * f, 2, 5.0});
+  return n64.us < n128.us * LRCNN_NARROW_GAIN ? ConvTiles{64, n64.s} : ConvTiles{128, n128.s};
 }
 // split count of a convolution launch (the planner sizes partial sums with it)
 inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {

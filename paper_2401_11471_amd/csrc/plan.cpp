@@ -316,7 +316,10 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   const int vec_e = 16 / P.es;
   L.cpad = P.shp[0].c % vec_e ? (P.shp[0].c + vec_e - 1) / vec_e * vec_e : 0;
   int xrows = 0;
-  const size_t pcap = (size_t)24 << 20;
+#ifndef LRCNN_PART_MIB
+#define LRCNN_PART_MIB 24
+#endif
+  const size_t pcap = (size_t)LRCNN_PART_MIB << 20;
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
