@@ -13,6 +13,8 @@ Modules:
   rows    -- the row-partitioned runner (two-phase sharing and overlapping
              partitioning) with its own interval arithmetic
   brute   -- scalar loops for tiny shapes that pin ``column``
+  head    -- classifier head, softmax cross-entropy and SGD of a full training
+             step (Algorithm 1's fully connected FP/BP, loss and update)
 
 Parity status: every function is pinned by tests in ``tests/test_oracle_*``
 (brute force, library routines, adjoint identities, finite differences,
