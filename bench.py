@@ -59,6 +59,12 @@ def parse():
                     help="band-count study instead of the throughput line: comma-separated "
                          "N values; for each, the CARRY and RECOMPUTE steps' speed, peak "
                          "activation bytes, shared rows and halo rows (use with --batch)")
+    ap.add_argument("--train-steps", type=int, default=0,
+                    help="full-training study instead of the throughput line: this many "
+                         "SGD steps (classifier head, softmax cross-entropy, update) of the "
+                         "row-centric and the layer-wise step from the same initial values "
+                         "on one synthetic labelled batch; prints both loss curves")
+    ap.add_argument("--lr", type=float, default=1e-5)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a "
                          "known-size reference for hardware byte counters)")
@@ -300,6 +306,60 @@ def band_sweep(args):
     print(json.dumps(out), flush=True)
 
 
+def train_study(args):
+    """Loss curves of full training steps (Algorithm 1 with its fully
+    connected head, loss and update): row-centric against layer-wise, same
+    initial parameters, one synthetic batch with random labels (10 classes);
+    also the time of a full row-centric training step."""
+    import numpy as np
+    import torch
+    from paper_2401_11471_amd import lrcnn as L
+    from paper_2401_11471_amd.device import DeviceModel
+    from paper_2401_11471_amd.train import Trainer
+    from workloads import CONFIGS, config_inputs, BF16
+
+    c = dict(CONFIGS[args.config])
+    if args.batch:
+        c["batch"] = args.batch
+    nb = args.bands or c["bands"]
+    nodes, inp = config_inputs(args.config, batch=c["batch"])
+    B, H, W, Cin = inp.x.shape
+    g = np.random.default_rng(args.config)
+    labels = g.integers(0, 10, B)
+    out = {"metric": "training loss per SGD step (classifier head, softmax cross-entropy)",
+           "n_gpus": 1, "dtype": "bf16" if inp.dtype == BF16 else "f32",
+           "config": {"workload": c["name"], "net": c["net"], "batch": B, "bands": nb,
+                      "classes": 10, "lr": args.lr},
+           "data": "synthetic N(0,1) inputs, random labels"}
+    for key, lw in (("row_centric", False), ("layerwise", True)):
+        plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, nb)
+        oh, ow, oc = plan.node_shape(len(nodes) - 1)
+        k = oh * ow * oc
+        gh = np.random.default_rng(7)
+        fw = (gh.standard_normal((10, k)) / np.sqrt(k)).astype(np.float32)
+        fb = np.zeros(10, np.float32)
+        dm = DeviceModel.from_inputs(nodes, inp)
+        tr = Trainer(plan, dm, fw, fb, labels, layerwise=lw)
+        losses = []
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.train_steps):
+            losses.append(tr.step(args.lr).clone())
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.train_steps
+        out[key] = {"losses": [round(float(v.item()), 6) for v in losses],
+                    "ms_per_step": round(ms, 3), "images_per_s": round(B * 1000.0 / ms, 3)}
+        print(f"train {key}: loss {losses[0].item():.4f} -> {losses[-1].item():.4f}, "
+              f"{ms:.2f} ms/step", file=sys.stderr, flush=True)
+        del tr, dm
+        torch.cuda.empty_cache()
+    a, b = np.array(out["row_centric"]["losses"]), np.array(out["layerwise"]["losses"])
+    out["max_rel_loss_difference"] = float(np.max(np.abs(a - b) / np.abs(b)))
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -314,6 +374,9 @@ def main():
         return
     if args.sweep_bands:
         band_sweep(args)
+        return
+    if args.train_steps:
+        train_study(args)
         return
 
     import torch

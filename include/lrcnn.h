@@ -269,6 +269,43 @@ int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
                                   void *dx, void *workspace, size_t ws_bytes,
                                   void *const *mask_out, void *stream);
 
+/* ---- Full training step: classifier head, loss, update (Algorithm 1:
+ * fully connected FP, Loss, fully connected BP after the last band's FP, and
+ * the parameter update once every band's BP is done). Readings: one fully
+ * connected layer over the trunk output flattened per image in NHWC order
+ * (K = H_L * W_L * C_L features), softmax cross-entropy averaged over the
+ * batch, plain SGD; the fixed affine parameters are not trained. */
+
+/* Device scratch bytes lrcnn_head_loss needs for n_classes classes (1..64).
+ * Errors: EINVAL. */
+int lrcnn_head_workspace_bytes(const lrcnn_plan_t *plan, int32_t n_classes,
+                               size_t *bytes);
+
+/* y: the trunk output written by lrcnn_forward_rows (plan dtype,
+ * [B][H_L][W_L][C_L]); fc_w: float32 [n_classes][K]; fc_b: float32
+ * [n_classes]; labels: int32 [B] in [0, n_classes). Writes logits (float32
+ * [B][n_classes]), loss (one float32: the batch mean), dy = dL/dy (plan
+ * dtype, shape of y: the upstream gradient for lrcnn_backward_rows),
+ * d_fc_w and d_fc_b (float32, overwritten). head_ws: device scratch of
+ * lrcnn_head_workspace_bytes. A label outside [0, n_classes) makes the loss
+ * NaN (nothing is read out of bounds). All device pointers 16-byte aligned.
+ * Errors: EINVAL, EWORKSPACE, EHIP. */
+int lrcnn_head_loss(const lrcnn_plan_t *plan, const void *y, const float *fc_w,
+                    const float *fc_b, const int32_t *labels, int32_t n_classes,
+                    float *logits, float *loss, void *dy, float *d_fc_w,
+                    float *d_fc_b, void *head_ws, size_t head_ws_bytes,
+                    void *stream);
+
+/* theta <- theta - lr * g for every conv node's weights w[v] (plan dtype,
+ * updated in float32 and rounded to the storage dtype) with dw[v] (float32,
+ * from lrcnn_backward_rows), and, when fc_w is not NULL, for the head
+ * (fc_w, fc_b with d_fc_w, d_fc_b; n_classes classes). Errors: EINVAL,
+ * EHIP. */
+int lrcnn_sgd_update(const lrcnn_plan_t *plan, float lr, void *const *w,
+                     float *const *dw, float *fc_w, const float *d_fc_w,
+                     float *fc_b, const float *d_fc_b, int32_t n_classes,
+                     void *stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *lrcnn_last_error(void);
 

@@ -96,6 +96,9 @@ def _load():
     lib.lrcnn_backward_rows.argtypes = [vp, vp, pp, pp, pp, vp, pp, vp, vp, sz, vp]
     lib.lrcnn_layerwise_reference_gpu.argtypes = [vp, vp, pp, pp, pp, vp, vp, pp, vp,
                                                   vp, sz, pp, vp]
+    lib.lrcnn_head_workspace_bytes.argtypes = [vp, i32, C.POINTER(sz)]
+    lib.lrcnn_head_loss.argtypes = [vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.lrcnn_sgd_update.argtypes = [vp, C.c_float, pp, pp, vp, vp, vp, vp, i32, vp]
     lib.lrcnn_last_error.restype = C.c_char_p
     lib.lrcnn_debug_dry_run.argtypes = [C.c_int]
     lib.lrcnn_debug_dry_run.restype = None
@@ -109,7 +112,8 @@ def _load():
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
               "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
               "lrcnn_layerwise_reference_gpu", "lrcnn_plan_step_bytes",
-              "lrcnn_plan_for_budget", "lrcnn_max_batch"):
+              "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_head_workspace_bytes",
+              "lrcnn_head_loss", "lrcnn_sgd_update"):
         getattr(lib, f).restype = C.c_int
     return lib
 
@@ -119,7 +123,8 @@ LIB = _load()
 # Names the header declares (checked by the tests against the shared object).
 EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_plan_step_bytes",
-           "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_forward_rows",
+           "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_head_workspace_bytes",
+           "lrcnn_head_loss", "lrcnn_sgd_update", "lrcnn_forward_rows",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
            "lrcnn_debug_dry_run", "lrcnn_debug_profile", "lrcnn_debug_profile_collect",
            "lrcnn_debug_profile_entry")
@@ -255,6 +260,31 @@ def lrcnn_layerwise_reference_gpu(plan, x, weights, scales, shifts, dy, y, dws, 
         _ptr_array(shifts), _ptr(dy), _ptr(y), _ptr_array(dws), _ptr(dx),
         _ptr(workspace), workspace.numel(),
         _ptr_array(masks) if masks is not None else None, _stream(stream)))
+
+
+def lrcnn_head_workspace_bytes(plan, n_classes):
+    out = C.c_size_t()
+    _check(LIB.lrcnn_head_workspace_bytes(plan.handle, n_classes, C.byref(out)))
+    return out.value
+
+
+def lrcnn_head_loss(plan, y, fc_w, fc_b, labels, logits, loss, dy, d_fc_w, d_fc_b, head_ws,
+                    stream=None):
+    """Classifier head + softmax cross-entropy: logits, loss, dL/dy, head
+    gradients (all device tensors; n_classes = fc_w.shape[0])."""
+    _check(LIB.lrcnn_head_loss(
+        plan.handle, _ptr(y), _ptr(fc_w), _ptr(fc_b), _ptr(labels), fc_w.shape[0],
+        _ptr(logits), _ptr(loss), _ptr(dy), _ptr(d_fc_w), _ptr(d_fc_b), _ptr(head_ws),
+        head_ws.numel(), _stream(stream)))
+
+
+def lrcnn_sgd_update(plan, lr, weights, dws, fc_w=None, d_fc_w=None, fc_b=None, d_fc_b=None,
+                     stream=None):
+    """theta -= lr * g for every conv weight and (when given) the head."""
+    n_classes = fc_w.shape[0] if fc_w is not None else 0
+    _check(LIB.lrcnn_sgd_update(
+        plan.handle, C.c_float(lr), _ptr_array(weights), _ptr_array(dws), _ptr(fc_w),
+        _ptr(d_fc_w), _ptr(fc_b), _ptr(d_fc_b), n_classes, _stream(stream)))
 
 
 def lrcnn_debug_dry_run(on):
