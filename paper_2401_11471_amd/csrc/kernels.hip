@@ -1242,12 +1242,13 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   // quotients)
   if ((long long)a.B * (a.y1 - a.y0) >= (1LL << 22)) return (int)hipErrorInvalidValue;
   constexpr int BK = Cfg<T>::BK;
-  int splits = wgrad_split_count(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
+  const WgradTiles wt = wgrad_tiles(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
+  int splits = wt.splits;
   const int KT = (K + BK - 1) / BK;
   const int kchunk = (KT + splits - 1) / splits * BK;
   splits = (K + kchunk - 1) / kchunk;
   const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
-  const int wbm = wgrad_tile_rows(a.Co);
+  const int wbm = wt.rows;
   dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
   int pr = -1;
   if (prof::on)

@@ -147,14 +147,32 @@ struct WgradArgs {
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels
 inline int wgrad_k_iters(long long K, int es) { return (int)((K + 64 / es - 1) / (64 / es)); }
-// rows of a weight-gradient tile (output channels): 64 for narrow layers
-inline int wgrad_tile_rows(int Co) { return Co <= 64 ? 64 : 128; }
-// weight gradient: Co x N outputs (N = taps * C_in) over K pixels
+// Rows (output channels) and split count of a weight-gradient tile of a
+// launch with Co x N outputs (N = taps * C_in) over K pixels: 64-row tiles
+// for layers with at most 64 output channels; otherwise, in bfloat16, the
+// cheaper estimate of 64- and 128-row tiles (narrow tiles give more
+// workgroups when a layer has few output tiles; measured faster on the
+// ResNet-50 bands), and in float32 128 rows (measured faster on VGG-16).
+#ifndef LRCNN_WG_NARROW
+#define LRCNN_WG_NARROW 1
+#endif
+struct WgradTiles {
+  int rows, splits;
+};
+inline WgradTiles wgrad_tiles(int Co, long long N, long long K, size_t cap, int es) {
+  const double f = es == 2 ? 1.1 : 1.5;
+  const int KT = wgrad_k_iters(K, es);
+  const long long nt = (N + 127) / 128;
+  const SplitChoice r64 = split_choice(((Co + 63) / 64) * nt, KT, (long long)Co * N, cap,
+                                       SplitCost{f * 0.55, 3, 12.0});
+  if (Co <= 64) return WgradTiles{64, r64.s};
+  const SplitChoice r128 = split_choice(((Co + 127) / 128) * nt, KT, (long long)Co * N, cap,
+                                        SplitCost{f, 3, 12.0});
+  if (LRCNN_WG_NARROW && es == 2 && r64.us < r128.us) return WgradTiles{64, r64.s};
+  return WgradTiles{128, r128.s};
+}
 inline int wgrad_split_count(int Co, long long N, long long K, size_t cap, int es) {
-  const int tr = wgrad_tile_rows(Co);
-  const long long tiles = ((Co + tr - 1) / tr) * ((N + 127) / 128);
-  SplitCost c{(es == 2 ? 1.1 : 1.5) * (tr == 64 ? 0.55 : 1.0), 3, 12.0};
-  return split_count(tiles, wgrad_k_iters(K, es), (long long)Co * N, cap, c);
+  return wgrad_tiles(Co, N, K, cap, es).splits;
 }
 
 struct PoolArgs {
