@@ -921,6 +921,9 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   const ConvTiles ct = conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
   const int bn = ct.bn;
   const int splits = ct.splits;
+  // split partial sums must fit the buffer (the schedule never exceeds it)
+  if (splits > 1 && (!a.part || (size_t)splits * (size_t)M * (size_t)a.N * 4 > a.part_bytes))
+    return (int)hipErrorInvalidValue;
   a.kts = (KT + splits - 1) / splits;
   dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
   int pr = -1;
@@ -1247,6 +1250,8 @@ static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
   const int KT = (K + BK - 1) / BK;
   const int kchunk = (KT + splits - 1) / splits * BK;
   splits = (K + kchunk - 1) / kchunk;
+  if (splits > 1 && (!a.out || (size_t)splits * (size_t)a.Co * (size_t)N * 4 > a.part_bytes))
+    return (int)hipErrorInvalidValue;
   const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
   const int wbm = wt.rows;
   dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
