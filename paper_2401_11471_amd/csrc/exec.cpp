@@ -326,9 +326,10 @@ struct Run {
     {
       int r0, r1;
       in_rows(d, su.h, a, b, r0, r1);
-      bool ok = holds(act[v], a, b) && holds(dlt[v], a, b) && holds(act[u], r0, r1) &&
-                holds(dlt[u], r0, r1);
-      if (d.op == LRCNN_OP_ADD) ok = ok && holds(act[d.in1], r0, r1) && holds(dlt[d.in1], r0, r1);
+      bool ok = holds(act[v], a, b) && (fused(v) || holds(dlt[v], a, b)) &&
+                holds(act[u], r0, r1) && (fused(u) || holds(dlt[u], r0, r1));
+      if (d.op == LRCNN_OP_ADD)
+        ok = ok && holds(act[d.in1], r0, r1) && (fused(d.in1) || holds(dlt[d.in1], r0, r1));
       if (!ok)
         return lrcnn_fail(LRCNN_EINVAL, "internal: backward rows of node " + std::to_string(v) +
                                             " not held by its buffers");
@@ -343,9 +344,14 @@ struct Run {
                   L.carry_cap[v]};
         if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
       }
-      LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a, b,
-                            sv.w, sv.c, stream, carries ? &cv : nullptr, q.lo, q.a),
-             "error operand");
+      if (fused(v)) {
+        // the add's backward already wrote this conv's error operand
+        if (carries) return lrcnn_fail(LRCNN_EINVAL, "internal: fused conv carries rows");
+      } else {
+        LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a,
+                              b, sv.w, sv.c, stream, carries ? &cv : nullptr, q.lo, q.a),
+               "error operand");
+      }
       WgradArgs g{};
       g.dc = dc;
       g.src = act[u];
@@ -420,11 +426,31 @@ struct Run {
       p.kh = d.kh, p.kw = d.kw, p.sh = d.sh, p.sw = d.sw, p.ph = d.ph, p.pw = d.pw;
       LAUNCH(launch_pool_bwd(p, stream), "max-pool backward");
     } else {
-      LAUNCH(launch_add_bwd(dt, dlt[v], act[v], dlt[d.in0], dlt[d.in1], d.relu, B, a, b, sv.w,
+      AddSide side_in[2];
+      const int in_ids[2] = {d.in0, d.in1};
+      for (int k = 0; k < 2; ++k) {
+        const int x = in_ids[k];
+        AddSide &sd = side_in[k];
+        sd = AddSide{dlt[x], nullptr, nullptr, sv.c};
+        if (fused(x)) {
+          // own rows of the conv input equal the add's rows (1 x 1 window)
+          const Rows qx = band_rows(r, x);
+          if (qx.a != a || qx.b != b)
+            return lrcnn_fail(LRCNN_EINVAL, "internal: fused conv rows differ from the add's");
+          sd.dc = ws + L.dc[x];
+          sd.scale = P.nodes[x].affine ? sc[x] : nullptr;
+        }
+      }
+      LAUNCH(launch_add_bwd(dt, dlt[v], act[v], side_in[0], side_in[1], d.relu, B, a, b, sv.w,
                             sv.c, stream),
              "add backward");
     }
     return LRCNN_OK;
+  }
+
+  // a conv whose error operand the add's backward writes (no error window)
+  bool fused(int u) const {
+    return u > 0 && u < (int)P.fuse_add.size() && P.fuse_add[u] != 0;
   }
 
   // BP of band r after its feature maps are in place.
@@ -451,7 +477,7 @@ struct Run {
       }
       int ins[2] = {d.in0, d.op == LRCNN_OP_ADD ? d.in1 : -1};
       for (int u : ins)
-        if (u >= 0 && first_consumer[u] == v) {
+        if (u >= 0 && first_consumer[u] == v && !fused(u)) {
           int st = init_delta(r, u);
           if (st != LRCNN_OK) return st;
         }

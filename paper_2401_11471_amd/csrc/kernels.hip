@@ -1447,12 +1447,36 @@ int launch_add_fwd(int dt, View a, View b, View z, int relu, uint8_t *mask,
   return (int)hipGetLastError();
 }
 
+// One input side of the residual add's backward: either accumulate the
+// error into the input's float32 window (dc == nullptr), or, when the input
+// is a conv without ReLU whose only consumer is this add, write that conv's
+// error operand rnd(scale[c] * d) directly (contiguous own rows, the layout
+// act_bwd_kernel writes), which makes its window and its act_bwd pass
+// unnecessary.
 template <typename T, int V>
-__global__ void add_bwd_kernel(View dz, View z, View da, View db, int relu, RowIter it) {
+__device__ __forceinline__ void add_bwd_side(const AddSide &sd, long long idx, int in, int b,
+                                             int y, const float (&d)[4]) {
+  if (sd.dc) {
+    float e[4];
+#pragma unroll
+    for (int k = 0; k < V; ++k) e[k] = sd.scale ? d[k] * sd.scale[(in + k) % sd.C] : d[k];
+    stv<T, V>((T *)sd.dc + idx * V, e);
+  } else {
+    float x[4];
+    float *p = (float *)sd.win.p + view_off(sd.win, b, y, in);
+    ldv<float, V>(p, x);
+#pragma unroll
+    for (int k = 0; k < V; ++k) x[k] += d[k];
+    stv<float, V>(p, x);
+  }
+}
+
+template <typename T, int V>
+__global__ void add_bwd_kernel(View dz, View z, AddSide sa, AddSide sb, int relu, RowIter it) {
   GRID_STRIDE(idx, it.total) {
     int b, y, in;
     it.at(idx, V, b, y, in);
-    float d[4], zz[4], x[4];
+    float d[4], zz[4];
     ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
     if (relu) {
       ldv<T, V>((const T *)z.p + view_off(z, b, y, in), zz);
@@ -1460,32 +1484,24 @@ __global__ void add_bwd_kernel(View dz, View z, View da, View db, int relu, RowI
       for (int e = 0; e < V; ++e)
         if (!(zz[e] > 0.f)) d[e] = 0.f;
     }
-    float *pa = (float *)da.p + view_off(da, b, y, in);
-    ldv<float, V>(pa, x);
-#pragma unroll
-    for (int e = 0; e < V; ++e) x[e] += d[e];
-    stv<float, V>(pa, x);
-    float *pb = (float *)db.p + view_off(db, b, y, in);
-    ldv<float, V>(pb, x);
-#pragma unroll
-    for (int e = 0; e < V; ++e) x[e] += d[e];
-    stv<float, V>(pb, x);
+    add_bwd_side<T, V>(sa, idx, in, b, y, d);
+    add_bwd_side<T, V>(sb, idx, in, b, y, d);
   }
 }
 
-int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
-                   int y0, int y1, int W, int C, void *stream) {
+int launch_add_bwd(int dt, View dz, View z, const AddSide &sa, const AddSide &sb, int relu,
+                   int B, int y0, int y1, int W, int C, void *stream) {
   const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
   RowIter it = row_iter(B, y0, y1, W, C, V);
   if (it.total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
   const unsigned g = grid_for(it.total);
   if (dt == DT_F32) {
-    if (V == 4) add_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
-    else add_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+    if (V == 4) add_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
+    else add_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
   } else {
-    if (V == 4) add_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
-    else add_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, da, db, relu, it);
+    if (V == 4) add_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
+    else add_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
   }
   return (int)hipGetLastError();
 }

@@ -200,9 +200,18 @@ int launch_pool_bwd(const PoolBwdArgs &a, void *stream);
 int launch_add_fwd(int dt, View a, View b, View z, int relu, uint8_t *mask,
                    int mask_h, int B, int y0, int y1, int W, int C,
                    void *stream);
-// d = dz * [z > 0]; da += d; db += d (float32 windows) over rows [y0, y1).
-int launch_add_bwd(int dt, View dz, View z, View da, View db, int relu, int B,
-                   int y0, int y1, int W, int C, void *stream);
+// d = dz * [z > 0] over rows [y0, y1), sent to both inputs of the add:
+// win += d (float32 window), or, when dc is set, dc = rnd(scale[c] * d)
+// written contiguously over the rows (the error operand of a conv input
+// without ReLU whose only consumer is the add; scale nullable, C channels).
+struct AddSide {
+  View win;
+  void *dc;
+  const float *scale;
+  int C;
+};
+int launch_add_bwd(int dt, View dz, View z, const AddSide &sa, const AddSide &sb, int relu,
+                   int B, int y0, int y1, int W, int C, void *stream);
 // Error operand of a conv: dc = rnd(scale[c] * dz * [z > 0]) over rows
 // [y0, y1), written contiguously (storage dtype).
 // `carry` (nullable): also copy rows [c0, c1) of dz (float32) into it.

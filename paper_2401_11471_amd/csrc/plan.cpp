@@ -394,7 +394,9 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
     int nxt = 0;  // next conv in backward order
     for (int u = v - 1; u >= 1 && !nxt; --u)
       if (P.nodes[u].op == LRCNN_OP_CONV) nxt = u;
-    const int s0 = n - 1 - v, s1 = nxt ? n - 2 - nxt : n - 1;
+    // (a conv fed by an add's backward gets its error operand at the add's step)
+    const int s0 = n - 1 - (P.fuse_add.empty() || !P.fuse_add[v] ? v : P.fuse_add[v]);
+    const int s1 = nxt ? n - 2 - nxt : n - 1;
     dc_i[v] = (int)bufs.size();
     bufs.push_back(LiveBuf{s0, s1, P.elems(v, own[v]) * P.es, 0});
     if (wpn[v] > 0) {
@@ -505,6 +507,17 @@ static int build(Plan &P) {
   P.rows_fp = P.rows;
   if (carry) carry_rows(P, bb); else cone_rows(P, bb);
   const int nb = P.nb;
+  // convs whose error operand the residual add's backward can write
+  P.fuse_add.assign(n, 0);
+  for (int v = 1; v < n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV || d.relu || P.cons[v].size() != 1) continue;
+    const int c = P.cons[v][0];
+    if (P.nodes[c].op != LRCNN_OP_ADD || P.nodes[c].in0 == P.nodes[c].in1) continue;
+    bool ok = true;
+    for (int r = 0; r < nb && ok; ++r) ok = P.rows[r][v].lo == P.rows[r][v].a;
+    if (ok) P.fuse_add[v] = c;
+  }
   // capacities
   std::vector<int> cap(n, 0), own(n, 0), cry(n, 0), fcap(n, 0);
   for (int r = 0; r < nb; ++r)

@@ -66,6 +66,10 @@ struct Plan {
   std::vector<std::vector<Rows>> rows; // [backward band][node]
   std::vector<std::vector<Rows>> rows_fp;  // [forward band][node]
   std::vector<std::vector<int>> tail;  // CARRY: [backward band][node] first kept row
+  // per node: the ADD node whose backward writes this conv's error operand
+  // directly (a conv without ReLU whose only consumer is that add and that
+  // carries no rows between backward bands), else 0
+  std::vector<int> fuse_add;
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   double tau = 0, flops_rows = 0;
