@@ -115,7 +115,10 @@ struct Run {
   }
 
   // Forward of node v over rows [a, b) into `dst`.
-  int node_fwd(int v, int a, int b, View dst, uint8_t *am, uint8_t *mask) {
+  // `res` (conv only, nullable view): the residual add fused into the
+  // epilogue; dst and mask are then the add's, res_relu its ReLU
+  int node_fwd(int v, int a, int b, View dst, uint8_t *am, uint8_t *mask,
+               const View *res = nullptr, int res_relu = 0) {
     if (b <= a) return LRCNN_OK;
     const lrcnn_node &d = P.nodes[v];
     const Shape &sv = P.shp[v], &su = P.shp[d.in0];
@@ -123,7 +126,7 @@ struct Run {
     {
       int r0, r1;
       in_rows(d, su.h, a, b, r0, r1);
-      bool ok = holds(dst, a, b) && holds(act[d.in0], r0, r1);
+      bool ok = holds(dst, a, b) && holds(act[d.in0], r0, r1) && (!res || holds(*res, a, b));
       if (d.op == LRCNN_OP_ADD) ok = ok && holds(act[d.in1], r0, r1);
       if (!ok)
         return lrcnn_fail(LRCNN_EINVAL, "internal: band rows of node " + std::to_string(v) +
@@ -152,6 +155,10 @@ struct Run {
       c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
       c.part = (float *)(ws + L.part);
       c.part_bytes = L.part_bytes;
+      if (res) {
+        c.res = *res;
+        c.res_relu = res_relu;
+      }
       LAUNCH(launch_conv(dt, 0, c, stream), "conv forward");
     } else if (d.op == LRCNN_OP_MAXPOOL) {
       PoolArgs p{};
@@ -260,8 +267,25 @@ struct Run {
       }
       uint8_t *am = ((bp || keep) && P.nodes[v].op == LRCNN_OP_MAXPOOL)
                         ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
-      uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
-      if ((st = node_fwd(v, q.a, q.b, dst, am, mk)) != LRCNN_OK) return st;
+      // (not with lifetime-packed forward windows: the add's window may
+      // still belong to another node while the conv runs)
+      const bool can_fuse = !packed && !P.fuse_fwd.empty();
+      const int fa = can_fuse ? P.fuse_fwd[v] : 0;
+      const lrcnn_node &nd = P.nodes[v];
+      if (fa) {
+        // this conv's epilogue computes the residual add fa (its only
+        // consumer): output into the add's view, with the add's mask
+        const lrcnn_node &an = P.nodes[fa];
+        const View other = act[an.in0 == v ? an.in1 : an.in0];
+        uint8_t *amk = mask_out ? (uint8_t *)mask_out[fa] : nullptr;
+        if ((st = node_fwd(v, q.a, q.b, act[fa], am, amk, &other, an.relu)) != LRCNN_OK)
+          return st;
+      } else if (can_fuse && nd.op == LRCNN_OP_ADD && P.fuse_fwd[std::max(nd.in0, nd.in1)] == v) {
+        // computed with its later input
+      } else {
+        uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
+        if ((st = node_fwd(v, q.a, q.b, dst, am, mk)) != LRCNN_OK) return st;
+      }
       if (v == n - 1 && y && keep)
         LAUNCH(launch_rows_copy(dt, dt, dst, full(y, v), 0, P.cfg.batch, q.a, q.b,
                                 P.shp[v].w, P.shp[v].c, stream),

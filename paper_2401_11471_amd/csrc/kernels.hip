@@ -756,7 +756,25 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       const int y = a.y0 + t % R;
       const int b = t / R;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
-      const uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
+      uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
+      if (a.res.p) {
+        // fused residual add: the stored conv value plus the add's other
+        // input, then the add's ReLU
+        union {
+          uint4 u;
+          T e[E];
+        } cv, rv;
+        cv.u = q;
+        rv.u = *(const uint4 *)((const T *)a.res.p + b * a.res.bs + (y - a.res.row0) * drow +
+                                (long long)x * a.N + n);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          float v = ldf(&cv.e[e]) + ldf(&rv.e[e]);
+          if (a.res_relu) v = v > 0.f ? v : 0.f;
+          stf(&cv.e[e], v);
+        }
+        q = cv.u;
+      }
       *(uint4 *)((T *)a.dst.p + off) = q;
       if (a.mask) {
         union {
@@ -893,10 +911,21 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
     for (int k = 0; k < V; ++k) q[k] += val[k];
     stv<float, V>(d, q);
   } else {
+    float rv[4];
+    if (a.res.p)
+      ldv<T, V>((const T *)a.res.p + b * a.res.bs + (y - a.res.row0) * drow +
+                    (long long)x * a.N + n, rv);
 #pragma unroll
     for (int k = 0; k < V; ++k) {
       if (a.scale) val[k] = val[k] * a.scale[n + k] + a.shift[n + k];
       if (a.relu) val[k] = val[k] > 0.f ? val[k] : 0.f;
+      if (a.res.p) {
+        // fused residual add on the value as stored, then the add's ReLU
+        T t;
+        stf(&t, val[k]);
+        val[k] = ldf(&t) + rv[k];
+        if (a.res_relu) val[k] = val[k] > 0.f ? val[k] : 0.f;
+      }
       if (a.mask)
         a.mask[(((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n + k] = val[k] > 0.f ? 1 : 0;
     }
@@ -921,6 +950,8 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   const ConvTiles ct = conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
   const int bn = ct.bn;
   const int splits = ct.splits;
+  // a fused residual add needs the vector epilogues of the forward
+  if (a.res.p && (DGRAD || (a.N % CF::E) != 0)) return (int)hipErrorInvalidValue;
   // split partial sums must fit the buffer (the schedule never exceeds it)
   if (splits > 1 && (!a.part || (size_t)splits * (size_t)M * (size_t)a.N * 4 > a.part_bytes))
     return (int)hipErrorInvalidValue;

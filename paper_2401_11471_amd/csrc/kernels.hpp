@@ -36,6 +36,12 @@ struct ConvArgs {
   float *part;        // split-K partial sums (nullable: no split)
   size_t part_bytes;  // capacity of `part`
   int kts;            // K iterations per split (set by the launcher)
+  // forward only: residual add fused into the epilogue (res.p nullable):
+  // the conv value (rounded to the storage dtype) plus the other input of
+  // the add at the same element, then the add's ReLU when res_relu; dst and
+  // mask are then the add's
+  View res;
+  int res_relu;
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 

@@ -518,6 +518,19 @@ static int build(Plan &P) {
     for (int r = 0; r < nb && ok; ++r) ok = P.rows[r][v].lo == P.rows[r][v].a;
     if (ok) P.fuse_add[v] = c;
   }
+  P.fuse_fwd.assign(n, 0);
+  for (int v = 1; v < n; ++v) {
+    const int c = P.fuse_add[v];
+    if (!c || v != std::max(P.nodes[c].in0, P.nodes[c].in1)) continue;
+    if (P.shp[v].c % (16 / P.es) != 0) continue;
+    bool ok = true;
+    for (int r = 0; r < nb && ok; ++r)
+      ok = P.rows[r][v].a == P.rows[r][c].a && P.rows[r][v].b == P.rows[r][c].b;
+    for (size_t r = 0; r < P.rows_fp.size() && ok; ++r)
+      ok = P.rows_fp[r][v].a == P.rows_fp[r][c].a && P.rows_fp[r][v].b == P.rows_fp[r][c].b &&
+           P.rows_fp[r][v].lo == P.rows_fp[r][v].a;
+    if (ok) P.fuse_fwd[v] = c;
+  }
   // capacities
   std::vector<int> cap(n, 0), own(n, 0), cry(n, 0), fcap(n, 0);
   for (int r = 0; r < nb; ++r)

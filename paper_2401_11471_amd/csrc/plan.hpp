@@ -70,6 +70,10 @@ struct Plan {
   // directly (a conv without ReLU whose only consumer is that add and that
   // carries no rows between backward bands), else 0
   std::vector<int> fuse_add;
+  // per node: the ADD node whose forward this conv's epilogue computes (the
+  // add's later input, fused in its backward, same rows in every band and
+  // whole 16-byte channel vectors), else 0
+  std::vector<int> fuse_fwd;
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   double tau = 0, flops_rows = 0;
