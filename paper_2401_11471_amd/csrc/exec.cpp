@@ -73,6 +73,11 @@ struct Run {
   std::vector<View> dlt;   // current float32 error view of every node
   std::vector<int> first_consumer;
   std::vector<char> dw_set;  // per conv: a band has written its weight gradient
+  // per node: its error window is initialized by the pending input gradient
+  // (with the carried rows in dinit_cv from row dinit_t when dinit_carry)
+  std::vector<char> dinit, dinit_carry;
+  std::vector<View> dinit_cv;
+  std::vector<int> dinit_t;
   hipStream_t side = nullptr;  // weight-gradient stream (backward only)
   bool wg_pending = false;     // a weight gradient on `side` not yet joined
   bool dx_f32 = false;         // store dL/dx as float32 (a checkpoint's error)
@@ -85,6 +90,10 @@ struct Run {
     act.resize(P.n);
     dlt.resize(P.n);
     first_consumer.assign(P.n, -1);
+    dinit.assign(P.n, 0);
+    dinit_carry.assign(P.n, 0);
+    dinit_cv.assign(P.n, View{});
+    dinit_t.assign(P.n, 0);
     for (int v = 0; v < P.n; ++v)
       for (int c : P.cons[v]) first_consumer[v] = std::max(first_consumer[v], c);
     const Shape &s0 = P.shp[0];
@@ -313,6 +322,35 @@ struct Run {
     return P.rows[r][v];
   }
 
+  // Error window of node u for band r: its view, and, in CARRY mode, the
+  // rows [t, b) whose error band r+1 carried (returns false if none).
+  bool delta_view(int r, int u, View &cv, int &t) {
+    const Rows q = band_rows(r, u);
+    const Shape &s = P.shp[u];
+    dlt[u] = win(L.delta[u], u, L.win_cap[u], q.lo);
+    if (sched == S_CARRY && r + 1 < P.nb) {
+      t = P.tail[r][u];
+      if (q.b > t) {
+        cv = View{ws + L.carry[u], (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
+                  L.carry_cap[u]};
+        return true;
+      }
+    }
+    return false;
+  }
+
+  // The input gradient of conv v initializes u's error window itself (no
+  // zeroing pass) when it writes every row of the window this band uses.
+  bool init_by_dgrad(int r, int v, int u, bool want_dx) const {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV || (u == 0 && !want_dx)) return false;
+    const Rows qv = band_rows(r, v), qu = band_rows(r, u);
+    if (qv.b <= qv.a) return false;
+    const int y0 = std::max(0, qv.a * d.sh - d.ph);
+    const int y1 = std::min(P.shp[u].h, (qv.b - 1) * d.sh - d.ph + d.kh);
+    return y0 == qu.lo && y1 == qu.hi;
+  }
+
   // Zero node u's error window for band r and bring in the error carried
   // from band r+1 (CARRY).
   int init_delta(int r, int u) {
@@ -432,6 +470,17 @@ struct Run {
         c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
         c.part = (float *)(ws + L.part);
         c.part_bytes = L.part_bytes;
+        if (dinit[u]) {
+          // this launch writes every row of u's window: no zeroing pass
+          c.dst_init = 1;
+          if (dinit_carry[u]) {
+            if (!holds(dinit_cv[u], dinit_t[u], band_rows(r, u).b))
+              return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+            c.cinit = dinit_cv[u];
+            c.cinit_t = dinit_t[u];
+          }
+          dinit[u] = 0;
+        }
         LAUNCH(launch_conv(dt, 1, c, stream), "input gradient");
       }
     } else if (d.op == LRCNN_OP_MAXPOOL) {
@@ -502,6 +551,18 @@ struct Run {
       int ins[2] = {d.in0, d.op == LRCNN_OP_ADD ? d.in1 : -1};
       for (int u : ins)
         if (u >= 0 && first_consumer[u] == v && !fused(u)) {
+          if (u == 0 && !want_dx && P.nodes[v].op == LRCNN_OP_CONV) {
+            // nothing reads the input's error: only its view is needed
+            View cv;
+            int t = 0;
+            delta_view(r, u, cv, t);
+            continue;
+          }
+          if (init_by_dgrad(r, v, u, want_dx)) {
+            dinit[u] = 1;
+            dinit_carry[u] = delta_view(r, u, dinit_cv[u], dinit_t[u]) ? 1 : 0;
+            continue;
+          }
           int st = init_delta(r, u);
           if (st != LRCNN_OK) return st;
         }

@@ -453,6 +453,17 @@ static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
   for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; \
        idx += (long long)gridDim.x * blockDim.x)
 
+// Base value an input-gradient element is added to: the error window's
+// current value, or, when the launch initializes the window, the carried
+// error (rows >= cinit_t) or zero. `inner` = x * C + c.
+__device__ __forceinline__ const float *dgrad_base(const ConvArgs &a, int b, int y,
+                                                   long long inner, const float *cur) {
+  if (!a.dst_init) return cur;
+  if (a.cinit.p && y >= a.cinit_t)
+    return (const float *)a.cinit.p + view_off(a.cinit, b, y, (int)inner);
+  return nullptr;
+}
+
 // ------------------------------------------- conv forward / input grad
 template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1>
 // bfloat16: three workgroups per CU (the register budget is set for it;
@@ -822,7 +833,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       float4 *d = (float4 *)((float *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow +
                              (long long)x * a.N + n);
       const float4 q = *(const float4 *)&Ct[(r - h0) * FP + cc * 4];
-      float4 o = *d;
+      const float *bp = dgrad_base(a, b, y, (long long)x * a.N + n, (const float *)d);
+      float4 o = bp ? *(const float4 *)bp : make_float4(0.f, 0.f, 0.f, 0.f);
       o.x += q.x, o.y += q.y, o.z += q.z, o.w += q.w;
       *d = o;
     }
@@ -847,7 +859,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         float val = acc[i][j][v];
         if (DGRAD) {
           float *d = (float *)a.dst.p + off + n;
-          *d += val;
+          const float *bp = dgrad_base(a, b, y, (long long)x * a.N + n, d);
+          *d = (bp ? *bp : 0.f) + val;
         } else {
           if (a.scale) val = val * a.scale[n] + a.shift[n];
           if (a.relu) val = val > 0.f ? val : 0.f;
@@ -905,8 +918,9 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
   const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
   if (DGRAD) {
     float *d = (float *)a.dst.p + off;
-    float q[4];
-    ldv<float, V>(d, q);
+    const float *bp = dgrad_base(a, b, y, (long long)x * a.N + n, d);
+    float q[4] = {0.f, 0.f, 0.f, 0.f};
+    if (bp) ldv<float, V>(bp, q);
 #pragma unroll
     for (int k = 0; k < V; ++k) q[k] += val[k];
     stv<float, V>(d, q);

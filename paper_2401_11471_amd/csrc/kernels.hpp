@@ -42,6 +42,14 @@ struct ConvArgs {
   // mask are then the add's
   View res;
   int res_relu;
+  // input gradient only: dst_init = 1 makes this launch initialize the
+  // error window instead of adding to it: it writes cinit's float32 value
+  // (the error carried from the next band, rows >= cinit_t, when cinit.p is
+  // set; zero elsewhere) plus the gradient. The launch must cover every row
+  // of the window the band uses.
+  int dst_init;
+  View cinit;
+  int cinit_t;
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 
