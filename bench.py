@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the layer-wise / recompute comparison runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=4)
+    ap.add_argument("--cpu-images", type=int, default=16)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel from the host in the timed region "
                          "(default: the step is captured once in a HIP graph and replayed)")
@@ -79,9 +80,10 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def cpu_baseline(cfg_id, n_img):
-    """Column oracle (float64, numpy/BLAS) FP+BP on n_img images of the
-    workload, one image at a time; weight gradients are summed."""
+def cpu_baseline(cfg_id, n_img, seconds):
+    """Column oracle (float64, numpy/BLAS) FP+BP on up to n_img images of the
+    workload, one image at a time, stopping once `seconds` have passed (at
+    least one image); weight gradients are summed."""
     import numpy as np
     import threadpoolctl
     from oracle import column as OC
@@ -91,11 +93,14 @@ def cpu_baseline(cfg_id, n_img):
     info = threadpoolctl.threadpool_info()
     cores = max([i.get("num_threads", 1) for i in info] or [1])
     t0 = time.perf_counter()
-    for i in range(n_img):
-        x = inp.x[i:i + 1]
+    done = 0
+    while done < n_img and (done == 0 or time.perf_counter() - t0 < seconds):
+        x = inp.x[done:done + 1]
         acts, am = OC.forward(nodes, x, inp.weights, inp.scales, inp.shifts, bf16=bf)
         g = np.zeros(acts[-1].shape) + 1.0
         OC.backward(nodes, acts, am, inp.weights, inp.scales, g, bf16=bf, want_dx=False)
+        done += 1
+    n_img = done
     dt = time.perf_counter() - t0
     return {"value": round(n_img / dt, 4), "unit": "images/s", "cores": int(cores),
             "kind": "oracle",
@@ -604,7 +609,8 @@ def main():
             del rws, ry
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_images, B))
+        out["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_images, B),
+                                           args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
