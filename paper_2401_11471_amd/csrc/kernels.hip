@@ -429,11 +429,24 @@ __device__ __forceinline__ void stv(T *p, const float (&v)[4]) {
   else stf(p, v[0]);
 }
 
-// Decompose a flat index over B x rows x (W*C/V) into (b, row, inner).
+// Decompose a flat index over B x rows x (W*C/V) into (b, row, inner):
+// by multiply-shift division when every index fits in 32 bits, else by
+// 64-bit division.
 struct RowIter {
   long long inner, total;
   int R, r0;
+  int fast;
+  FastDiv fin, fr;
   __device__ __forceinline__ void at(long long idx, int V, int &b, int &y, int &in) const {
+    if (fast) {
+      uint32_t t, i, q, yy;
+      fdiv_qr((uint32_t)idx, fin, t, i);
+      fdiv_qr(t, fr, q, yy);
+      in = (int)i * V;
+      y = r0 + (int)yy;
+      b = (int)q;
+      return;
+    }
     const long long i = idx % inner;
     const long long t = idx / inner;
     in = (int)(i * V);
@@ -447,6 +460,11 @@ static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
   it.R = r1 - r0;
   it.r0 = r0;
   it.total = (long long)B * it.R * it.inner;
+  it.fast = it.total < (1ll << 32) && it.R > 0 && it.inner > 0;
+  if (it.fast) {
+    it.fin = fast_div((uint32_t)it.inner);
+    it.fr = fast_div((uint32_t)it.R);
+  }
   return it;
 }
 #define GRID_STRIDE(idx, total)                                                   \
@@ -517,10 +535,12 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     int m = m0 + tid / KR + RS * i;
     am[i] = m < M;
     int mm = am[i] ? m : 0;
-    ax[i] = mm % a.Wd;
-    int t = mm / a.Wd;
-    ay[i] = a.y0 + t % R;
-    abase[i] = (long long)(t / R) * a.src.bs - (long long)a.src.row0 * srow;
+    uint32_t t, x, b, y;
+    fdiv_qr((uint32_t)mm, a.fw, t, x);
+    fdiv_qr(t, a.fr, b, y);
+    ax[i] = (int)x;
+    ay[i] = a.y0 + (int)y;
+    abase[i] = (long long)b * a.src.bs - (long long)a.src.row0 * srow;
   }
   // source row / column of each A row before the tap offset, and its
   // address there: a K step then adds one uniform offset per tap and
@@ -762,10 +782,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     for (int r = h0 + tid / CPR; r < h0 + HR; r += RPP) {
       const int m = m0 + r;
       if (m >= M || n >= a.N) continue;
-      const int x = m % a.Wd;
-      const int t = m / a.Wd;
-      const int y = a.y0 + t % R;
-      const int b = t / R;
+      uint32_t t_, x_, b_, y_;
+      fdiv_qr((uint32_t)m, a.fw, t_, x_);
+      fdiv_qr(t_, a.fr, b_, y_);
+      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
       uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
       if (a.res.p) {
@@ -826,10 +846,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     for (int r = h0 + tid / CPR; r < h0 + HR; r += RPP) {
       const int m = m0 + r;
       if (m >= M || n >= a.N) continue;
-      const int x = m % a.Wd;
-      const int t = m / a.Wd;
-      const int y = a.y0 + t % R;
-      const int b = t / R;
+      uint32_t t_, x_, b_, y_;
+      fdiv_qr((uint32_t)m, a.fw, t_, x_);
+      fdiv_qr(t_, a.fr, b_, y_);
+      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
       float4 *d = (float4 *)((float *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow +
                              (long long)x * a.N + n);
       const float4 q = *(const float4 *)&Ct[(r - h0) * FP + cc * 4];
@@ -847,10 +867,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     for (int v = 0; v < 16; ++v) {
       const int m = m0 + wm + 32 * i + acc_row(v, lane);
       if (m >= M) continue;
-      const int x = m % a.Wd;
-      const int t = m / a.Wd;
-      const int y = a.y0 + t % R;
-      const int b = t / R;
+      uint32_t t_, x_, b_, y_;
+      fdiv_qr((uint32_t)m, a.fw, t_, x_);
+      fdiv_qr(t_, a.fr, b_, y_);
+      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
@@ -909,12 +929,12 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
   for (int gg = 0; gg < G; ++gg)
 #pragma unroll
     for (int k = 0; k < V; ++k) val[k] += red[(gg * epb + e) * 4 + k];
-  const int n = (int)(idx % a.N);
-  const long long m = idx / a.N;
-  const int x = (int)(m % a.Wd);
-  const long long t = m / a.Wd;
-  const int y = a.y0 + (int)(t % R);
-  const int b = (int)(t / R);
+  // M * N < 2^32 for every split launch (the launcher checks)
+  uint32_t m_, n_, t_, x_, b_, y_;
+  fdiv_qr((uint32_t)idx, a.fn, m_, n_);
+  fdiv_qr(m_, a.fw, t_, x_);
+  fdiv_qr(t_, a.fr, b_, y_);
+  const int n = (int)n_, x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
   const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
   if (DGRAD) {
     float *d = (float *)a.dst.p + off;
@@ -969,6 +989,10 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   // split partial sums must fit the buffer (the schedule never exceeds it)
   if (splits > 1 && (!a.part || (size_t)splits * (size_t)M * (size_t)a.N * 4 > a.part_bytes))
     return (int)hipErrorInvalidValue;
+  if (splits > 1 && (long long)M * a.N >= (1ll << 32)) return (int)hipErrorInvalidValue;
+  a.fw = fast_div((uint32_t)a.Wd);
+  a.fr = fast_div((uint32_t)(a.y1 - a.y0));
+  a.fn = fast_div((uint32_t)a.N);
   a.kts = (KT + splits - 1) / splits;
   dim3 grid((M + BM - 1) / BM, (a.N + bn - 1) / bn, splits);
   int pr = -1;
@@ -1342,13 +1366,23 @@ __global__ void pool_fwd_kernel(PoolArgs a) {
   const long long total = (long long)a.B * R * a.Wd * CV;
   const long long srow = (long long)a.src.W * a.src.C;
   const long long drow = (long long)a.Wd * a.C;
+  const bool fast = total < (1ll << 32);
   GRID_STRIDE(idx, total) {
-    const int c = (int)(idx % CV) * V;
-    long long t = idx / CV;
-    const int x = (int)(t % a.Wd);
-    t /= a.Wd;
-    const int yy = (int)(t % R);
-    const int b = (int)(t / R);
+    int c, x, yy, b;
+    if (fast) {
+      uint32_t t0, c0, t1, x0, b0, y0;
+      fdiv_qr((uint32_t)idx, a.fcv, t0, c0);
+      fdiv_qr(t0, a.fw, t1, x0);
+      fdiv_qr(t1, a.fr, b0, y0);
+      c = (int)c0 * V, x = (int)x0, yy = (int)y0, b = (int)b0;
+    } else {
+      c = (int)(idx % CV) * V;
+      long long t = idx / CV;
+      x = (int)(t % a.Wd);
+      t /= a.Wd;
+      yy = (int)(t % R);
+      b = (int)(t / R);
+    }
     const int y = a.y0 + yy;
     const T *src = (const T *)a.src.p + b * a.src.bs;
     float best[4];
@@ -1386,11 +1420,15 @@ __global__ void pool_fwd_kernel(PoolArgs a) {
 }
 
 
-int launch_pool_fwd(int dt, const PoolArgs &a, void *stream) {
-  const long long total = (long long)a.B * (a.y1 - a.y0) * a.Wd * a.C;
+int launch_pool_fwd(int dt, const PoolArgs &a0, void *stream) {
+  const long long total = (long long)a0.B * (a0.y1 - a0.y0) * a0.Wd * a0.C;
   if (total <= 0) return 0;
   hipStream_t s = (hipStream_t)stream;
-  const bool v4 = a.C % 4 == 0;
+  const bool v4 = a0.C % 4 == 0;
+  PoolArgs a = a0;
+  a.fcv = fast_div((uint32_t)(v4 ? a.C / 4 : a.C));
+  a.fw = fast_div((uint32_t)a.Wd);
+  a.fr = fast_div((uint32_t)(a.y1 - a.y0));
   const unsigned g = grid_for(v4 ? total / 4 : total);
   if (dt == DT_F32) {
     if (v4) pool_fwd_kernel<float, 4><<<g, 256, 0, s>>>(a);
@@ -1408,13 +1446,23 @@ __global__ void pool_bwd_kernel(PoolBwdArgs a) {
   const int CV = a.C / V;
   const long long total = (long long)a.B * Ru * a.Wu * CV;
   const long long vrow = (long long)a.Wv * a.C, urow = (long long)a.Wu * a.C;
+  const bool fast = total < (1ll << 32);
   GRID_STRIDE(idx, total) {
-    const int c = (int)(idx % CV) * V;
-    long long t = idx / CV;
-    const int xi = (int)(t % a.Wu);
-    t /= a.Wu;
-    const int yi = a.ua + (int)(t % Ru);
-    const int b = (int)(t / Ru);
+    int c, xi, yi, b;
+    if (fast) {
+      uint32_t t0, c0, t1, x0, b0, y0;
+      fdiv_qr((uint32_t)idx, a.fcv, t0, c0);
+      fdiv_qr(t0, a.fw, t1, x0);
+      fdiv_qr(t1, a.fr, b0, y0);
+      c = (int)c0 * V, xi = (int)x0, yi = a.ua + (int)y0, b = (int)b0;
+    } else {
+      c = (int)(idx % CV) * V;
+      long long t = idx / CV;
+      xi = (int)(t % a.Wu);
+      t /= a.Wu;
+      yi = a.ua + (int)(t % Ru);
+      b = (int)(t / Ru);
+    }
     // windows y with y*sh - ph <= yi < y*sh - ph + kh, inside [y0, y1)
     const int ylo = max(a.y0, fdiv(yi + a.ph - a.kh, a.sh) + 1);
     const int yhi = min(a.y1 - 1, fdiv(yi + a.ph, a.sh));
@@ -1441,9 +1489,13 @@ __global__ void pool_bwd_kernel(PoolBwdArgs a) {
   }
 }
 
-int launch_pool_bwd(const PoolBwdArgs &a, void *stream) {
-  const long long total = (long long)a.B * (a.ub - a.ua) * a.Wu * a.C;
+int launch_pool_bwd(const PoolBwdArgs &a0, void *stream) {
+  const long long total = (long long)a0.B * (a0.ub - a0.ua) * a0.Wu * a0.C;
   if (total <= 0) return 0;
+  PoolBwdArgs a = a0;
+  a.fcv = fast_div((uint32_t)(a.C % 4 == 0 ? a.C / 4 : a.C));
+  a.fw = fast_div((uint32_t)a.Wu);
+  a.fr = fast_div((uint32_t)(a.ub - a.ua));
   if (a.C % 4 == 0)
     pool_bwd_kernel<4><<<grid_for(total / 4), 256, 0, (hipStream_t)stream>>>(a);
   else

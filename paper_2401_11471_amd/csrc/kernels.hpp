@@ -6,7 +6,38 @@
 #include <cstddef>
 #include <cstdint>
 
+#if defined(__HIPCC__)
+#define LRCNN_HD __host__ __device__
+#else
+#define LRCNN_HD
+#endif
+
 namespace lrcnn {
+
+// Division of an unsigned 32-bit n by an invariant divisor 1 <= d < 2^31
+// with one multiply-high, an add and a shift (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", PLDI 1994,
+// Section 4): with l = ceil(log2 d) and m = floor(2^32 (2^l - d) / d) + 1,
+// which fits in 32 bits, n / d = (mulhi(m, n) + n) >> l, the sum taken in
+// 64 bits. The index arithmetic of the kernels uses it in place of integer
+// division, whose expansion costs tens of instructions per quotient.
+struct FastDiv {
+  uint32_t d, m, l;
+};
+inline FastDiv fast_div(uint32_t d) {
+  uint32_t l = 0;
+  while (l < 31 && (uint32_t(1) << l) < d) ++l;
+  const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
+  return FastDiv{d, (uint32_t)m, l};
+}
+LRCNN_HD inline uint32_t fdiv_q(uint32_t n, const FastDiv &f) {
+  return (uint32_t)(((((uint64_t)f.m * n) >> 32) + n) >> f.l);
+}
+// q = n / d and r = n % d
+LRCNN_HD inline void fdiv_qr(uint32_t n, const FastDiv &f, uint32_t &q, uint32_t &r) {
+  q = fdiv_q(n, f);
+  r = n - q * f.d;
+}
 
 // A band window of an NHWC feature map: element (b, y, x, c) of the global
 // map lives at p + b*bs + (y - row0)*W*C + x*C + c, for the rows the buffer
@@ -50,6 +81,7 @@ struct ConvArgs {
   int dst_init;
   View cinit;
   int cinit_t;
+  FastDiv fw, fr, fn;  // division by Wd, y1 - y0 and N (set by the launcher)
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 
@@ -196,6 +228,7 @@ struct PoolArgs {
   int mask_h;
   int B, y0, y1, Wd, C, Hs, Ws;
   int kh, kw, sh, sw, ph, pw;
+  FastDiv fcv, fw, fr;  // C / V, Wd, y1 - y0 (set by the launcher)
 };
 int launch_pool_fwd(int dt, const PoolArgs &a, void *stream);
 
@@ -207,6 +240,7 @@ struct PoolBwdArgs {
   const uint8_t *am;
   int B, y0, y1, Wv, C, ua, ub, Wu;
   int kh, kw, sh, sw, ph, pw;
+  FastDiv fcv, fw, fr;  // C / V, Wu, ub - ua (set by the launcher)
 };
 int launch_pool_bwd(const PoolBwdArgs &a, void *stream);
 
