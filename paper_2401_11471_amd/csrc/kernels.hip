@@ -520,7 +520,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   const int m0 = tl.x * BM, n0 = tl.y * BN;
   const int taps = a.kh * a.kw;
   const int CB = (a.KC + BK - 1) / BK;
-  const int KT = taps * CB;
+  const bool tpk = !VEC && !DGRAD && a.tpack;
+  const int KT = tpk ? (taps + KR - 1) / KR : taps * CB;
   const int kv = tid % KR;
   const T *src = (const T *)a.src.p;
   const T *w = (const T *)a.w;
@@ -579,10 +580,33 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   const int kend = min(KT, kbeg + a.kts);
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
+  int kpk = kbeg;  // tap-packed forward: current K iteration
 
   uint4 ra[NA], rb[NBL];
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   auto gload = [&]() {
+    if (tpk) {
+      // vector kv of a tile row holds channels [0, KC) of tap kpk*KR + kv
+      const int tp = kpk * KR + kv;
+      const bool tok = tp < taps;
+      uint32_t ti_, tj_;
+      fdiv_qr((uint32_t)(tok ? tp : 0), a.fkw, ti_, tj_);
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const int sy = by[i] + (int)ti_, sx = bx[i] + (int)tj_;
+        const bool ok = tok & am[i] & (sx >= 0) & (sy >= a.sy0) & (sy < a.sy1) & (sx < a.Ws);
+        const long long off = rbase[i] + (long long)ti_ * srow + (long long)tj_ * a.src.C;
+        ra[i] = load16<T, false>(ok ? src + off : src, ok, a.KC);
+      }
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) {
+        const bool ok = bvld[j] & tok;
+        const long long off = bbase[j] - kv * E + (long long)tp * a.KC;
+        rb[j] = load16<T, false>(ok ? w + off : w, ok, a.KC);
+      }
+      ++kpk;
+      return;
+    }
     const int cb = cbi * BK;
     const int c0 = cb + kv * E;
     const bool cok = c0 < a.KC;
@@ -980,7 +1004,9 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
   const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0);
-  const int KT = a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
+  a.tpack = !vec && conv_tap_packed(a.KC, (int)sizeof(T), DGRAD);
+  a.fkw = fast_div((uint32_t)a.kw);
+  const int KT = a.tpack ? (a.kh * a.kw + KR - 1) / KR : a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
   const ConvTiles ct = conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
   const int bn = ct.bn;
   const int splits = ct.splits;

@@ -82,6 +82,10 @@ struct ConvArgs {
   View cinit;
   int cinit_t;
   FastDiv fw, fr, fn;  // division by Wd, y1 - y0 and N (set by the launcher)
+  // forward with KC channels in one vector: each K iteration covers KR taps,
+  // one per 16-byte vector of a tile row (set by the launcher)
+  int tpack;
+  FastDiv fkw;  // division by kw
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 
@@ -176,7 +180,12 @@ inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
 #ifndef LRCNN_CONV_KR
 #define LRCNN_CONV_KR 4
 #endif
-inline int conv_k_iters(int taps, int kc, int es) {
+// A forward convolution whose input channels fit in one 16-byte vector
+// (kc * es < 16, e.g. a 3-channel image) packs LRCNN_CONV_KR taps into one
+// iteration instead (tap_packed).
+inline bool conv_tap_packed(int kc, int es, bool dgrad) { return !dgrad && kc * es < 16; }
+inline int conv_k_iters(int taps, int kc, int es, bool dgrad = false) {
+  if (conv_tap_packed(kc, es, dgrad)) return (taps + LRCNN_CONV_KR - 1) / LRCNN_CONV_KR;
   const int bk = 16 * LRCNN_CONV_KR / es;
   return taps * ((kc + bk - 1) / bk);
 }

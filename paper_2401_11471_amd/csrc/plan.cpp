@@ -342,7 +342,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
         const int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
         if (padded) xrows = std::max(xrows, u1 - u0);
         const long long md = (long long)P.cfg.batch * (u1 - u0) * su.w;
-        const int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es), pcap, P.es);
+        const int sd = conv_split_count(md, su.c, conv_k_iters(taps, sv.c, P.es, true), pcap, P.es);
         if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
       }
     }
