@@ -18,6 +18,13 @@ extern "C" {
  * tested on a machine without a GPU. on == 0 restores normal operation. */
 void lrcnn_debug_dry_run(int on);
 
+/* On the calling thread, the input gradient of a strided convolution
+ * (stride s in both directions) is computed as s^2 launches, one per phase
+ * of producer rows and columns ((y + pad) mod s), each with only the taps
+ * that reach it: mode 0 = when estimated faster than one launch over all
+ * taps (default), 1 = always, 2 = never. Results agree to rounding. */
+void lrcnn_debug_dgrad_phases(int mode);
+
 /* on != 0: clear and start recording two events on the launch stream around
  * every matrix-core kernel launch (convolution forward, input gradient,
  * weight gradient), with each launch's algorithmic FLOPs; on == 0 stops

@@ -847,6 +847,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
 }
 
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
+extern "C" void lrcnn_debug_dgrad_phases(int mode) { lrcnn::set_dgrad_phases(mode); }
 
 extern "C" void lrcnn_debug_profile(int on) { lrcnn::profile_enable(on); }
 extern "C" int lrcnn_debug_profile_collect(void) { return lrcnn::profile_collect(); }

@@ -515,6 +515,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
+  // pixel stride of a phase of a strided input gradient (else 1)
+  const int ps = DGRAD && a.pst > 1 ? a.pst : 1;
   // output-channel tiles fastest: a run of consecutive pixel tiles per XCD
   const TileId tl = xcd_tile(true);
   const int m0 = tl.x * BM, n0 = tl.y * BN;
@@ -539,8 +541,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     uint32_t t, x, b, y;
     fdiv_qr((uint32_t)mm, a.fw, t, x);
     fdiv_qr(t, a.fr, b, y);
-    ax[i] = (int)x;
-    ay[i] = a.y0 + (int)y;
+    ax[i] = a.px0 + ps * (int)x;
+    ay[i] = a.y0 + ps * (int)y;
     abase[i] = (long long)b * a.src.bs - (long long)a.src.row0 * srow;
   }
   // source row / column of each A row before the tap offset, and its
@@ -550,8 +552,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   long long rbase[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) {
-    by[i] = DGRAD ? ay[i] + a.ph : ay[i] * a.sh - a.ph;
-    bx[i] = DGRAD ? ax[i] + a.pw : ax[i] * a.sw - a.pw;
+    // (a phase: consumer row (y + ph) / s - i for its i-th tap, exactly)
+    by[i] = DGRAD ? (ps > 1 ? (ay[i] + a.ph) / ps : ay[i] + a.ph) : ay[i] * a.sh - a.ph;
+    bx[i] = DGRAD ? (ps > 1 ? (ax[i] + a.pw) / ps : ax[i] + a.pw) : ax[i] * a.sw - a.pw;
     rbase[i] = abase[i] + (long long)by[i] * srow + (long long)bx[i] * a.src.C;
   }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
@@ -568,10 +571,12 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     bvld[j] = bn[j] < a.N;
   }
   const int bk0 = tid / BV;
+  // taps of the weight tensor (a phase reads a subset of the full kernel)
+  const int wtaps = ps > 1 ? a.taps_full : taps;
   long long bbase[NBL];
 #pragma unroll
   for (int j = 0; j < NBL; ++j)
-    bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * taps * a.N + bn[j]
+    bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * wtaps * a.N + bn[j]
                      : (long long)bn[j] * taps * a.KC + kv * E;
 
   // K iterations of this workgroup (split-K over the tile's z), walked as
@@ -646,7 +651,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       if (DGRAD) {
         const int o = cb + bk0 + BKS * j;
         ok = bvld[j] & (o < a.KC);
-        off = bbase[j] + ((long long)cb * taps + tap) * a.N;
+        const int wtap = ps > 1 ? (a.ty0 + ps * ti) * a.kw_full + a.tx0 + ps * tj : tap;
+        off = bbase[j] + ((long long)cb * wtaps + wtap) * a.N;
         blim = a.N - bn[j];
       } else {
         ok = bvld[j] & cok;
@@ -772,7 +778,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
 
   // epilogue
   const int col = lane & 31;
-  const long long drow = (long long)a.Wd * a.N;
+  const long long drow = (long long)a.dst.W * a.N;
   if (!DGRAD && (a.N % E) == 0) {
     // forward: affine, ReLU (and the optional mask) in registers, the tile
     // staged in LDS, then whole 16-byte row chunks stored per thread
@@ -809,7 +815,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       uint32_t t_, x_, b_, y_;
       fdiv_qr((uint32_t)m, a.fw, t_, x_);
       fdiv_qr(t_, a.fr, b_, y_);
-      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
+      const int x = a.px0 + ps * (int)x_, y = a.y0 + ps * (int)y_, b = (int)b_;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
       uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
       if (a.res.p) {
@@ -873,7 +879,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       uint32_t t_, x_, b_, y_;
       fdiv_qr((uint32_t)m, a.fw, t_, x_);
       fdiv_qr(t_, a.fr, b_, y_);
-      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
+      const int x = a.px0 + ps * (int)x_, y = a.y0 + ps * (int)y_, b = (int)b_;
       float4 *d = (float4 *)((float *)a.dst.p + b * a.dst.bs + (y - a.dst.row0) * drow +
                              (long long)x * a.N + n);
       const float4 q = *(const float4 *)&Ct[(r - h0) * FP + cc * 4];
@@ -894,7 +900,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       uint32_t t_, x_, b_, y_;
       fdiv_qr((uint32_t)m, a.fw, t_, x_);
       fdiv_qr(t_, a.fr, b_, y_);
-      const int x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
+      const int x = a.px0 + ps * (int)x_, y = a.y0 + ps * (int)y_, b = (int)b_;
       const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
@@ -931,7 +937,8 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
   const int R = a.y1 - a.y0;
   const long long M = (long long)a.B * R * a.Wd;
   const long long MN = M * a.N;
-  const long long drow = (long long)a.Wd * a.N;
+  const long long drow = (long long)a.dst.W * a.N;
+  const int ps = DGRAD && a.pst > 1 ? a.pst : 1;
   const int epb = 256 / G;  // vectors per block
   const int g = threadIdx.x / epb, e = threadIdx.x - g * epb;
   const long long idx = ((long long)blockIdx.x * epb + e) * V;
@@ -958,7 +965,7 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
   fdiv_qr((uint32_t)idx, a.fn, m_, n_);
   fdiv_qr(m_, a.fw, t_, x_);
   fdiv_qr(t_, a.fr, b_, y_);
-  const int n = (int)n_, x = (int)x_, y = a.y0 + (int)y_, b = (int)b_;
+  const int n = (int)n_, x = a.px0 + ps * (int)x_, y = a.y0 + ps * (int)y_, b = (int)b_;
   const long long off = b * a.dst.bs + (y - a.dst.row0) * drow + (long long)x * a.N + n;
   if (DGRAD) {
     float *d = (float *)a.dst.p + off;
@@ -997,7 +1004,7 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
 #endif
 
 template <typename T, bool DGRAD>
-static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
+static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   constexpr int KR = LRCNN_CONV_KR;
   using CF = Cfg<T, KR>;
   ConvArgs a = a0;
@@ -1026,15 +1033,16 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
     // algorithmic FLOPs: forward 2*M*N*K; input gradient 2 * consumer pixels
     // * C_out * taps * C_in (taps that a stride skips are not counted)
     const double taps = (double)a.kh * a.kw;
-    const double fl = DGRAD ? 2.0 * a.B * (a.sy1 - a.sy0) * a.Ws * a.KC * taps * a.N
-                            : 2.0 * M * a.N * taps * a.KC;
+    const double fl = DGRAD && a.pst <= 1 ? 2.0 * a.B * (a.sy1 - a.sy0) * a.Ws * a.KC * taps * a.N
+                                          : 2.0 * M * a.N * taps * a.KC;
     std::string nm = std::string("conv_gemm_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                      ", " + std::to_string(bn) + (DGRAD ? ", dgrad" : ", fwd") +
                      (vec ? ", vec>" : ", scalar>");
     pr = prof::begin(nm, fl, s);
   }
   // the input gradient of a strided convolution divides by the stride
-  const bool s1 = !DGRAD || (a.sh == 1 && a.sw == 1);
+  // (a phase of it is dense)
+  const bool s1 = !DGRAD || (a.sh == 1 && a.sw == 1) || a.pst > 1;
   if (bn == 64) {
     if (!s1) {
       if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
@@ -1067,6 +1075,73 @@ static int conv_dispatch(const ConvArgs &a0, hipStream_t s) {
     prof::end(p2, s);
   }
   return (int)hipGetLastError();
+}
+
+// Phases of the input gradient of a strided convolution. Producer pixel y
+// receives tap i of the s-strided kernel only when (y + ph - i) is a
+// multiple of s, i.e. i = (y + ph) mod s + s * i'. Grouping producer rows
+// and columns by (y + ph) mod s gives s^2 dense problems, each with about
+// 1/s^2 of the taps, instead of one launch in which the MFMAs also multiply
+// the s^2 - 1 of every s^2 (pixel, tap) pairs that are zero. One dimension:
+// the first pixel >= lo of residue r, the count of such pixels below hi,
+// and the taps of the phase.
+struct PhaseDim {
+  int first, count, taps;
+};
+static PhaseDim phase_dim(int lo, int hi, int p, int k, int s, int r) {
+  PhaseDim d;
+  d.first = lo + (((r - (lo + p)) % s) + s) % s;
+  d.count = d.first < hi ? (hi - d.first + s - 1) / s : 0;
+  d.taps = r < k ? (k - r + s - 1) / s : 0;
+  return d;
+}
+
+static thread_local int g_phases = 0;  // 0: by estimate, 1: always, 2: never
+void set_dgrad_phases(int mode) { g_phases = mode; }
+
+template <typename T, bool DGRAD>
+static int conv_dispatch(const ConvArgs &a, hipStream_t s) {
+  if (!DGRAD || (a.sh == 1 && a.sw == 1) || a.sh != a.sw || a.pst > 1 || g_phases == 2)
+    return conv_launch<T, DGRAD>(a, s);
+  const int M = a.B * (a.y1 - a.y0) * a.Wd;
+  if (M <= 0 || a.N <= 0) return 0;
+  // phases when their estimated durations (plus a launch each) beat the
+  // single launch over all taps
+  const int es = (int)sizeof(T);
+  const size_t cap = a.part ? a.part_bytes : 0;
+  const double one = conv_tiles(M, a.N, conv_k_iters(a.kh * a.kw, a.KC, es, true), cap, es).us;
+  double ph = 0;
+  for (int ry = 0; ry < a.sh; ++ry)
+    for (int rx = 0; rx < a.sw; ++rx) {
+      const PhaseDim py = phase_dim(a.y0, a.y1, a.ph, a.kh, a.sh, ry);
+      const PhaseDim px = phase_dim(0, a.Wd, a.pw, a.kw, a.sw, rx);
+      if (py.count == 0 || px.count == 0 || (py.taps * px.taps == 0 && !a.dst_init)) continue;
+      ph += 5.0 + conv_tiles((long long)a.B * py.count * px.count, a.N,
+                             conv_k_iters(py.taps * px.taps, a.KC, es, true), cap, es).us;
+    }
+  if (ph >= one && g_phases != 1) return conv_launch<T, DGRAD>(a, s);
+  for (int ry = 0; ry < a.sh; ++ry)
+    for (int rx = 0; rx < a.sw; ++rx) {
+      const PhaseDim py = phase_dim(a.y0, a.y1, a.ph, a.kh, a.sh, ry);
+      const PhaseDim px = phase_dim(0, a.Wd, a.pw, a.kw, a.sw, rx);
+      // a phase without taps still writes its pixels when the launch
+      // initializes the error window
+      if (py.count == 0 || px.count == 0 || (py.taps * px.taps == 0 && !a.dst_init)) continue;
+      ConvArgs b = a;
+      b.pst = a.sh;
+      b.y0 = py.first;
+      b.y1 = py.first + py.count;
+      b.px0 = px.first;
+      b.Wd = px.count;
+      b.ty0 = ry;
+      b.tx0 = rx;
+      b.kw_full = a.kw;
+      b.taps_full = a.kh * a.kw;
+      b.kh = py.taps * px.taps == 0 ? 0 : py.taps;
+      b.kw = py.taps * px.taps == 0 ? 1 : px.taps;
+      if (int e = conv_launch<T, DGRAD>(b, s)) return e;
+    }
+  return 0;
 }
 
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream) {

@@ -86,8 +86,18 @@ struct ConvArgs {
   // one per 16-byte vector of a tile row (set by the launcher)
   int tpack;
   FastDiv fkw;  // division by kw
+  // input gradient of a strided convolution split into phases (pst > 1,
+  // set by the launcher): this launch covers the producer pixels
+  // y = y0 + pst * yy (yy < y1 - y0), x = px0 + pst * xx (xx < Wd), which
+  // receive exactly the taps (ty0 + pst * i, tx0 + pst * j), i < kh, j < kw,
+  // of the kh_full x kw_full kernel; W is read with the full kernel's
+  // strides (taps_full taps, kw_full columns)
+  int pst, px0, ty0, tx0, kw_full, taps_full;
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
+// input gradients of strided convolutions on the calling thread: 0 = split
+// into stride phases when estimated faster, 1 = always, 2 = never
+void set_dgrad_phases(int mode);
 
 // Split-K selection. A launch of `tiles` output tiles whose K loop has KT
 // iterations runs split s ways as tiles*s workgroups of ceil(KT/s)
@@ -160,16 +170,18 @@ inline int split_count(long long tiles, int KT, long long part_elems, size_t cap
 // tiles; the cheaper of the two estimates is taken.
 struct ConvTiles {
   int bn, splits;
+  double us;  // estimated duration
 };
 inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es) {
   const double f = es == 2 ? 0.75 : 1.0;
   const long long mt = (M + 127) / 128;
   SplitChoice n64 = split_choice(mt * ((N + 63) / 64), KT, M * (long long)N, cap,
                                  SplitCost{LRCNN_STEP_N64 * f, 3, 5.0});
-  if (N <= 64) return ConvTiles{64, n64.s};
+  if (N <= 64) return ConvTiles{64, n64.s, n64.us};
   SplitChoice n128 = split_choice(mt * ((N + 127) / 128), KT, M * (long long)N, cap,
                                   SplitCost{LRCNN_STEP_N128 * f, 2, 5.0});
-  return n64.us < n128.us * LRCNN_NARROW_GAIN ? ConvTiles{64, n64.s} : ConvTiles{128, n128.s};
+  return n64.us < n128.us * LRCNN_NARROW_GAIN ? ConvTiles{64, n64.s, n64.us}
+                                              : ConvTiles{128, n128.s, n128.us};
 }
 // split count of a convolution launch (the planner sizes partial sums with it)
 inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
