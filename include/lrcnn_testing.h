@@ -18,6 +18,13 @@ extern "C" {
  * tested on a machine without a GPU. on == 0 restores normal operation. */
 void lrcnn_debug_dry_run(int on);
 
+/* on == 0: plans created on the calling thread form every convolution's
+ * error operand by its own activation-backward pass; on != 0 (default) the
+ * input gradient of a convolution's only consumer, which completes the
+ * convolution's error, forms the error operand and carried rows itself
+ * (CARRY plans). Both do the same arithmetic, so results are bitwise equal. */
+void lrcnn_debug_act_fusion(int on);
+
 /* On the calling thread, the input gradient of a strided convolution
  * (stride s in both directions) is computed as s^2 launches, one per phase
  * of producer rows and columns ((y + pad) mod s), each with only the taps

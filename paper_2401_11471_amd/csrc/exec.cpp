@@ -76,6 +76,9 @@ struct Run {
   // per node: its error window is initialized by the pending input gradient
   // (with the carried rows in dinit_cv from row dinit_t when dinit_carry)
   std::vector<char> dinit, dinit_carry;
+  // per conv: its error operand (and carry) were formed by its consumer's
+  // input gradient in this band (no activation-backward pass)
+  std::vector<char> act_done;
   std::vector<View> dinit_cv;
   std::vector<int> dinit_t;
   hipStream_t side = nullptr;  // weight-gradient stream (backward only)
@@ -94,6 +97,7 @@ struct Run {
     dinit_carry.assign(P.n, 0);
     dinit_cv.assign(P.n, View{});
     dinit_t.assign(P.n, 0);
+    act_done.assign(P.n, 0);
     for (int v = 0; v < P.n; ++v)
       for (int c : P.cons[v]) first_consumer[v] = std::max(first_consumer[v], c);
     const Shape &s0 = P.shp[0];
@@ -324,6 +328,12 @@ struct Run {
 
   // Error window of node u for band r: its view, and, in CARRY mode, the
   // rows [t, b) whose error band r+1 carried (returns false if none).
+  // carry buffer of node u written by band `band` (and read by band - 1)
+  char *carry_ptr(int u, int band) const {
+    (void)band;
+    return ws + L.carry[u];
+  }
+
   bool delta_view(int r, int u, View &cv, int &t) {
     const Rows q = band_rows(r, u);
     const Shape &s = P.shp[u];
@@ -331,7 +341,7 @@ struct Run {
     if (sched == S_CARRY && r + 1 < P.nb) {
       t = P.tail[r][u];
       if (q.b > t) {
-        cv = View{ws + L.carry[u], (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
+        cv = View{carry_ptr(u, r + 1), (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
                   L.carry_cap[u]};
         return true;
       }
@@ -361,7 +371,7 @@ struct Run {
       const int t = P.tail[r][u];
       if (q.b > t) {
         // zero rows [lo, t), carried rows [t, b): one launch
-        View cv = View{ws + L.carry[u], (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
+        View cv = View{carry_ptr(u, r + 1), (long long)L.carry_cap[u] * s.w * s.c, t, s.w, s.c,
                        L.carry_cap[u]};
         if (!holds(cv, t, q.b) || !holds(dlt[u], q.lo, q.b) || q.b != q.hi)
           return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
@@ -402,13 +412,16 @@ struct Run {
       View cv{};
       const bool carries = sched == S_CARRY && r > 0 && q.a > q.lo;
       if (carries) {
-        cv = View{ws + L.carry[v], (long long)L.carry_cap[v] * sv.w * sv.c, q.lo, sv.w, sv.c,
+        cv = View{carry_ptr(v, r), (long long)L.carry_cap[v] * sv.w * sv.c, q.lo, sv.w, sv.c,
                   L.carry_cap[v]};
         if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
       }
       if (fused(v)) {
         // the add's backward already wrote this conv's error operand
         if (carries) return lrcnn_fail(LRCNN_EINVAL, "internal: fused conv carries rows");
+      } else if (act_done[v]) {
+        // the consumer's input gradient formed the error operand and carry
+        act_done[v] = 0;
       } else {
         LAUNCH(launch_act_bwd(dt, dlt[v], act[v], d.affine ? sc[v] : nullptr, d.relu, dc, B, a,
                               b, sv.w, sv.c, stream, carries ? &cv : nullptr, q.lo, q.a),
@@ -454,6 +467,8 @@ struct Run {
       }
       if (u != 0 || want_dx) {
         ConvArgs c{};
+        View stage{};     // carry buffer the staged carried-out rows go to
+        int stage_u = -1, stage_a = 0;
         c.src = View{dc, (long long)(b - a) * sv.w * sv.c, a, sv.w, sv.c, b - a};
         c.dst = dlt[u];
         c.w = w[v];
@@ -480,8 +495,49 @@ struct Run {
             c.cinit_t = dinit_t[u];
           }
           dinit[u] = 0;
+          // the launch completes u's error: it forms u's error operand and
+          // carry itself when v is u's only consumer
+          const Rows qu = band_rows(r, u);
+          const lrcnn_node &du = P.nodes[u];
+          if (!P.fuse_act.empty() && P.fuse_act[u] == v) {
+            if (qu.hi != qu.b || c.y0 != qu.lo || c.y1 != qu.b)
+              return lrcnn_fail(LRCNN_EINVAL, "internal: fused error operand rows");
+            const Shape &sh = P.shp[u];
+            const int oa = std::max(qu.a, qu.lo);
+            c.fa = oa;
+            c.fdc = View{ws + L.dc[u], (long long)(qu.b - oa) * sh.w * sh.c, oa, sh.w, sh.c,
+                         qu.b - oa};
+            c.fz = act[u];
+            c.frelu = du.relu;
+            c.fscale = du.affine ? sc[u] : nullptr;
+            if (oa > qu.lo) {
+              // carried-out rows staged in u's error window, moved to the
+              // carry buffer once the launch has read the rows carried in
+              if (sched != S_CARRY || r == 0)
+                return lrcnn_fail(LRCNN_EINVAL, "internal: rows below a band without carry");
+              c.fcarry = View{ws + L.delta[u], (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo,
+                              sh.w, sh.c, L.carry_cap[u]};
+              stage = View{carry_ptr(u, r), (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo,
+                           sh.w, sh.c, L.carry_cap[u]};
+              if (!holds(c.fcarry, qu.lo, oa) || !holds(stage, qu.lo, oa))
+                return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+              stage_u = u;
+              stage_a = oa;
+            }
+            if (oa < qu.b && !holds(act[u], oa, qu.b))
+              return lrcnn_fail(LRCNN_EINVAL, "internal: activation rows not held");
+            c.fact = 1;
+            act_done[u] = 1;
+          }
         }
         LAUNCH(launch_conv(dt, 1, c, stream), "input gradient");
+        if (stage_u >= 0) {
+          const Shape &sh = P.shp[stage_u];
+          const Rows qu = band_rows(r, stage_u);
+          LAUNCH(launch_rows_copy(DT_F32, DT_F32, c.fcarry, stage, 0, B, qu.lo, stage_a, sh.w,
+                                  sh.c, stream),
+                 "carry store");
+        }
       }
     } else if (d.op == LRCNN_OP_MAXPOOL) {
       PoolBwdArgs p{};
@@ -530,6 +586,7 @@ struct Run {
   int band_bwd(int r, const void *dy, float *const *dw, void *dx, float *dxacc) {
     const int n = P.n, B = P.cfg.batch;
     const bool want_dx = dx != nullptr;
+    std::fill(act_done.begin(), act_done.end(), 0);
     // seed: the band's own rows of dL/dy
     {
       const Rows q = band_rows(r, n - 1);
@@ -563,6 +620,18 @@ struct Run {
             dinit_carry[u] = delta_view(r, u, dinit_cv[u], dinit_t[u]) ? 1 : 0;
             continue;
           }
+          if (!P.fuse_act.empty() && P.fuse_act[u] == v) {
+            // v's input gradient forms u's error operand; a band without
+            // rows of v holds nothing of u (the planner checked), and u's
+            // error window has no memory of its own
+            const Rows qu = band_rows(r, u);
+            if (qu.b > qu.a || qu.lo != qu.a)
+              return lrcnn_fail(LRCNN_EINVAL, "internal: fused error operand without launch");
+            View cv;
+            int t = 0;
+            delta_view(r, u, cv, t);
+            continue;
+          }
           int st = init_delta(r, u);
           if (st != LRCNN_OK) return st;
         }
@@ -571,11 +640,12 @@ struct Run {
       // a conv's carried rows left with its error operand, unless the band
       // owns none of its rows (node_bwd then launches nothing)
       const Rows qv = band_rows(r, v);
-      if (sched == S_CARRY && r > 0 && (d.op != LRCNN_OP_CONV || qv.b <= qv.a)) {
+      if (sched == S_CARRY && r > 0 && (d.op != LRCNN_OP_CONV || qv.b <= qv.a) &&
+          !act_done[v]) {
         const Rows q = band_rows(r, v);
         if (q.a > q.lo) {
           const Shape &s = P.shp[v];
-          View cv{ws + L.carry[v], (long long)L.carry_cap[v] * s.w * s.c, q.lo, s.w, s.c,
+          View cv{carry_ptr(v, r), (long long)L.carry_cap[v] * s.w * s.c, q.lo, s.w, s.c,
                   L.carry_cap[v]};
           if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
           LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[v], cv, 0, B, q.lo, q.a, s.w, s.c, stream),
@@ -602,7 +672,7 @@ struct Run {
                                 s.w, s.c, stream),
                "input gradient store");
         if (sched == S_CARRY && r > 0 && q.a > q.lo) {
-          View cv{ws + L.carry[0], (long long)L.carry_cap[0] * s.w * s.c, q.lo, s.w, s.c,
+          View cv{carry_ptr(0, r), (long long)L.carry_cap[0] * s.w * s.c, q.lo, s.w, s.c,
                   L.carry_cap[0]};
           if (!holds(cv, q.lo, q.a)) return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
           LAUNCH(launch_rows_copy(DT_F32, DT_F32, dlt[0], cv, 0, B, q.lo, q.a, s.w, s.c, stream),
@@ -847,6 +917,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
 }
 
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
+extern "C" void lrcnn_debug_act_fusion(int on) { lrcnn::g_no_act_fusion = on == 0; }
 extern "C" void lrcnn_debug_dgrad_phases(int mode) { lrcnn::set_dgrad_phases(mode); }
 
 extern "C" void lrcnn_debug_profile(int on) { lrcnn::profile_enable(on); }

@@ -482,6 +482,37 @@ __device__ __forceinline__ const float *dgrad_base(const ConvArgs &a, int b, int
   return nullptr;
 }
 
+// Store V input-gradient values o of pixel (b, y, x), channels n.., at d
+// in the error window, or, when the launch completes the producer's error
+// (fact), as the producer's error operand (ReLU mask, affine scale,
+// storage dtype; the same arithmetic as the activation backward) or its
+// float32 carry to the previous band.
+template <typename T, int V>
+__device__ __forceinline__ void dgrad_out(const ConvArgs &a, int b, int y, int x, int n,
+                                          float (&o)[4], float *d) {
+  if (!a.fact) {
+    stv<float, V>(d, o);
+    return;
+  }
+  const int inner = x * a.N + n;
+  if (y < a.fa) {
+    stv<float, V>((float *)a.fcarry.p + view_off(a.fcarry, b, y, inner), o);
+    return;
+  }
+  if (a.frelu) {
+    float zz[4];
+    ldv<T, V>((const T *)a.fz.p + view_off(a.fz, b, y, inner), zz);
+#pragma unroll
+    for (int e = 0; e < V; ++e)
+      if (!(zz[e] > 0.f)) o[e] = 0.f;
+  }
+  if (a.fscale) {
+#pragma unroll
+    for (int e = 0; e < V; ++e) o[e] *= a.fscale[n + e];
+  }
+  stv<T, V>((T *)a.fdc.p + view_off(a.fdc, b, y, inner), o);
+}
+
 // ------------------------------------------- conv forward / input grad
 template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1>
 // bfloat16: three workgroups per CU (the register budget is set for it;
@@ -885,8 +916,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       const float4 q = *(const float4 *)&Ct[(r - h0) * FP + cc * 4];
       const float *bp = dgrad_base(a, b, y, (long long)x * a.N + n, (const float *)d);
       float4 o = bp ? *(const float4 *)bp : make_float4(0.f, 0.f, 0.f, 0.f);
-      o.x += q.x, o.y += q.y, o.z += q.z, o.w += q.w;
-      *d = o;
+      float ov[4] = {o.x + q.x, o.y + q.y, o.z + q.z, o.w + q.w};
+      dgrad_out<T, 4>(a, b, y, x, n, ov, (float *)d);
     }
     }
     return;
@@ -910,7 +941,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         if (DGRAD) {
           float *d = (float *)a.dst.p + off + n;
           const float *bp = dgrad_base(a, b, y, (long long)x * a.N + n, d);
-          *d = (bp ? *bp : 0.f) + val;
+          float ov[4] = {(bp ? *bp : 0.f) + val, 0.f, 0.f, 0.f};
+          dgrad_out<T, 1>(a, b, y, x, n, ov, d);
         } else {
           if (a.scale) val = val * a.scale[n] + a.shift[n];
           if (a.relu) val = val > 0.f ? val : 0.f;
@@ -974,7 +1006,7 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
     if (bp) ldv<float, V>(bp, q);
 #pragma unroll
     for (int k = 0; k < V; ++k) q[k] += val[k];
-    stv<float, V>(d, q);
+    dgrad_out<T, V>(a, b, y, x, n, q, d);
   } else {
     float rv[4];
     if (a.res.p)

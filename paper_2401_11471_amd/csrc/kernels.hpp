@@ -93,6 +93,14 @@ struct ConvArgs {
   // of the kh_full x kw_full kernel; W is read with the full kernel's
   // strides (taps_full taps, kw_full columns)
   int pst, px0, ty0, tx0, kw_full, taps_full;
+  // input gradient with fact = 1 (the launch completes the producer's
+  // error): no error window is written; rows >= fa, masked by ReLU of fz
+  // (when frelu) and scaled by fscale (nullable), are stored in the
+  // storage dtype to the error operand fdc, rows < fa as float32 to fcarry
+  int fact;
+  View fdc, fz, fcarry;
+  const float *fscale;
+  int frelu, fa;
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 // input gradients of strided convolutions on the calling thread: 0 = split

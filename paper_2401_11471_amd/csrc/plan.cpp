@@ -35,6 +35,8 @@ extern "C" const char *lrcnn_last_error(void) { return g_err.c_str(); }
 
 namespace lrcnn {
 
+thread_local bool g_no_act_fusion = false;
+
 // k, s, p of the window through which node v reads its input(s); an ADD
 // reads row y of each input for output row y.
 static void ksp(const lrcnn_node &nd, int &k, int &s, int &p) {
@@ -386,7 +388,11 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   for (int v = 0; v < n; ++v) {
     int first = v;
     for (int c : P.cons[v]) first = std::max(first, c);
-    bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, cap[v]) * 4, 0};
+    // (an act-fused conv's error window only stages the rows its consumer's
+    // input gradient carries out, which the launch may not write into the
+    // carry buffer it reads the rows carried in from)
+    const bool staged = !P.fuse_act.empty() && P.fuse_act[v];
+    bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, staged ? carry[v] : cap[v]) * 4, 0};
   }
   std::vector<int> dc_i(n, -1), wp_i(n, -1);
   for (int v = 1; v < n; ++v) {
@@ -395,7 +401,11 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
     for (int u = v - 1; u >= 1 && !nxt; --u)
       if (P.nodes[u].op == LRCNN_OP_CONV) nxt = u;
     // (a conv fed by an add's backward gets its error operand at the add's step)
-    const int s0 = n - 1 - (P.fuse_add.empty() || !P.fuse_add[v] ? v : P.fuse_add[v]);
+    // (or at the step of the conv whose input gradient forms it)
+    const int early = !P.fuse_add.empty() && P.fuse_add[v]   ? P.fuse_add[v]
+                      : !P.fuse_act.empty() && P.fuse_act[v] ? P.fuse_act[v]
+                                                             : v;
+    const int s0 = n - 1 - early;
     const int s1 = nxt ? n - 2 - nxt : n - 1;
     dc_i[v] = (int)bufs.size();
     bufs.push_back(LiveBuf{s0, s1, P.elems(v, own[v]) * P.es, 0});
@@ -531,6 +541,32 @@ static int build(Plan &P) {
            P.rows_fp[r][v].lo == P.rows_fp[r][v].a;
     if (ok) P.fuse_fwd[v] = c;
   }
+  // convs whose error operand the input gradient of their only consumer v
+  // forms: in every band (and in the layer-wise schedule) v's launch must
+  // cover exactly u's error-window rows, which end with u's own rows, or
+  // the band must hold nothing of u; u's float32 error window is then never
+  // used
+  P.fuse_act.assign(n, 0);
+  if (carry && !g_no_act_fusion)
+    for (int u = 1; u < n; ++u) {
+      if (P.nodes[u].op != LRCNN_OP_CONV || P.fuse_add[u] || P.cons[u].size() != 1) continue;
+      const int v = P.cons[u][0];
+      const lrcnn_node &d = P.nodes[v];
+      if (d.op != LRCNN_OP_CONV) continue;
+      const int hu = P.shp[u].h;
+      bool ok = std::min(hu, (P.shp[v].h - 1) * d.sh - d.ph + d.kh) == hu;  // layer-wise
+      for (int r = 0; r < nb && ok; ++r) {
+        const Rows &qv = P.rows[r][v], &qu = P.rows[r][u];
+        if (qv.b > qv.a) {
+          const int y0 = std::max(0, qv.a * d.sh - d.ph);
+          const int y1 = std::min(hu, (qv.b - 1) * d.sh - d.ph + d.kh);
+          ok = y0 == qu.lo && y1 == qu.hi && qu.hi == qu.b && qu.lo <= qu.a;
+        } else {
+          ok = qu.b <= qu.a && qu.lo == qu.a;
+        }
+      }
+      if (ok) P.fuse_act[u] = v;
+    }
   // capacities
   std::vector<int> cap(n, 0), own(n, 0), cry(n, 0), fcap(n, 0);
   for (int r = 0; r < nb; ++r)

@@ -74,6 +74,11 @@ struct Plan {
   // add's later input, fused in its backward, same rows in every band and
   // whole 16-byte channel vectors), else 0
   std::vector<int> fuse_fwd;
+  // per conv u (CARRY / layer-wise): its only consumer, a conv v, whose
+  // input gradient may form u's error operand and carry directly (when that
+  // launch initializes u's whole error window); u's error operand then lives
+  // from v's backward step
+  std::vector<int> fuse_act;
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   double tau = 0, flops_rows = 0;
@@ -110,6 +115,10 @@ struct Plan {
 
 // Releases the executor's side stream and events of a plan (exec.cpp).
 void release_side(Plan &P);
+
+// planning on the calling thread forms every error operand by its own
+// activation-backward pass (test hook)
+extern thread_local bool g_no_act_fusion;
 
 }  // namespace lrcnn
 
