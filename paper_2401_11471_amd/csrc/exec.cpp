@@ -349,11 +349,58 @@ struct Run {
     return false;
   }
 
-  // The input gradient of conv v initializes u's error window itself (no
-  // zeroing pass) when it writes every row of the window this band uses.
+  // When v's backward launch (rows [y0, y1) of u) completes u's error and v
+  // is u's only consumer, the launch forms u's error operand and carried
+  // rows itself (eo); the carried-out rows are staged in u's error window
+  // and moved to `stage` (u's carry buffer) after the launch, which reads
+  // the rows carried in from that buffer. stage_a = 0 when nothing is staged.
+  int fuse_err(int r, int v, int u, int y0, int y1, ErrOut &eo, View &stage, int &stage_a) {
+    stage_a = 0;
+    if (P.fuse_act.empty() || P.fuse_act[u] != v) return LRCNN_OK;
+    const Rows qu = band_rows(r, u);
+    const lrcnn_node &du = P.nodes[u];
+    const Shape &sh = P.shp[u];
+    if (qu.hi != qu.b || y0 != qu.lo || y1 != qu.b)
+      return lrcnn_fail(LRCNN_EINVAL, "internal: fused error operand rows");
+    const int oa = std::max(qu.a, qu.lo);
+    eo.fact = 1;
+    eo.fa = oa;
+    eo.dc = View{ws + L.dc[u], (long long)(qu.b - oa) * sh.w * sh.c, oa, sh.w, sh.c, qu.b - oa};
+    eo.z = act[u];
+    eo.relu = du.relu;
+    eo.scale = du.affine ? sc[u] : nullptr;
+    if (oa < qu.b && !holds(act[u], oa, qu.b))
+      return lrcnn_fail(LRCNN_EINVAL, "internal: activation rows not held");
+    if (oa > qu.lo) {
+      if (sched != S_CARRY || r == 0)
+        return lrcnn_fail(LRCNN_EINVAL, "internal: rows below a band without carry");
+      eo.carry = View{ws + L.delta[u], (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo, sh.w,
+                      sh.c, L.carry_cap[u]};
+      stage = View{carry_ptr(u, r), (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo, sh.w, sh.c,
+                   L.carry_cap[u]};
+      if (!holds(eo.carry, qu.lo, oa) || !holds(stage, qu.lo, oa))
+        return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+      stage_a = oa;
+    }
+    act_done[u] = 1;
+    return LRCNN_OK;
+  }
+  int unstage(int r, int u, const ErrOut &eo, const View &stage, int stage_a) {
+    if (!stage_a) return LRCNN_OK;
+    const Shape &sh = P.shp[u];
+    const Rows qu = band_rows(r, u);
+    LAUNCH(launch_rows_copy(DT_F32, DT_F32, eo.carry, stage, 0, P.cfg.batch, qu.lo, stage_a,
+                            sh.w, sh.c, stream),
+           "carry store");
+    return LRCNN_OK;
+  }
+
+  // The backward launch of v (a conv's input gradient, a max-pool's
+  // backward) initializes u's error window itself (no zeroing pass) when it
+  // writes every row of the window this band uses.
   bool init_by_dgrad(int r, int v, int u, bool want_dx) const {
     const lrcnn_node &d = P.nodes[v];
-    if (d.op != LRCNN_OP_CONV || (u == 0 && !want_dx)) return false;
+    if ((d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) || (u == 0 && !want_dx)) return false;
     const Rows qv = band_rows(r, v), qu = band_rows(r, u);
     if (qv.b <= qv.a) return false;
     const int y0 = std::max(0, qv.a * d.sh - d.ph);
@@ -467,8 +514,8 @@ struct Run {
       }
       if (u != 0 || want_dx) {
         ConvArgs c{};
-        View stage{};     // carry buffer the staged carried-out rows go to
-        int stage_u = -1, stage_a = 0;
+        View stage{};  // carry buffer the staged carried-out rows go to
+        int stage_a = 0;
         c.src = View{dc, (long long)(b - a) * sv.w * sv.c, a, sv.w, sv.c, b - a};
         c.dst = dlt[u];
         c.w = w[v];
@@ -497,47 +544,10 @@ struct Run {
           dinit[u] = 0;
           // the launch completes u's error: it forms u's error operand and
           // carry itself when v is u's only consumer
-          const Rows qu = band_rows(r, u);
-          const lrcnn_node &du = P.nodes[u];
-          if (!P.fuse_act.empty() && P.fuse_act[u] == v) {
-            if (qu.hi != qu.b || c.y0 != qu.lo || c.y1 != qu.b)
-              return lrcnn_fail(LRCNN_EINVAL, "internal: fused error operand rows");
-            const Shape &sh = P.shp[u];
-            const int oa = std::max(qu.a, qu.lo);
-            c.fa = oa;
-            c.fdc = View{ws + L.dc[u], (long long)(qu.b - oa) * sh.w * sh.c, oa, sh.w, sh.c,
-                         qu.b - oa};
-            c.fz = act[u];
-            c.frelu = du.relu;
-            c.fscale = du.affine ? sc[u] : nullptr;
-            if (oa > qu.lo) {
-              // carried-out rows staged in u's error window, moved to the
-              // carry buffer once the launch has read the rows carried in
-              if (sched != S_CARRY || r == 0)
-                return lrcnn_fail(LRCNN_EINVAL, "internal: rows below a band without carry");
-              c.fcarry = View{ws + L.delta[u], (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo,
-                              sh.w, sh.c, L.carry_cap[u]};
-              stage = View{carry_ptr(u, r), (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo,
-                           sh.w, sh.c, L.carry_cap[u]};
-              if (!holds(c.fcarry, qu.lo, oa) || !holds(stage, qu.lo, oa))
-                return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
-              stage_u = u;
-              stage_a = oa;
-            }
-            if (oa < qu.b && !holds(act[u], oa, qu.b))
-              return lrcnn_fail(LRCNN_EINVAL, "internal: activation rows not held");
-            c.fact = 1;
-            act_done[u] = 1;
-          }
+          if (int e = fuse_err(r, v, u, c.y0, c.y1, c.eo, stage, stage_a)) return e;
         }
         LAUNCH(launch_conv(dt, 1, c, stream), "input gradient");
-        if (stage_u >= 0) {
-          const Shape &sh = P.shp[stage_u];
-          const Rows qu = band_rows(r, stage_u);
-          LAUNCH(launch_rows_copy(DT_F32, DT_F32, c.fcarry, stage, 0, B, qu.lo, stage_a, sh.w,
-                                  sh.c, stream),
-                 "carry store");
-        }
+        if (int e = unstage(r, u, c.eo, stage, stage_a)) return e;
       }
     } else if (d.op == LRCNN_OP_MAXPOOL) {
       PoolBwdArgs p{};
@@ -553,7 +563,22 @@ struct Run {
       p.ub = std::min(su.h, (b - 1) * d.sh - d.ph + d.kh);
       p.Wu = su.w;
       p.kh = d.kh, p.kw = d.kw, p.sh = d.sh, p.sw = d.sw, p.ph = d.ph, p.pw = d.pw;
-      LAUNCH(launch_pool_bwd(p, stream), "max-pool backward");
+      View stage{};
+      int stage_a = 0;
+      if (dinit[u]) {
+        // this launch writes every row of u's window: no zeroing pass
+        p.dst_init = 1;
+        if (dinit_carry[u]) {
+          if (!holds(dinit_cv[u], dinit_t[u], band_rows(r, u).b))
+            return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+          p.cinit = dinit_cv[u];
+          p.cinit_t = dinit_t[u];
+        }
+        dinit[u] = 0;
+        if (int e = fuse_err(r, v, u, p.ua, p.ub, p.eo, stage, stage_a)) return e;
+      }
+      LAUNCH(launch_pool_bwd(dt, p, stream), "max-pool backward");
+      if (int e = unstage(r, u, p.eo, stage, stage_a)) return e;
     } else {
       AddSide side_in[2];
       const int in_ids[2] = {d.in0, d.in1};

@@ -474,43 +474,52 @@ static RowIter row_iter(int B, int r0, int r1, int W, int C, int V) {
 // Base value an input-gradient element is added to: the error window's
 // current value, or, when the launch initializes the window, the carried
 // error (rows >= cinit_t) or zero. `inner` = x * C + c.
-__device__ __forceinline__ const float *dgrad_base(const ConvArgs &a, int b, int y,
-                                                   long long inner, const float *cur) {
-  if (!a.dst_init) return cur;
-  if (a.cinit.p && y >= a.cinit_t)
-    return (const float *)a.cinit.p + view_off(a.cinit, b, y, (int)inner);
+__device__ __forceinline__ const float *err_base(int init, const View &cinit, int cinit_t, int b,
+                                                 int y, long long inner, const float *cur) {
+  if (!init) return cur;
+  if (cinit.p && y >= cinit_t)
+    return (const float *)cinit.p + view_off(cinit, b, y, (int)inner);
   return nullptr;
 }
+__device__ __forceinline__ const float *dgrad_base(const ConvArgs &a, int b, int y,
+                                                   long long inner, const float *cur) {
+  return err_base(a.dst_init, a.cinit, a.cinit_t, b, y, inner, cur);
+}
 
-// Store V input-gradient values o of pixel (b, y, x), channels n.., at d
-// in the error window, or, when the launch completes the producer's error
-// (fact), as the producer's error operand (ReLU mask, affine scale,
+// Store V error values o of pixel (b, y, x), channels n.. of C, at d in
+// the error window, or, when the launch completes the producer's error
+// (eo.fact), as the producer's error operand (ReLU mask, affine scale,
 // storage dtype; the same arithmetic as the activation backward) or its
 // float32 carry to the previous band.
 template <typename T, int V>
-__device__ __forceinline__ void dgrad_out(const ConvArgs &a, int b, int y, int x, int n,
-                                          float (&o)[4], float *d) {
-  if (!a.fact) {
+__device__ __forceinline__ void err_out(const ErrOut &eo, int C, int b, int y, int x, int n,
+                                        float (&o)[4], float *d) {
+  if (!eo.fact) {
     stv<float, V>(d, o);
     return;
   }
-  const int inner = x * a.N + n;
-  if (y < a.fa) {
-    stv<float, V>((float *)a.fcarry.p + view_off(a.fcarry, b, y, inner), o);
+  const int inner = x * C + n;
+  if (y < eo.fa) {
+    stv<float, V>((float *)eo.carry.p + view_off(eo.carry, b, y, inner), o);
     return;
   }
-  if (a.frelu) {
+  if (eo.relu) {
     float zz[4];
-    ldv<T, V>((const T *)a.fz.p + view_off(a.fz, b, y, inner), zz);
+    ldv<T, V>((const T *)eo.z.p + view_off(eo.z, b, y, inner), zz);
 #pragma unroll
     for (int e = 0; e < V; ++e)
       if (!(zz[e] > 0.f)) o[e] = 0.f;
   }
-  if (a.fscale) {
+  if (eo.scale) {
 #pragma unroll
-    for (int e = 0; e < V; ++e) o[e] *= a.fscale[n + e];
+    for (int e = 0; e < V; ++e) o[e] *= eo.scale[n + e];
   }
-  stv<T, V>((T *)a.fdc.p + view_off(a.fdc, b, y, inner), o);
+  stv<T, V>((T *)eo.dc.p + view_off(eo.dc, b, y, inner), o);
+}
+template <typename T, int V>
+__device__ __forceinline__ void dgrad_out(const ConvArgs &a, int b, int y, int x, int n,
+                                          float (&o)[4], float *d) {
+  err_out<T, V>(a.eo, a.N, b, y, x, n, o, d);
 }
 
 // ------------------------------------------- conv forward / input grad
@@ -1573,7 +1582,7 @@ int launch_pool_fwd(int dt, const PoolArgs &a0, void *stream) {
   return (int)hipGetLastError();
 }
 
-template <int V>
+template <typename T, int V>
 __global__ void pool_bwd_kernel(PoolBwdArgs a) {
   const int Ru = a.ub - a.ua, R = a.y1 - a.y0;
   const int CV = a.C / V;
@@ -1614,25 +1623,32 @@ __global__ void pool_bwd_kernel(PoolBwdArgs a) {
           if (a.am[ai + e] == tp) sum[e] += dv[e];
       }
     float *d = (float *)a.du.p + b * a.du.bs + (yi - a.du.row0) * urow + (long long)xi * a.C + c;
-    float q[4];
-    ldv<float, V>(d, q);
+    const float *bp = err_base(a.dst_init, a.cinit, a.cinit_t, b, yi, (long long)xi * a.C + c, d);
+    float q[4] = {0.f, 0.f, 0.f, 0.f};
+    if (bp) ldv<float, V>(bp, q);
 #pragma unroll
     for (int e = 0; e < V; ++e) q[e] += sum[e];
-    stv<float, V>(d, q);
+    err_out<T, V>(a.eo, a.C, b, yi, xi, c, q, d);
   }
 }
 
-int launch_pool_bwd(const PoolBwdArgs &a0, void *stream) {
+int launch_pool_bwd(int dt, const PoolBwdArgs &a0, void *stream) {
   const long long total = (long long)a0.B * (a0.ub - a0.ua) * a0.Wu * a0.C;
   if (total <= 0) return 0;
   PoolBwdArgs a = a0;
   a.fcv = fast_div((uint32_t)(a.C % 4 == 0 ? a.C / 4 : a.C));
   a.fw = fast_div((uint32_t)a.Wu);
   a.fr = fast_div((uint32_t)(a.ub - a.ua));
-  if (a.C % 4 == 0)
-    pool_bwd_kernel<4><<<grid_for(total / 4), 256, 0, (hipStream_t)stream>>>(a);
-  else
-    pool_bwd_kernel<1><<<grid_for(total), 256, 0, (hipStream_t)stream>>>(a);
+  hipStream_t s = (hipStream_t)stream;
+  const bool v4 = a.C % 4 == 0;
+  const unsigned g = grid_for(v4 ? total / 4 : total);
+  if (dt == DT_F32) {
+    if (v4) pool_bwd_kernel<float, 4><<<g, 256, 0, s>>>(a);
+    else pool_bwd_kernel<float, 1><<<g, 256, 0, s>>>(a);
+  } else {
+    if (v4) pool_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(a);
+    else pool_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(a);
+  }
   return (int)hipGetLastError();
 }
 

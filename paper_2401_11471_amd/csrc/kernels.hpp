@@ -52,6 +52,18 @@ struct View {
 
 enum Dt { DT_F32 = 0, DT_BF16 = 1 };
 
+// Where a backward launch that completes a producer's error for the band
+// puts it (fact = 1): rows >= fa, masked by ReLU of z (when relu) and
+// scaled per channel by scale (nullable), go in the storage dtype to the
+// producer's error operand dc; rows < fa go as float32 to carry. With
+// fact = 0 the launch writes the producer's float32 error window.
+struct ErrOut {
+  int fact;
+  View dc, z, carry;
+  const float *scale;
+  int relu, fa;
+};
+
 // Conv forward over rows [y0, y1) of the output, or (dgrad = 1) the input
 // gradient over rows [y0, y1) of the producer from the consumer rows
 // [sy0, sy1). See kernels.hip for the operand conventions.
@@ -93,14 +105,8 @@ struct ConvArgs {
   // of the kh_full x kw_full kernel; W is read with the full kernel's
   // strides (taps_full taps, kw_full columns)
   int pst, px0, ty0, tx0, kw_full, taps_full;
-  // input gradient with fact = 1 (the launch completes the producer's
-  // error): no error window is written; rows >= fa, masked by ReLU of fz
-  // (when frelu) and scaled by fscale (nullable), are stored in the
-  // storage dtype to the error operand fdc, rows < fa as float32 to fcarry
-  int fact;
-  View fdc, fz, fcarry;
-  const float *fscale;
-  int frelu, fa;
+  // input gradient: where the producer's completed error goes
+  ErrOut eo;
 };
 int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream);
 // input gradients of strided convolutions on the calling thread: 0 = split
@@ -270,8 +276,15 @@ struct PoolBwdArgs {
   int B, y0, y1, Wv, C, ua, ub, Wu;
   int kh, kw, sh, sw, ph, pw;
   FastDiv fcv, fw, fr;  // C / V, Wu, ub - ua (set by the launcher)
+  // dst_init = 1: initialize the producer's error window (the float32
+  // carry from rows >= cinit_t when cinit.p is set, else zero) instead of
+  // adding to it; rows [ua, ub) must be every row of the window
+  int dst_init;
+  View cinit;
+  int cinit_t;
+  ErrOut eo;  // where the completed error goes
 };
-int launch_pool_bwd(const PoolBwdArgs &a, void *stream);
+int launch_pool_bwd(int dt, const PoolBwdArgs &a, void *stream);
 
 // z = relu?(a + b) over rows [y0, y1) (storage dtype).
 int launch_add_fwd(int dt, View a, View b, View z, int relu, uint8_t *mask,

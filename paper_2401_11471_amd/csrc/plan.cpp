@@ -541,8 +541,8 @@ static int build(Plan &P) {
            P.rows_fp[r][v].lo == P.rows_fp[r][v].a;
     if (ok) P.fuse_fwd[v] = c;
   }
-  // convs whose error operand the input gradient of their only consumer v
-  // forms: in every band (and in the layer-wise schedule) v's launch must
+  // convs whose error operand the backward launch of their only consumer v
+  // (a conv's input gradient, a max-pool's backward) forms: in every band (and in the layer-wise schedule) v's launch must
   // cover exactly u's error-window rows, which end with u's own rows, or
   // the band must hold nothing of u; u's float32 error window is then never
   // used
@@ -552,7 +552,7 @@ static int build(Plan &P) {
       if (P.nodes[u].op != LRCNN_OP_CONV || P.fuse_add[u] || P.cons[u].size() != 1) continue;
       const int v = P.cons[u][0];
       const lrcnn_node &d = P.nodes[v];
-      if (d.op != LRCNN_OP_CONV) continue;
+      if (d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) continue;
       const int hu = P.shp[u].h;
       bool ok = std::min(hu, (P.shp[v].h - 1) * d.sh - d.ph + d.kh) == hu;  // layer-wise
       for (int r = 0; r < nb && ok; ++r) {
