@@ -25,6 +25,14 @@ void lrcnn_debug_dry_run(int on);
  * (CARRY plans). Both do the same arithmetic, so results are bitwise equal. */
 void lrcnn_debug_act_fusion(int on);
 
+/* on != 0: on the calling thread, lrcnn_forward_rows of CARRY plans with
+ * more than one band runs consecutive bands on two streams, each step of a
+ * band waiting only until the previous band no longer reads the windows it
+ * writes (split-K partial sums of the second stream in the idle backward
+ * arena); on == 0 (default) the bands run one after another on the
+ * caller's stream. Results are bitwise equal. */
+void lrcnn_debug_fp_pipeline(int on);
+
 /* On the calling thread, the input gradient of a strided convolution
  * (stride s in both directions) is computed as s^2 launches, one per phase
  * of producer rows and columns ((y + pad) mod s), each with only the taps

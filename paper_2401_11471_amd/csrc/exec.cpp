@@ -20,6 +20,10 @@ enum Sched { S_CARRY, S_RECOMPUTE, S_LAYERWISE };
 // Dry-run mode (test hook): the executor walks the schedule and runs every
 // host-side check but enqueues nothing, so it runs without a GPU.
 thread_local bool g_dry = false;
+// forward bands one after another (the pipelined forward is opt-in: a
+// ResNet-50 bfloat16 graph-captured run with it ended in an abort whose
+// cause is not yet known)
+thread_local bool g_no_fp_pipe = true;
 
 #define LAUNCH(call, what)                                                 \
   do {                                                                     \
@@ -58,6 +62,26 @@ bool ensure_side(Plan &P) {
   return true;
 }
 
+// Events of the pipelined forward pass (created once per plan and device,
+// with the side stream).
+bool ensure_fp_events(Plan &P) {
+  if ((int)P.ev_fp.size() == 2 * P.n && P.ev_fork) return true;
+  for (void *e : P.ev_fp)
+    if (e) (void)hipEventDestroy((hipEvent_t)e);
+  P.ev_fp.assign(2 * P.n, nullptr);
+  for (auto &e : P.ev_fp) {
+    hipEvent_t h = nullptr;
+    if (hipEventCreateWithFlags(&h, hipEventDisableTiming) != hipSuccess) return false;
+    e = h;
+  }
+  if (!P.ev_fork) {
+    hipEvent_t h = nullptr;
+    if (hipEventCreateWithFlags(&h, hipEventDisableTiming) != hipSuccess) return false;
+    P.ev_fork = h;
+  }
+  return true;
+}
+
 struct Run {
   Plan &P;
   const Layout &L;
@@ -84,6 +108,12 @@ struct Run {
   hipStream_t side = nullptr;  // weight-gradient stream (backward only)
   bool wg_pending = false;     // a weight gradient on `side` not yet joined
   bool dx_f32 = false;         // store dL/dx as float32 (a checkpoint's error)
+  // forward pass pipelined over bands (two streams by band parity): band r's
+  // step of node v waits until band r-1 has finished every step that reads
+  // the windows this step writes, and records ev_cur[v]
+  bool pipe = false;
+  hipEvent_t *ev_cur = nullptr, *ev_prev = nullptr;
+  size_t part_off = 0;  // split-K partial sums of this band's stream
 
   Run(Plan &p, const Layout &l, Sched s, void *wsp, const void *x_,
       const void *const *w_, const float *const *sc_, const float *const *sf_,
@@ -102,6 +132,28 @@ struct Run {
       for (int c : P.cons[v]) first_consumer[v] = std::max(first_consumer[v], c);
     const Shape &s0 = P.shp[0];
     act[0] = View{const_cast<void *>(x), (long long)s0.h * s0.w * s0.c, 0, s0.w, s0.c, s0.h};
+    part_off = L.part;
+  }
+
+  // last step (node index) of a band that reads node v's window
+  int last_reader(int v) const {
+    int c = v;
+    for (int k : P.cons[v]) c = std::max(c, k);
+    return c;
+  }
+  // the windows node v's step writes (its own, and the residual add's when
+  // the conv computes it) are no longer read by the previous band
+  int pipe_wait(int v) {
+    if (!pipe || !ev_prev) return LRCNN_OK;
+    int w = last_reader(v);
+    if (!P.fuse_fwd.empty() && P.fuse_fwd[v]) w = std::max(w, last_reader(P.fuse_fwd[v]));
+    LAUNCH(hipStreamWaitEvent((hipStream_t)stream, ev_prev[w], 0), "band wait");
+    return LRCNN_OK;
+  }
+  int pipe_record(int v) {
+    if (!pipe) return LRCNN_OK;
+    LAUNCH(hipEventRecord(ev_cur[v], (hipStream_t)stream), "band record");
+    return LRCNN_OK;
   }
 
   View full(void *p, int v) const {
@@ -166,7 +218,7 @@ struct Run {
       c.sy0 = 0;
       c.sy1 = su.h;
       c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
-      c.part = (float *)(ws + L.part);
+      c.part = (float *)(ws + part_off);
       c.part_bytes = L.part_bytes;
       if (res) {
         c.res = *res;
@@ -236,7 +288,8 @@ struct Run {
     const int n = P.n;
     const bool fp = !bp && sched != S_LAYERWISE;
     const bool packed = fp && L.fp_packed;
-    const bool batch = !packed;
+    // (pipelined: strips loaded and stored at each node's own step)
+    const bool batch = !packed && !(fp && pipe);
     std::vector<CopySeg> segs;
     int st;
     // views of every node's rows, and the strip loads
@@ -269,6 +322,7 @@ struct Run {
     for (int v = 1; v < n; ++v) {
       const Rows q = fp ? P.rows_fp[r][v] : band_rows(r, v);
       const View dst = act[v];
+      if (fp && (st = pipe_wait(v)) != LRCNN_OK) return st;
       if (sched == S_CARRY && r > 0 && q.a > q.lo && !batch) {
         const int sidx = fp ? r * P.refine - 1 : r - 1;
         View strip = win(L.strip[sidx][v], v, q.a - q.lo, q.lo);
@@ -317,6 +371,7 @@ struct Run {
             return st;
         }
       }
+      if (fp && (st = pipe_record(v)) != LRCNN_OK) return st;
     }
     return flush_copies(segs, "strip store");
   }
@@ -777,6 +832,11 @@ uint64_t g_epoch = 0;
 }  // namespace
 
 void release_side(Plan &P) {
+  for (void *e : P.ev_fp)
+    if (e) (void)hipEventDestroy((hipEvent_t)e);
+  P.ev_fp.clear();
+  if (P.ev_fork) (void)hipEventDestroy((hipEvent_t)P.ev_fork);
+  P.ev_fork = nullptr;
   if (P.ev_act) (void)hipEventDestroy((hipEvent_t)P.ev_act);
   if (P.ev_wg) (void)hipEventDestroy((hipEvent_t)P.ev_wg);
   if (P.side_stream) (void)hipStreamDestroy((hipStream_t)P.side_stream);
@@ -856,9 +916,38 @@ extern "C" int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x, const void 
   // the last band's maps can serve the BP only when both passes use the
   // same partition
   const bool keep = P.refine == 1 && !P.no_keep;
-  for (int r = 0; r < P.nb_fp; ++r)
+  // bands on alternating streams (the backward's side stream is idle here),
+  // the second one with its partial sums in the idle backward arena
+  // (a dry run walks the same schedule with placeholder events)
+  std::vector<void *> dry_ev;
+  const bool pipe = P.cfg.mode == LRCNN_CARRY && P.nb_fp > 1 && !P.rc.fp_packed &&
+                    P.rc.arena_bytes >= P.rc.part_bytes && !g_no_fp_pipe &&
+                    (g_dry || (ensure_side(P) && ensure_fp_events(P)));
+  if (pipe && g_dry) dry_ev.assign(2 * P.n, nullptr);
+  void **evs = g_dry ? dry_ev.data() : P.ev_fp.data();
+  hipStream_t sides[2] = {(hipStream_t)stream, pipe ? (hipStream_t)P.side_stream : nullptr};
+  if (pipe) {
+    LAUNCH(hipEventRecord((hipEvent_t)P.ev_fork, sides[0]), "event record");
+    if (!sides[1] && !g_dry) return lrcnn_fail(LRCNN_EHIP, "side stream");
+    LAUNCH(hipStreamWaitEvent(sides[1], (hipEvent_t)P.ev_fork, 0), "stream fork");
+    run.pipe = true;
+  }
+  for (int r = 0; r < P.nb_fp; ++r) {
+    if (pipe) {
+      run.stream = sides[r & 1];
+      run.part_off = r & 1 ? P.rc.arena : P.rc.part;
+      run.ev_cur = (hipEvent_t *)evs + (r & 1) * P.n;
+      run.ev_prev = r ? (hipEvent_t *)evs + ((r + 1) & 1) * P.n : nullptr;
+    }
     if ((st = run.band_fwd(r, y, mask_out, false, keep && r == P.nb_fp - 1)) != LRCNN_OK)
       return st;
+  }
+  if (pipe) {
+    // the caller's stream joins the side stream's last band
+    const int rs = (P.nb_fp - 1) & 1 ? P.nb_fp - 1 : P.nb_fp - 2;
+    LAUNCH(hipStreamWaitEvent(sides[0], (hipEvent_t)evs[(rs & 1) * P.n + P.n - 1], 0),
+           "stream join");
+  }
   P.fwd_workspace = workspace;
   P.last_band_kept = keep;
   P.fwd_epoch = ++g_epoch;
@@ -943,6 +1032,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
 
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
 extern "C" void lrcnn_debug_act_fusion(int on) { lrcnn::g_no_act_fusion = on == 0; }
+extern "C" void lrcnn_debug_fp_pipeline(int on) { lrcnn::g_no_fp_pipe = on == 0; }
 extern "C" void lrcnn_debug_dgrad_phases(int mode) { lrcnn::set_dgrad_phases(mode); }
 
 extern "C" void lrcnn_debug_profile(int on) { lrcnn::profile_enable(on); }

@@ -416,6 +416,8 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   }
   size_t dpeak = pack(bufs);
   size_t d0 = A.take(dpeak);
+  L.arena = d0;
+  L.arena_bytes = dpeak;
   for (int v = 0; v < n; ++v) L.delta[v] = d0 + bufs[v].off;
   L.dc.assign(n, 0);
   L.wpart.assign(n, 0);

@@ -24,6 +24,7 @@ struct Rows {
 // Byte offsets of every buffer inside one workspace.
 struct Layout {
   size_t total = 0;
+  size_t arena = 0, arena_bytes = 0;  // backward arena (idle during the forward pass)
   size_t ubase = 0;              // start of the region FP and BP share
   std::vector<size_t> win;       // per node: feature-map window ([B][cap][W][C])
   std::vector<int> win_cap;      // rows of each window
@@ -90,6 +91,10 @@ struct Plan {
   // side stream and two events of the backward, created by the executor on
   // first use for the device current at that call (opaque HIP handles)
   void *side_stream = nullptr, *ev_act = nullptr, *ev_wg = nullptr;
+  // forward pass pipelined over bands: per node, an event after each of two
+  // bands' steps (band parity), and one to fork the side stream
+  std::vector<void *> ev_fp;
+  void *ev_fork = nullptr;
   int side_dev = -1;
   // hybrid depth: nodes < hyb row-centric (sub-plan `row`, nodes 0..hyb-1),
   // nodes >= hyb layer-wise (sub-plan `col`, re-indexed from the checkpoint

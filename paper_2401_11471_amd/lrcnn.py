@@ -102,6 +102,8 @@ def _load():
     lib.lrcnn_last_error.restype = C.c_char_p
     lib.lrcnn_debug_dry_run.argtypes = [C.c_int]
     lib.lrcnn_debug_dry_run.restype = None
+    lib.lrcnn_debug_fp_pipeline.argtypes = [C.c_int]
+    lib.lrcnn_debug_fp_pipeline.restype = None
     lib.lrcnn_debug_act_fusion.argtypes = [C.c_int]
     lib.lrcnn_debug_act_fusion.restype = None
     lib.lrcnn_debug_dgrad_phases.argtypes = [C.c_int]
@@ -130,7 +132,8 @@ EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_head_workspace_bytes",
            "lrcnn_head_loss", "lrcnn_sgd_update", "lrcnn_forward_rows",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
-           "lrcnn_debug_dry_run", "lrcnn_debug_act_fusion", "lrcnn_debug_dgrad_phases",
+           "lrcnn_debug_dry_run", "lrcnn_debug_fp_pipeline", "lrcnn_debug_act_fusion",
+           "lrcnn_debug_dgrad_phases",
            "lrcnn_debug_profile",
            "lrcnn_debug_profile_collect", "lrcnn_debug_profile_entry")
 
@@ -295,6 +298,12 @@ def lrcnn_sgd_update(plan, lr, weights, dws, fc_w=None, d_fc_w=None, fc_b=None, 
 def lrcnn_debug_dry_run(on):
     """Test hook: walk schedules with all host checks but launch nothing."""
     LIB.lrcnn_debug_dry_run(1 if on else 0)
+
+
+def lrcnn_debug_fp_pipeline(on):
+    """Test hook: forward bands pipelined on two streams (on) or sequential (off,
+    the default)."""
+    LIB.lrcnn_debug_fp_pipeline(1 if on else 0)
 
 
 def lrcnn_debug_act_fusion(on):

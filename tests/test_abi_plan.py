@@ -401,3 +401,16 @@ def test_hybrid_auto_picks_the_smallest_workspace(cid):
     assert auto["hybrid_from"] in sizes
     assert auto["workspace_bytes"] == min(sizes.values())
     assert auto["workspace_bytes"] == sizes[auto["hybrid_from"]]
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_executor_dry_run_pipelined_forward(cid):
+    # the opt-in pipelined forward walks the same host checks (windows,
+    # strips, carried rows) with its per-node waits and records
+    c = CONFIGS[cid]
+    L.lrcnn_debug_fp_pipeline(True)
+    try:
+        dry_run(net_nodes(c["net"]), c["batch"], c["h"], c["w"], c["dtype"], L.CARRY,
+                c["bands"])
+    finally:
+        L.lrcnn_debug_fp_pipeline(False)
