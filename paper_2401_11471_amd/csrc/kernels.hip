@@ -523,7 +523,10 @@ __device__ __forceinline__ void dgrad_out(const ConvArgs &a, int b, int y, int x
 }
 
 // ------------------------------------------- conv forward / input grad
-template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1>
+// ONE: a single tap (1x1 kernel, or a phase with one tap): each A row's
+// validity and address are fixed for the launch, so a K step only adds the
+// channel offset.
+template <typename T, int BN, int KR, bool DGRAD, bool VEC, bool S1, bool ONE = false>
 // bfloat16: three workgroups per CU (the register budget is set for it;
 // the swizzled LDS tiles fit three); float32 keeps the registers of two
 __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(ConvArgs a) {
@@ -597,6 +600,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     bx[i] = DGRAD ? (ps > 1 ? (ax[i] + a.pw) / ps : ax[i] + a.pw) : ax[i] * a.sw - a.pw;
     rbase[i] = abase[i] + (long long)by[i] * srow + (long long)bx[i] * a.src.C;
   }
+  bool rowok[NA];
+#pragma unroll
+  for (int i = 0; i < NA; ++i)
+    rowok[i] = ONE && am[i] & (bx[i] >= 0) & (by[i] >= a.sy0) & (by[i] < a.sy1) & (bx[i] < a.Ws);
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
   // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output
   // channel of the consumer), contiguous along n, so each 16-byte load
@@ -662,6 +669,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       int sy, sx;
       bool ok;
       long long off;
+      if (ONE) {
+        ra[i] = load16z(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok);
+        continue;
+      }
       if (DGRAD && !S1) {
         const int ty = by[i] - ti, tx = bx[i] - tj;
         sy = ty / a.sh;
@@ -1084,10 +1095,13 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   // the input gradient of a strided convolution divides by the stride
   // (a phase of it is dense)
   const bool s1 = !DGRAD || (a.sh == 1 && a.sw == 1) || a.pst > 1;
+  const bool one = vec && s1 && a.kh == 1 && a.kw == 1;
   if (bn == 64) {
     if (!s1) {
       if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
       else conv_gemm_kernel<T, 64, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+    } else if (one) {
+      conv_gemm_kernel<T, 64, KR, DGRAD, true, true, true><<<grid, 256, 0, s>>>(a);
     } else if (vec) {
       conv_gemm_kernel<T, 64, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
     } else {
@@ -1097,6 +1111,8 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
     if (!s1) {
       if (vec) conv_gemm_kernel<T, 128, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
       else conv_gemm_kernel<T, 128, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+    } else if (one) {
+      conv_gemm_kernel<T, 128, KR, DGRAD, true, true, true><<<grid, 256, 0, s>>>(a);
     } else if (vec) {
       conv_gemm_kernel<T, 128, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
     } else {
