@@ -455,7 +455,14 @@ struct Run {
   // writes every row of the window this band uses.
   bool init_by_dgrad(int r, int v, int u, bool want_dx) const {
     const lrcnn_node &d = P.nodes[v];
-    if ((d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) || (u == 0 && !want_dx)) return false;
+    if (u == 0 && !want_dx) return false;
+    if (d.op == LRCNN_OP_ADD) {
+      // the add's backward writes its own rows of each input (not when both
+      // inputs are the same node: the second side adds to the first)
+      const Rows qv = band_rows(r, v), qu = band_rows(r, u);
+      return d.in0 != d.in1 && qv.b > qv.a && qv.a == qu.lo && qv.b == qu.hi;
+    }
+    if (d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) return false;
     const Rows qv = band_rows(r, v), qu = band_rows(r, u);
     if (qv.b <= qv.a) return false;
     const int y0 = std::max(0, qv.a * d.sh - d.ph);
@@ -640,7 +647,18 @@ struct Run {
       for (int k = 0; k < 2; ++k) {
         const int x = in_ids[k];
         AddSide &sd = side_in[k];
-        sd = AddSide{dlt[x], nullptr, nullptr, sv.c};
+        sd = AddSide{dlt[x], nullptr, nullptr, sv.c, 0, View{}, 0};
+        if (dinit[x]) {
+          // this launch writes every row of x's window: no zeroing pass
+          sd.init = 1;
+          if (dinit_carry[x]) {
+            if (!holds(dinit_cv[x], dinit_t[x], band_rows(r, x).b))
+              return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+            sd.cinit = dinit_cv[x];
+            sd.cinit_t = dinit_t[x];
+          }
+          dinit[x] = 0;
+        }
         if (fused(x)) {
           // own rows of the conv input equal the add's rows (1 x 1 window)
           const Rows qx = band_rows(r, x);

@@ -1724,9 +1724,10 @@ __device__ __forceinline__ void add_bwd_side(const AddSide &sd, long long idx, i
     for (int k = 0; k < V; ++k) e[k] = sd.scale ? d[k] * sd.scale[(in + k) % sd.C] : d[k];
     stv<T, V>((T *)sd.dc + idx * V, e);
   } else {
-    float x[4];
+    float x[4] = {0.f, 0.f, 0.f, 0.f};
     float *p = (float *)sd.win.p + view_off(sd.win, b, y, in);
-    ldv<float, V>(p, x);
+    const float *bp = err_base(sd.init, sd.cinit, sd.cinit_t, b, y, in, p);
+    if (bp) ldv<float, V>(bp, x);
 #pragma unroll
     for (int k = 0; k < V; ++k) x[k] += d[k];
     stv<float, V>(p, x);

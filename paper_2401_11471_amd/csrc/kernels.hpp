@@ -299,6 +299,12 @@ struct AddSide {
   void *dc;
   const float *scale;
   int C;
+  // window path: init = 1 stores the initial value (the float32 carry from
+  // rows >= cinit_t when cinit.p is set, else zero) plus the error instead
+  // of adding to the window
+  int init;
+  View cinit;
+  int cinit_t;
 };
 int launch_add_bwd(int dt, View dz, View z, const AddSide &sa, const AddSide &sb, int relu,
                    int B, int y0, int y1, int W, int C, void *stream);
