@@ -1208,15 +1208,6 @@ int launch_conv(int dt, int dgrad, const ConvArgs &a, void *stream) {
   return dgrad ? conv_dispatch<bf16, true>(a, s) : conv_dispatch<bf16, false>(a, s);
 }
 
-// q = p / d, r = p % d for 0 <= p with p / d < 2^22, by a float
-// reciprocal and one correction step (the estimate is off by at most one).
-__device__ __forceinline__ void divmod_rcp(int p, int d, float inv, int &q, int &r) {
-  q = (int)((float)p * inv);
-  r = p - q * d;
-  const bool lo = r < 0, hi = r >= d;
-  q += hi ? 1 : (lo ? -1 : 0);
-  r += hi ? -d : (lo ? d : 0);
-}
 
 // ------------------------------------------------------------ weight grad
 // A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
@@ -1274,7 +1265,6 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   V16 ra[NPA], rb[2];
   int k0 = kbeg;
   const bool ovok = ov < a.Co, nbok = nb0 < N;
-  const float invW = 1.0f / (float)a.Wv, invR = 1.0f / (float)R;
   // channel counts that are not a multiple of E (the first layer): the
   // (tap, channel) of each of this thread's E columns, fixed for the launch
   int cti[BVEC ? 1 : E], ctj[BVEC ? 1 : E], cc[BVEC ? 1 : E];
@@ -1311,10 +1301,10 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
       // B: E input values of pixel p under the column's tap
       const int p = k0 + kk0 + KS * i;
       const bool pk = p < kend;
-      int t, x, yy, b;
-      divmod_rcp(pk ? p : 0, a.Wv, invW, t, x);
-      divmod_rcp(t, R, invR, b, yy);
-      const int y = a.y0 + yy;
+      uint32_t t, x, yy, b;
+      fdiv_qr((uint32_t)(pk ? p : 0), a.fw, t, x);
+      fdiv_qr(t, a.fr, b, yy);
+      const int y = a.y0 + (int)yy;
       if (BVEC) {
         const int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
         const bool ok = pk & nbok & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
@@ -1464,13 +1454,14 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, fl
 }
 
 template <typename T>
-static int wgrad_dispatch(const WgradArgs &a, float *dw, hipStream_t s) {
+static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
+  WgradArgs a = a0;
   const int K = a.B * (a.y1 - a.y0) * a.Wv;
   const int N = a.kh * a.kw * a.Ci;
   if (K <= 0) return 0;
-  // the kernel splits pixel indices with float reciprocals (exact below 2^22
-  // quotients)
-  if ((long long)a.B * (a.y1 - a.y0) >= (1LL << 22)) return (int)hipErrorInvalidValue;
+  // pixel indices are split by multiply-shift division
+  a.fw = fast_div((uint32_t)a.Wv);
+  a.fr = fast_div((uint32_t)(a.y1 - a.y0));
   constexpr int BK = Cfg<T>::BK;
   const WgradTiles wt = wgrad_tiles(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
   int splits = wt.splits;

@@ -224,6 +224,7 @@ struct WgradArgs {
   int B, y0, y1, Wv, Co, Ci, Hs, Ws;
   int kh, kw, sh, sw, ph, pw;
   int overwrite;  // 1: dw = this launch's sum (the first band); 0: dw += it
+  FastDiv fw, fr;  // division by Wv and by y1 - y0 (set by the launcher)
 };
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels
