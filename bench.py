@@ -369,7 +369,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} "
+        print(f"bench.py: the library runs on one GPU only; --gpus {args.gpus} "
               f"(WORLD_SIZE={world}) is not supported. Multi-GPU sharding is a "
               "design note, not an implemented path.", file=sys.stderr)
         sys.exit(2)
