@@ -129,6 +129,14 @@ __device__ __forceinline__ int fdiv(int a, int b) {
 #ifndef LRCNN_SWZ
 #define LRCNN_SWZ 1
 #endif
+// forward convolution operands copied from global memory straight into LDS
+#ifndef LRCNN_LDS_DMA
+#define LRCNN_LDS_DMA 1
+#endif
+// LDS stages of the direct-copy ring (3 or 4)
+#ifndef LRCNN_DMA_ST
+#define LRCNN_DMA_ST 3
+#endif
 template <typename T, int KR = 4>
 struct Cfg {
   static constexpr int E = 16 / (int)sizeof(T);  // elements per 16 bytes
@@ -324,6 +332,47 @@ __device__ __align__(16) uint4 g_zero16[1] = {};
 __device__ __forceinline__ uint4 load16z(const void *base, long long off_bytes, bool ok) {
   const uint4 *q = ok ? (const uint4 *)((const char *)base + off_bytes) : &g_zero16[0];
   return *q;
+}
+// The same 16 bytes (or zeros) copied from global memory straight into LDS
+// (global_load_lds_dwordx4): lane l of the wave writes bytes
+// [16 l, 16 l + 16) after the wave-uniform LDS address `lds` (in M0). The
+// copy is counted by vmcnt like any global load; no registers hold the
+// data. It is issued as inline assembly so that the compiler does not
+// track it: its waitcnt pass cannot tell one LDS stage from another and
+// would wait for every copy before each LDS read. The caller orders the
+// copies with explicit vmcnt waits and barriers; the "memory" clobber keeps
+// the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void load16_lds_p(const void *p, bool ok, void *lds) {
+  const void *q = ok ? p : (const void *)&g_zero16[0];
+  const uint32_t la = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(la), "v"(q)
+               : "memory", "m0");
+}
+// the same with the LDS destination given as a byte address and the zero
+// block's address `zero` passed in (held in registers by the caller)
+__device__ __forceinline__ void load16_lds_a(const void *p, bool ok, uint32_t lds,
+                                             const void *zero) {
+  const void *q = ok ? p : zero;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(q)
+               : "memory", "m0");
+}
+// the same at byte offset off_bytes from base
+__device__ __forceinline__ void load16_lds(const void *base, long long off_bytes, bool ok,
+                                           void *lds) {
+  load16_lds_p((const char *)base + off_bytes, ok, lds);
+}
+// s_waitcnt with only the vector-memory counter limited to N (gfx9
+// encoding: vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt at their
+// maxima, i.e. not waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // Instruction schedule of one steady-state tile step: the MFMAs of the
@@ -536,9 +585,17 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   constexpr int NA = KR / 2;             // A rows loaded per thread
   constexpr int NBL = BN * KR / 256;     // B vectors loaded per thread
   constexpr int RS = 256 / KR;           // row stride between a thread's loads
-  // three LDS stages: while tile t is multiplied, the fragments of t+1 are
-  // read, tile t+2 is written and tile t+3 is fetched from global memory
-  constexpr int ST = 3;
+  // forward with 16-byte rows: both operands copied straight from global
+  // memory into their LDS stage (no registers, no LDS writes by the wave).
+  // The K vector of a thread's tile rows is then chosen so that its
+  // swizzled LDS slot is lane & 3: each wave's rows fill 1 KiB of LDS in
+  // lane order, the layout of a direct copy.
+  constexpr bool LANE_SLOT = KR == 4 && LRCNN_SWZ;
+  constexpr bool DMA = LRCNN_LDS_DMA && LANE_SLOT && !DGRAD && VEC;
+  // LDS stages. Register staging: while tile t is multiplied, the
+  // fragments of t+1 are read, tile t+2 is written and tile t+3 is fetched
+  // from global memory. Direct copies: tiles t+2 .. t+ST-1 are in flight.
+  constexpr int ST = DMA ? LRCNN_DMA_ST : 3;
   // input gradient: weights staged k-major (16-byte stores)
   constexpr int BKM = DGRAD ? 1 : 0;
   constexpr int PB = BN + E;
@@ -555,7 +612,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   __shared__ __align__(16) char smem[RING > CTILE ? RING : CTILE];
   T (*As)[BM * LDK] = reinterpret_cast<T (*)[BM * LDK]>(smem);
   T (*Bs)[BSZ] = reinterpret_cast<T (*)[BSZ]>(smem + sizeof(T) * ST * BM * LDK);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (wave index read from lane 0 so the compiler keeps it, and the LDS
+  // addresses derived from it, in scalar registers)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int R = a.y1 - a.y0;
   const int M = a.B * R * a.Wd;
   // pixel stride of a phase of a strided input gradient (else 1)
@@ -567,7 +627,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   const int CB = (a.KC + BK - 1) / BK;
   const bool tpk = !VEC && !DGRAD && a.tpack;
   const int KT = tpk ? (taps + KR - 1) / KR : taps * CB;
-  const int kv = tid % KR;
+  // K vector of this thread's tile rows: (l & 3) ^ ((l >> 4) & 3) for lane
+  // l puts it in LDS slot l & 3 (the swizzle is an XOR with (row >> 2) & 3)
+  const int kv = LANE_SLOT ? ((tid & 3) ^ ((tid >> 4) & 3)) : tid % KR;
+  const int wrow = wave * (64 / KR);  // first tile row of this wave's pass
   const T *src = (const T *)a.src.p;
   const T *w = (const T *)a.w;
   const long long srow = (long long)a.src.W * a.src.C;
@@ -604,6 +667,27 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
 #pragma unroll
   for (int i = 0; i < NA; ++i)
     rowok[i] = ONE && am[i] & (bx[i] >= 0) & (by[i] >= a.sy0) & (by[i] < a.sy1) & (bx[i] < a.Ws);
+  // Forward direct copies (the launcher sends only kernels of up to 64
+  // taps here): the taps under which an A row reads inside the source
+  // window, as bits tap = ti * kw + tj (rows ti in [sy0 - by, sy1 - by),
+  // columns tj in [-bx, Ws - bx)), and the address of the row's first
+  // element at tap 0; a K step then tests one bit and adds one uniform
+  // offset.
+  constexpr bool TMASK = DMA && !ONE;
+  uint64_t tmask[TMASK ? NA : 1];
+  const char *rp[TMASK ? NA : 1];
+  if (TMASK) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) {
+      const int r0 = max(0, a.sy0 - by[i]), r1 = min(a.kh, a.sy1 - by[i]);
+      const int q0 = max(0, -bx[i]), q1 = min(a.kw, a.Ws - bx[i]);
+      const uint64_t cm = q1 > q0 ? ((1ull << (q1 - q0)) - 1ull) << q0 : 0ull;
+      uint64_t m = 0;
+      for (int r = r0; r < r1; ++r) m |= cm << (r * a.kw);
+      tmask[i] = am[i] ? m : 0ull;
+      rp[i] = (const char *)src + (rbase[i] + kv * E) * (long long)sizeof(T);
+    }
+  }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
   // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output
   // channel of the consumer), contiguous along n, so each 16-byte load
@@ -625,6 +709,15 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   for (int j = 0; j < NBL; ++j)
     bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * wtaps * a.N + bn[j]
                      : (long long)bn[j] * taps * a.KC + kv * E;
+  const char *wp[TMASK ? NBL : 1];
+  if (TMASK) {
+#pragma unroll
+    for (int j = 0; j < NBL; ++j) wp[j] = (const char *)w + bbase[j] * (long long)sizeof(T);
+  }
+  // LDS byte addresses of the stages (uniform)
+  const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  constexpr uint32_t ASB = sizeof(T) * BM * LDK, BSB = sizeof(T) * BSZ;
+  const uint32_t lds_b = lds_a + ST * ASB;
 
   // K iterations of this workgroup (split-K over the tile's z), walked as
   // (tap, channel block) without divisions in the loop
@@ -633,10 +726,29 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
   int kpk = kbeg;  // tap-packed forward: current K iteration
+  // tap-mask loader: byte offsets of the current (tap, channel block) in the
+  // source (ti * row pitch + tj * C + cb) and in a weight row (tap * KC +
+  // cb), advanced by uniform deltas: next channel block, next tap, next
+  // kernel row
+  constexpr long long ES = sizeof(T);
+  long long ub = ((long long)ti * srow + (long long)tj * a.src.C + cbi * BK) * ES;
+  long long wb = ((long long)tap * a.KC + cbi * BK) * ES;
+  const long long d_step = BK * ES, d_tap = (a.src.C - (long long)(CB - 1) * BK) * ES;
+  const long long d_row = (srow - (long long)(a.kw - 1) * a.src.C - (long long)(CB - 1) * BK) * ES;
+  const long long dw_tap = (a.KC - (long long)(CB - 1) * BK) * ES;
+  // the advance as masked adds (a conditional 64-bit choice compiles to
+  // branches): + d_step, + (d_tap - d_step) on a new tap, + (d_row - d_tap)
+  // on a new kernel row
+  const long long dd_tap = d_tap - d_step, dd_row = d_row - d_tap, ddw_tap = dw_tap - d_step;
+  // the zero block's address, made opaque so that it is computed once and
+  // not rebuilt in the loop
+  const void *zblk = &g_zero16[0];
+  asm volatile("" : "+s"(zblk));
 
   uint4 ra[NA], rb[NBL];
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
-  auto gload = [&]() {
+  // (st: the LDS stage a direct copy writes)
+  auto gload = [&](int st) {
     if (tpk) {
       // vector kv of a tile row holds channels [0, KC) of tap kpk*KR + kv
       const int tp = kpk * KR + kv;
@@ -664,13 +776,27 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     const bool cok = c0 < a.KC;
     const int lim = a.KC - c0;
     const long long tofs = (long long)ti * srow + (long long)tj * a.src.C;  // uniform
+    if (TMASK) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        load16_lds_a(rp[i] + ub, ((uint32_t)(tmask[i] >> tap) & 1u) & cok,
+                     lds_a + st * ASB + (wrow + RS * i) * LDK * (uint32_t)sizeof(T), zblk);
+#pragma unroll
+      for (int j = 0; j < NBL; ++j)
+        load16_lds_a(wp[j] + wb, bvld[j] & cok,
+                     lds_b + st * BSB + (wrow + RS * j) * LDK * (uint32_t)sizeof(T), zblk);
+    } else {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
       int sy, sx;
       bool ok;
       long long off;
       if (ONE) {
-        ra[i] = load16z(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok);
+        if (DMA)
+          load16_lds(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok,
+                     &As[st][(wrow + RS * i) * LDK]);
+        else
+          ra[i] = load16z(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok);
         continue;
       }
       if (DGRAD && !S1) {
@@ -686,7 +812,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         off = (DGRAD ? rbase[i] - tofs : rbase[i] + tofs) + c0;
       }
       ok = ok & am[i] & cok & (sy >= a.sy0) & (sy < a.sy1) & (sx < a.Ws);
-      if (VEC) {
+      if (DMA) {
+        load16_lds(src, off * (long long)sizeof(T), ok, &As[st][(wrow + RS * i) * LDK]);
+      } else if (VEC) {
         ra[i] = load16z(src, off * (long long)sizeof(T), ok);
       } else {
         const T *p = src;
@@ -710,21 +838,29 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         off = bbase[j] + (long long)tap * a.KC + cb;
         blim = lim;
       }
-      if (VEC) {
+      if (DMA) {
+        load16_lds(w, off * (long long)sizeof(T), ok, &Bs[st][(wrow + RS * j) * LDK]);
+      } else if (VEC) {
         rb[j] = load16z(w, off * (long long)sizeof(T), ok);
       } else {
         const T *p = ok ? w + off : w;
         rb[j] = load16<T, VEC>(p, ok, blim);
       }
     }
+    }
     // advance to the next (tap, channel block) without branches
     const bool wrap = ++cbi == CB;
     cbi = wrap ? 0 : cbi;
     tap += wrap ? 1 : 0;
     tj += wrap ? 1 : 0;
-    const bool wrow = tj == a.kw;
-    tj = wrow ? 0 : tj;
-    ti += wrow ? 1 : 0;
+    const bool nrow = tj == a.kw;
+    tj = nrow ? 0 : tj;
+    ti += nrow ? 1 : 0;
+    if (TMASK) {
+      const long long mw = -(long long)wrap, mr = -(long long)nrow;
+      ub += d_step + (dd_tap & mw) + (dd_row & mr);
+      wb += d_step + (ddw_tap & mw);
+    }
   };
 
   f32x16 acc[2][NB];
@@ -759,25 +895,77 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     }
   };
   const int n = kend - kbeg;
+  using FR = Frag<T, BN, KR, 0, BKM>;
+  FR f0, f1;
+  int t = 0;
+  if constexpr (DMA) {
+    // Tile t+ST is copied into the stage of tile t once every wave has read
+    // tile t; a step waits only for tile t+1, so a copy has ST-1 steps to
+    // arrive. LD: copies per thread per tile; wait_tiles(k) leaves the
+    // copies of the k most recent tiles in flight.
+    constexpr int LD = NA + NBL;
+    auto wait_tiles = [](int k) {
+      if (ST > 3 && k >= 2) wait_vmcnt<(ST > 3 ? 2 : 0) * LD>();
+      else if (k == 1) wait_vmcnt<LD>();
+      else wait_vmcnt<0>();
+    };
+#pragma unroll
+    for (int i = 0; i < ST; ++i)
+      if (i < n) gload(i);
+    wait_tiles(min(n, ST) - 1);
+    __syncthreads();
+    if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
+    int sc = 0;  // stage of tile t
+    auto dstep = [&](int t, FR &cur, FR &nxt) {
+      const int s1 = sc == ST - 1 ? 0 : sc + 1;
+      if (t + 1 < n) {
+        wait_tiles(min(n - 1, t + ST - 1) - t - 1);
+        __syncthreads();
+        nxt.load(As[s1], Bs[s1], wm, wn, lane);
+        if (t + ST < n) gload(sc);
+      }
+      cur.mma(acc);
+      sc = s1;
+    };
+    auto dstep_full = [&](FR &cur, FR &nxt) {
+      const int s1 = sc == ST - 1 ? 0 : sc + 1;
+      wait_vmcnt<(ST - 2) * LD>();
+      __syncthreads();
+      nxt.load(As[s1], Bs[s1], wm, wn, lane);
+      gload(sc);
+      cur.mma(acc);
+      interleave_step<FR::NMFMA, FR::NDSR, 0, LD>();
+      sc = s1;
+    };
+    for (; t + ST + 1 < n; t += 2) {
+      dstep_full(f0, f1);
+      dstep_full(f1, f0);
+    }
+    for (; t + 1 < n; t += 2) {
+      dstep(t, f0, f1);
+      dstep(t + 1, f1, f0);
+    }
+    if (t < n) dstep(t, f0, f1);
+    // the stages are reused by the epilogue
+    __syncthreads();
+  } else {
   if (n > 0) {
-    gload();
+    gload(0);
     store(0);
   }
   if (n > 1) {
-    gload();
+    gload(0);
     store(1);
   }
-  if (n > 2) gload();
+  if (n > 2) gload(0);
   __syncthreads();
-  using FR = Frag<T, BN, KR, 0, BKM>;
-  FR f0, f1;
   if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
   int s1 = 1, s2 = 2;  // stages of tiles t+1 and t+2
   auto step = [&](int t, FR &cur, FR &nxt) {
     if (t + 1 < n) nxt.load(As[s1], Bs[s1], wm, wn, lane);
     if (t + 2 < n) {
       store(s2);
-      if (t + 3 < n) gload();
+      if (t + 3 < n) gload(0);
     }
     cur.mma(acc);
     s1 = s2;
@@ -790,14 +978,13 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   auto step_full = [&](FR &cur, FR &nxt) {
     nxt.load(As[s1], Bs[s1], wm, wn, lane);
     store(s2);
-    gload();
+    gload(0);
     cur.mma(acc);
     interleave_step<FR::NMFMA, FR::NDSR, NDSW, NA + NBL>();
     s1 = s2;
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
   };
-  int t = 0;
   for (; t + 4 < n; t += 2) {
     step_full(f0, f1);
     step_full(f1, f0);
@@ -807,6 +994,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     step(t + 1, f1, f0);
   }
   if (t < n) step(t, f0, f1);
+  }
 
   if (gridDim.z > 1) {
     // split-K: raw partial sums, reduced in split order by the epilogue kernel
@@ -1062,7 +1250,10 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   ConvArgs a = a0;
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
-  const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0);
+  // (the forward's 16-byte loader tests taps against a 64-bit mask: larger
+  // kernels take the element-wise loader)
+  const bool vec = (a.KC % CF::E) == 0 &&
+                   (DGRAD ? (a.N % CF::E) == 0 : a.kh * a.kw <= 64 && a.kw < 64);
   a.tpack = !vec && conv_tap_packed(a.KC, (int)sizeof(T), DGRAD);
   a.fkw = fast_div((uint32_t)a.kw);
   const int KT = a.tpack ? (a.kh * a.kw + KR - 1) / KR : a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
