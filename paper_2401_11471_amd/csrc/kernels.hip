@@ -675,7 +675,11 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // offset.
   constexpr bool TMASK = DMA && !ONE;
   uint64_t tmask[TMASK ? NA : 1];
-  const char *rp[TMASK ? NA : 1];
+  const char *rp[DMA ? NA : 1];
+  if (DMA) {
+#pragma unroll
+    for (int i = 0; i < NA; ++i) rp[i] = (const char *)src + (rbase[i] + kv * E) * (long long)sizeof(T);
+  }
   if (TMASK) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
@@ -685,7 +689,6 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       uint64_t m = 0;
       for (int r = r0; r < r1; ++r) m |= cm << (r * a.kw);
       tmask[i] = am[i] ? m : 0ull;
-      rp[i] = (const char *)src + (rbase[i] + kv * E) * (long long)sizeof(T);
     }
   }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
@@ -709,8 +712,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   for (int j = 0; j < NBL; ++j)
     bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * wtaps * a.N + bn[j]
                      : (long long)bn[j] * taps * a.KC + kv * E;
-  const char *wp[TMASK ? NBL : 1];
-  if (TMASK) {
+  const char *wp[DMA ? NBL : 1];
+  if (DMA) {
 #pragma unroll
     for (int j = 0; j < NBL; ++j) wp[j] = (const char *)w + bbase[j] * (long long)sizeof(T);
   }
@@ -776,6 +779,20 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     const bool cok = c0 < a.KC;
     const int lim = a.KC - c0;
     const long long tofs = (long long)ti * srow + (long long)tj * a.src.C;  // uniform
+    if (DMA && ONE) {
+      // one tap: the row's validity is fixed, K steps through channel blocks
+      const long long co = (long long)cb * sizeof(T);
+#pragma unroll
+      for (int i = 0; i < NA; ++i)
+        load16_lds_a(rp[i] + co, rowok[i] & cok,
+                     lds_a + st * ASB + (wrow + RS * i) * LDK * (uint32_t)sizeof(T), zblk);
+#pragma unroll
+      for (int j = 0; j < NBL; ++j)
+        load16_lds_a(wp[j] + co, bvld[j] & cok,
+                     lds_b + st * BSB + (wrow + RS * j) * LDK * (uint32_t)sizeof(T), zblk);
+      ++cbi;
+      return;
+    }
     if (TMASK) {
 #pragma unroll
       for (int i = 0; i < NA; ++i)
