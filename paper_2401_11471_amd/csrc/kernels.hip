@@ -361,6 +361,14 @@ __device__ __forceinline__ void load16_lds_a(const void *p, bool ok, uint32_t ld
                : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(q)
                : "memory", "m0");
 }
+// 16 bytes at p if ok, else the zero block at `zero`, read as a global
+// memory load (the selected pointer is generic to the compiler)
+__device__ __forceinline__ uint4 load16_sel(const void *p, bool ok, const void *zero) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const u32x4 g_u32x4;
+  const u32x4 v = *(g_u32x4 *)(ok ? p : zero);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 // the same at byte offset off_bytes from base
 __device__ __forceinline__ void load16_lds(const void *base, long long off_bytes, bool ok,
                                            void *lds) {
@@ -673,18 +681,25 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // columns tj in [-bx, Ws - bx)), and the address of the row's first
   // element at tap 0; a K step then tests one bit and adds one uniform
   // offset.
+  // (input gradient, stride 1 or a stride phase: the same test with the
+  // taps mirrored, sy = by - ti and sx = bx - tj, operands staged through
+  // registers)
   constexpr bool TMASK = DMA && !ONE;
-  uint64_t tmask[TMASK ? NA : 1];
-  const char *rp[DMA ? NA : 1];
-  if (DMA) {
+  constexpr bool RMASK = DGRAD && S1 && VEC && !ONE;
+  constexpr bool MASK = TMASK || RMASK;
+  uint64_t tmask[MASK ? NA : 1];
+  const char *rp[DMA || RMASK ? NA : 1];
+  if (DMA || RMASK) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) rp[i] = (const char *)src + (rbase[i] + kv * E) * (long long)sizeof(T);
   }
-  if (TMASK) {
+  if (MASK) {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {
-      const int r0 = max(0, a.sy0 - by[i]), r1 = min(a.kh, a.sy1 - by[i]);
-      const int q0 = max(0, -bx[i]), q1 = min(a.kw, a.Ws - bx[i]);
+      const int r0 = DGRAD ? max(0, by[i] - a.sy1 + 1) : max(0, a.sy0 - by[i]);
+      const int r1 = DGRAD ? min(a.kh, by[i] - a.sy0 + 1) : min(a.kh, a.sy1 - by[i]);
+      const int q0 = DGRAD ? max(0, bx[i] - a.Ws + 1) : max(0, -bx[i]);
+      const int q1 = DGRAD ? min(a.kw, bx[i] + 1) : min(a.kw, a.Ws - bx[i]);
       const uint64_t cm = q1 > q0 ? ((1ull << (q1 - q0)) - 1ull) << q0 : 0ull;
       uint64_t m = 0;
       for (int r = r0; r < r1; ++r) m |= cm << (r * a.kw);
@@ -712,8 +727,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   for (int j = 0; j < NBL; ++j)
     bbase[j] = DGRAD ? (long long)(bk0 + BKS * j) * wtaps * a.N + bn[j]
                      : (long long)bn[j] * taps * a.KC + kv * E;
-  const char *wp[DMA ? NBL : 1];
-  if (DMA) {
+  const char *wp[DMA || RMASK ? NBL : 1];
+  if (DMA || RMASK) {
 #pragma unroll
     for (int j = 0; j < NBL; ++j) wp[j] = (const char *)w + bbase[j] * (long long)sizeof(T);
   }
@@ -729,20 +744,32 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   int tap = kbeg / CB, cbi = kbeg - (kbeg / CB) * CB;
   int ti = tap / a.kw, tj = tap - (tap / a.kw) * a.kw;
   int kpk = kbeg;  // tap-packed forward: current K iteration
-  // tap-mask loader: byte offsets of the current (tap, channel block) in the
-  // source (ti * row pitch + tj * C + cb) and in a weight row (tap * KC +
-  // cb), advanced by uniform deltas: next channel block, next tap, next
-  // kernel row
+  // tap-mask loaders: byte offsets of the current (tap, channel block) in
+  // the source (+-(ti * row pitch + tj * C) + cb) and in the weights
+  // (forward: tap * KC + cb along a weight row; input gradient: cb *
+  // taps * N + wtap * N down a column, wtap the tap of the full kernel),
+  // advanced by uniform deltas: next channel block, next tap, next kernel
+  // row
   constexpr long long ES = sizeof(T);
-  long long ub = ((long long)ti * srow + (long long)tj * a.src.C + cbi * BK) * ES;
-  long long wb = ((long long)tap * a.KC + cbi * BK) * ES;
-  const long long d_step = BK * ES, d_tap = (a.src.C - (long long)(CB - 1) * BK) * ES;
-  const long long d_row = (srow - (long long)(a.kw - 1) * a.src.C - (long long)(CB - 1) * BK) * ES;
-  const long long dw_tap = (a.KC - (long long)(CB - 1) * BK) * ES;
+  constexpr long long SG = DGRAD ? -1 : 1;
+  long long ub = (SG * ((long long)ti * srow + (long long)tj * a.src.C) + cbi * BK) * ES;
+  const long long d_step = BK * ES, d_tap = (SG * a.src.C - (long long)(CB - 1) * BK) * ES;
+  const long long d_row =
+      (SG * (srow - (long long)(a.kw - 1) * a.src.C) - (long long)(CB - 1) * BK) * ES;
+  const long long wst = DGRAD ? (long long)wtaps * a.N : 1;  // per channel
+  const long long wtp = DGRAD ? a.N : a.KC;                 // per tap
+  const int dwt = ps > 1 ? ps : 1;                          // next tap in a row
+  const int dwr = ps > 1 ? ps * a.kw_full - ps * (a.kw - 1) : 1;  // next kernel row
+  const int wtap0 = ps > 1 ? (a.ty0 + ps * ti) * a.kw_full + a.tx0 + ps * tj : tap;
+  long long wb = ((long long)cbi * BK * wst + (long long)wtap0 * wtp) * ES;
+  const long long dw_step = BK * wst * ES;
+  const long long dw_tap = (-(long long)(CB - 1) * BK * wst + (long long)dwt * wtp) * ES;
+  const long long dw_row = (-(long long)(CB - 1) * BK * wst + (long long)dwr * wtp) * ES;
   // the advance as masked adds (a conditional 64-bit choice compiles to
-  // branches): + d_step, + (d_tap - d_step) on a new tap, + (d_row - d_tap)
-  // on a new kernel row
-  const long long dd_tap = d_tap - d_step, dd_row = d_row - d_tap, ddw_tap = dw_tap - d_step;
+  // branches): + step, + (tap - step) on a new tap, + (row - tap) on a new
+  // kernel row
+  const long long dd_tap = d_tap - d_step, dd_row = d_row - d_tap;
+  const long long ddw_tap = dw_tap - dw_step, ddw_row = dw_row - dw_tap;
   // the zero block's address, made opaque so that it is computed once and
   // not rebuilt in the loop
   const void *zblk = &g_zero16[0];
@@ -793,7 +820,18 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       ++cbi;
       return;
     }
-    if (TMASK) {
+    if (RMASK) {
+#pragma unroll
+      for (int i = 0; i < NA; ++i) {
+        const bool ok = ((uint32_t)(tmask[i] >> tap) & 1u) & cok;
+        ra[i] = load16_sel(rp[i] + ub, ok, zblk);
+      }
+#pragma unroll
+      for (int j = 0; j < NBL; ++j) {
+        const bool ok = bvld[j] & (cb + bk0 + BKS * j < a.KC);
+        rb[j] = load16_sel(wp[j] + wb, ok, zblk);
+      }
+    } else if (TMASK) {
 #pragma unroll
       for (int i = 0; i < NA; ++i)
         load16_lds_a(rp[i] + ub, ((uint32_t)(tmask[i] >> tap) & 1u) & cok,
@@ -873,10 +911,10 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     const bool nrow = tj == a.kw;
     tj = nrow ? 0 : tj;
     ti += nrow ? 1 : 0;
-    if (TMASK) {
+    if (MASK) {
       const long long mw = -(long long)wrap, mr = -(long long)nrow;
       ub += d_step + (dd_tap & mw) + (dd_row & mr);
-      wb += d_step + (ddw_tap & mw);
+      wb += dw_step + (ddw_tap & mw) + (ddw_row & mr);
     }
   };
 
@@ -1267,10 +1305,10 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   ConvArgs a = a0;
   const int M = a.B * (a.y1 - a.y0) * a.Wd;
   if (M <= 0 || a.N <= 0) return 0;
-  // (the forward's 16-byte loader tests taps against a 64-bit mask: larger
-  // kernels take the element-wise loader)
-  const bool vec = (a.KC % CF::E) == 0 &&
-                   (DGRAD ? (a.N % CF::E) == 0 : a.kh * a.kw <= 64 && a.kw < 64);
+  // (the 16-byte loaders test taps against a 64-bit mask: larger kernels
+  // take the element-wise loader)
+  const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0) &&
+                   a.kh * a.kw <= 64 && a.kw < 64;
   a.tpack = !vec && conv_tap_packed(a.KC, (int)sizeof(T), DGRAD);
   a.fkw = fast_div((uint32_t)a.kw);
   const int KT = a.tpack ? (a.kh * a.kw + KR - 1) / KR : a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
