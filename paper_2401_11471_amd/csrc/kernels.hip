@@ -695,16 +695,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   }
   if (MASK) {
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-      const int r0 = DGRAD ? max(0, by[i] - a.sy1 + 1) : max(0, a.sy0 - by[i]);
-      const int r1 = DGRAD ? min(a.kh, by[i] - a.sy0 + 1) : min(a.kh, a.sy1 - by[i]);
-      const int q0 = DGRAD ? max(0, bx[i] - a.Ws + 1) : max(0, -bx[i]);
-      const int q1 = DGRAD ? min(a.kw, bx[i] + 1) : min(a.kw, a.Ws - bx[i]);
-      const uint64_t cm = q1 > q0 ? ((1ull << (q1 - q0)) - 1ull) << q0 : 0ull;
-      uint64_t m = 0;
-      for (int r = r0; r < r1; ++r) m |= cm << (r * a.kw);
-      tmask[i] = am[i] ? m : 0ull;
-    }
+    for (int i = 0; i < NA; ++i)
+      tmask[i] = am[i] ? tap_window_mask(by[i], bx[i], a.kh, a.kw, a.sy0, a.sy1, a.Ws, DGRAD)
+                       : 0ull;
   }
   // B operand. Forward: B[k][n] = W[n][tap][k], contiguous along k, stored
   // as 16-byte rows. Input gradient: B[k][n] = W[k][tap][n] (k = output

@@ -39,6 +39,23 @@ LRCNN_HD inline void fdiv_qr(uint32_t n, const FastDiv &f, uint32_t &q, uint32_t
   r = n - q * f.d;
 }
 
+// Taps of a kh x kw kernel (at most 64 taps, kw < 64) under which an
+// implicit-GEMM row whose tap-0 source position is (by, bx) reads inside
+// the source window (rows [sy0, sy1), columns [0, Ws)), as bits
+// tap = ti * kw + tj. Forward: source (by + ti, bx + tj). Mirrored (input
+// gradient): source (by - ti, bx - tj).
+LRCNN_HD inline uint64_t tap_window_mask(int by, int bx, int kh, int kw, int sy0, int sy1,
+                                         int Ws, bool mirrored) {
+  const int r0 = mirrored ? (by - sy1 + 1 > 0 ? by - sy1 + 1 : 0) : (sy0 - by > 0 ? sy0 - by : 0);
+  const int r1 = mirrored ? (by - sy0 + 1 < kh ? by - sy0 + 1 : kh) : (sy1 - by < kh ? sy1 - by : kh);
+  const int q0 = mirrored ? (bx - Ws + 1 > 0 ? bx - Ws + 1 : 0) : (-bx > 0 ? -bx : 0);
+  const int q1 = mirrored ? (bx + 1 < kw ? bx + 1 : kw) : (Ws - bx < kw ? Ws - bx : kw);
+  const uint64_t cm = q1 > q0 ? ((1ull << (q1 - q0)) - 1ull) << q0 : 0ull;
+  uint64_t m = 0;
+  for (int r = r0; r < r1; ++r) m |= cm << (r * kw);
+  return m;
+}
+
 // A band window of an NHWC feature map: element (b, y, x, c) of the global
 // map lives at p + b*bs + (y - row0)*W*C + x*C + c, for the rows the buffer
 // holds. Strides are in elements of the buffer's type.
