@@ -333,26 +333,16 @@ __device__ __forceinline__ uint4 load16z(const void *base, long long off_bytes, 
   const uint4 *q = ok ? (const uint4 *)((const char *)base + off_bytes) : &g_zero16[0];
   return *q;
 }
-// The same 16 bytes (or zeros) copied from global memory straight into LDS
+// 16 bytes at p (or, if !ok, the zero block at `zero`, whose address the
+// caller holds in registers) copied from global memory straight into LDS
 // (global_load_lds_dwordx4): lane l of the wave writes bytes
-// [16 l, 16 l + 16) after the wave-uniform LDS address `lds` (in M0). The
-// copy is counted by vmcnt like any global load; no registers hold the
+// [16 l, 16 l + 16) after the wave-uniform LDS byte address `lds` (in M0).
+// The copy is counted by vmcnt like any global load; no registers hold the
 // data. It is issued as inline assembly so that the compiler does not
 // track it: its waitcnt pass cannot tell one LDS stage from another and
 // would wait for every copy before each LDS read. The caller orders the
 // copies with explicit vmcnt waits and barriers; the "memory" clobber keeps
 // the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void load16_lds_p(const void *p, bool ok, void *lds) {
-  const void *q = ok ? p : (const void *)&g_zero16[0];
-  const uint32_t la = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void *)lds);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(la), "v"(q)
-               : "memory", "m0");
-}
-// the same with the LDS destination given as a byte address and the zero
-// block's address `zero` passed in (held in registers by the caller)
 __device__ __forceinline__ void load16_lds_a(const void *p, bool ok, uint32_t lds,
                                              const void *zero) {
   const void *q = ok ? p : zero;
@@ -368,11 +358,6 @@ __device__ __forceinline__ uint4 load16_sel(const void *p, bool ok, const void *
   typedef __attribute__((address_space(1))) const u32x4 g_u32x4;
   const u32x4 v = *(g_u32x4 *)(ok ? p : zero);
   return make_uint4(v.x, v.y, v.z, v.w);
-}
-// the same at byte offset off_bytes from base
-__device__ __forceinline__ void load16_lds(const void *base, long long off_bytes, bool ok,
-                                           void *lds) {
-  load16_lds_p((const char *)base + off_bytes, ok, lds);
 }
 // s_waitcnt with only the vector-memory counter limited to N (gfx9
 // encoding: vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt at their
@@ -840,11 +825,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       bool ok;
       long long off;
       if (ONE) {
-        if (DMA)
-          load16_lds(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok,
-                     &As[st][(wrow + RS * i) * LDK]);
-        else
-          ra[i] = load16z(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok);
+        ra[i] = load16z(src, (rbase[i] + c0) * (long long)sizeof(T), rowok[i] & cok);
         continue;
       }
       if (DGRAD && !S1) {
@@ -860,9 +841,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         off = (DGRAD ? rbase[i] - tofs : rbase[i] + tofs) + c0;
       }
       ok = ok & am[i] & cok & (sy >= a.sy0) & (sy < a.sy1) & (sx < a.Ws);
-      if (DMA) {
-        load16_lds(src, off * (long long)sizeof(T), ok, &As[st][(wrow + RS * i) * LDK]);
-      } else if (VEC) {
+      if (VEC) {
         ra[i] = load16z(src, off * (long long)sizeof(T), ok);
       } else {
         const T *p = src;
@@ -886,9 +865,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         off = bbase[j] + (long long)tap * a.KC + cb;
         blim = lim;
       }
-      if (DMA) {
-        load16_lds(w, off * (long long)sizeof(T), ok, &Bs[st][(wrow + RS * j) * LDK]);
-      } else if (VEC) {
+      if (VEC) {
         rb[j] = load16z(w, off * (long long)sizeof(T), ok);
       } else {
         const T *p = ok ? w + off : w;
