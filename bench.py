@@ -7,13 +7,16 @@ recompute, input gradients, weight gradients). Inputs are synthetic N(0, 1)
 tensors with the paper's shapes (ImageNet is not available), resident in HBM
 before timing starts. Prints one JSON line.
 
-Default workload: VGG-16 conv trunk, float32, batch 8, 3x224x224, 4 row bands
-of 56 rows, two-phase sharing. The timed step is captured once in a HIP graph
-and replayed (--eager launches every kernel from the host instead). Also reported: peak activation bytes of the
-row-centric step against the layer-wise baseline (same kernels, every
-feature map kept), the layer-wise step's speed, the overlapping-recompute
-mode's speed (halo overhead), a roofline line for the dominant kernel, and
-the CPU oracle's speed on a bounded sample.
+Default workload: the largest single-GPU one, ResNet-50 conv trunk,
+bfloat16 storage with float32 accumulation, batch 8, 3x2400x3600, 32 row
+bands of 75 rows, two-phase sharing. The timed step is captured once in a
+HIP graph and replayed (--eager launches every kernel from the host
+instead). Also reported: peak activation bytes of the row-centric step
+against the layer-wise baseline (same kernels, every feature map kept), the
+layer-wise step's speed, the overlapping-recompute mode's speed (halo
+overhead), the finer-backward and hybrid-depth variants, a roofline line for
+the dominant kernel, the CPU oracle's speed on a bounded sample, and compact
+lines (speed, roofline, memory ratio) for the 224x224 workloads.
 """
 from __future__ import annotations
 
@@ -35,8 +38,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload id 1..5")
-    ap.add_argument("--mode", default="carry", choices=["carry", "balanced", "recompute"])
+    ap.add_argument("--config", type=int, default=5, help="workload id 1..5")
+    ap.add_argument("--extra-configs", default="2,3",
+                    help="comma-separated workload ids measured in compact form after "
+                         "the main line (empty: none)")
+    ap.add_argument("--mode", default="carry",
+                    choices=["carry", "balanced", "paper2ps", "recompute"])
     ap.add_argument("--bands", type=int, default=0, help="override the band count")
     ap.add_argument("--bp-refine", type=int, default=1,
                     help="backward bands per forward band (finer BP partition)")
@@ -72,39 +79,68 @@ def parse():
     return ap.parse_args()
 
 
+KERNEL_SOURCES = ("kernels.hpp", "kdev.hpp", "kconv.hpp", "kernels.hip", "conv_f32_fwd.hip",
+                  "conv_f32_dgrad.hip", "conv_bf16_fwd.hip", "conv_bf16_dgrad.hip",
+                  "wgrad.hip")
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.hpp"):
+    for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2401_11471_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def policy_of(L, mode):
+    return {"balanced": L.BALANCED, "paper2ps": L.PAPER_2PS}.get(mode, L.EVEN)
+
+
 def cpu_baseline(cfg_id, n_img, seconds):
-    """Column oracle (float64, numpy/BLAS) FP+BP on up to n_img images of the
+    """Column oracle (float64, numpy/BLAS) FP+BP on a bounded sample of the
     workload, one image at a time, stopping once `seconds` have passed (at
-    least one image); weight gradients are summed."""
+    least one piece); weight gradients are summed. Images of more than 448
+    rows are taken in strips of 1/8 of their rows (a strip is an image of
+    its own, zero-padded at its edges, and costs 1/8 of an image's work), so
+    that the sample stays within the time; images/s counts the rows done."""
     import numpy as np
     import threadpoolctl
     from oracle import column as OC
     from workloads import config_inputs, BF16
     nodes, inp = config_inputs(cfg_id, batch=n_img)
     bf = inp.dtype == BF16
+    H = inp.x.shape[1]
+    strip = H if H <= 448 else H // 8
     info = threadpoolctl.threadpool_info()
     cores = max([i.get("num_threads", 1) for i in info] or [1])
     t0 = time.perf_counter()
-    done = 0
-    while done < n_img and (done == 0 or time.perf_counter() - t0 < seconds):
-        x = inp.x[done:done + 1]
+    rows = 0
+    pieces = 0
+    while rows < n_img * H and (pieces == 0 or time.perf_counter() - t0 < seconds):
+        img, r0 = divmod(rows, H)
+        x = inp.x[img:img + 1, r0:r0 + strip]
         acts, am = OC.forward(nodes, x, inp.weights, inp.scales, inp.shifts, bf16=bf)
         g = np.zeros(acts[-1].shape) + 1.0
         OC.backward(nodes, acts, am, inp.weights, inp.scales, g, bf16=bf, want_dx=False)
-        done += 1
-    n_img = done
+        rows += x.shape[1]
+        pieces += 1
     dt = time.perf_counter() - t0
-    return {"value": round(n_img / dt, 4), "unit": "images/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": f"{n_img} image(s) of the same workload, float64 column FP+BP "
+    images = rows / H
+    what = (f"{pieces} image(s)" if strip == H else
+            f"{pieces} strip(s) of {strip} of the {H} rows ({images:.3f} images)")
+    return {"value": round(images / dt, 5), "unit": "images/s", "cores": int(cores),
+            "cpu": cpu_model(), "kind": "oracle",
+            "sample": f"{what} of the same workload, float64 column FP+BP "
                       f"(numpy/BLAS), {dt:.1f} s"}
 
 
@@ -155,6 +191,104 @@ def timed_steps(torch, step, steps, warmup, eager, profile=None):
     return e0.elapsed_time(e1) / steps, 1, graph
 
 
+def compact_workload(args, cid):
+    """Compact measurement of another workload: the default row-centric step
+    (graph replay; dominant-kernel roofline from an eager pass with the
+    library's per-launch events), the layer-wise step, and the variants that
+    trade speed for memory (peak-minimising band placement, the hybrid depth
+    at the planner's checkpoint, finer backward bands), each with its peak
+    activation bytes against the layer-wise step's."""
+    import torch
+    from paper_2401_11471_amd import lrcnn as L
+    from paper_2401_11471_amd.device import DeviceModel
+    from workloads import CONFIGS, config_inputs, BF16
+
+    c = dict(CONFIGS[cid])
+    nodes, inp = config_inputs(cid)
+    B, H, W, Cin = inp.x.shape
+    dts = "bf16" if inp.dtype == BF16 else "f32"
+    dm = DeviceModel.from_inputs(nodes, inp)
+    base = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, c["bands"])
+    out_shape = (B,) + base.node_shape(len(nodes) - 1)
+    dy = dm.to_device(inp.grad(out_shape))
+
+    def run(plan, layerwise=False, profile=False):
+        info = plan.info()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        b0 = torch.cuda.memory_allocated()
+        ws = dm.workspace(info["layerwise_workspace_bytes" if layerwise else
+                               "workspace_bytes"])
+        y = dm.empty(out_shape)
+
+        def step():
+            if layerwise:
+                L.lrcnn_layerwise_reference_gpu(plan, dm.x, dm.w, dm.sc, dm.sf, dy, y, dm.dw,
+                                                None, ws)
+            else:
+                L.lrcnn_forward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, y, ws)
+                L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, ws)
+        step()
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - b0
+        ms, _, g = timed_steps(torch, step, args.steps, args.warmup, False)
+        del g
+        prof = None
+        if profile:
+            _, ps, _ = timed_steps(torch, step, args.steps, 0, True, L.lrcnn_debug_profile)
+            prof = (L.lrcnn_debug_profile_collect(), ps)
+        del ws, y
+        return ms, int(peak), prof
+
+    ms, peak, (kern, ps) = run(base, profile=True)
+    dom_name, (dom_n, dom_ms, dom_fl) = max(kern.items(), key=lambda kv: kv[1][2])
+    bound, pk, unit = PEAK[dts]
+    achieved = dom_fl / (dom_ms * 1e-3) / 1e12
+    lw_ms, lw_peak, _ = run(base, layerwise=True)
+    res = {"value": round(B * 1000.0 / ms, 3), "unit": "images/s", "ms_per_step": round(ms, 3),
+           "dtype": dts,
+           "config": {"workload": c["name"], "net": c["net"], "batch": B,
+                      "input": [Cin, H, W], "bands": c["bands"], "mode": "carry",
+                      "policy": "even", "bp_bands": base.info()["bp_bands"]},
+           "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": pk,
+                        "unit": unit, "frac": round(achieved / pk, 4), "kernel": dom_name,
+                        "launches_per_step": dom_n // ps,
+                        "avg_launch_ms": round(dom_ms / dom_n, 4)},
+           "peak_act_bytes": peak,
+           "layerwise": {"images_per_s": round(B * 1000.0 / lw_ms, 3),
+                         "ms_per_step": round(lw_ms, 3), "peak_act_bytes": lw_peak},
+           "mem_ratio_layerwise_over_rows": round(lw_peak / peak, 3)}
+    variants = {}
+    for label, kw in (("balanced", dict(policy=L.BALANCED)),
+                      ("hybrid", dict(hybrid_from=L.HYBRID_AUTO)),
+                      ("balanced_hybrid", dict(policy=L.BALANCED, hybrid_from=L.HYBRID_AUTO)),
+                      ("finer_bp", dict(bp_refine=2)),
+                      ("finer_bp_hybrid", dict(bp_refine=2, hybrid_from=L.HYBRID_AUTO))):
+        plan = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, c["bands"], **kw)
+        info = plan.info()
+        v_ms, v_peak, _ = run(plan)
+        variants[label] = {"images_per_s": round(B * 1000.0 / v_ms, 3),
+                           "ms_per_step": round(v_ms, 3), "peak_act_bytes": v_peak,
+                           "mem_ratio_layerwise_over_rows": round(lw_peak / v_peak, 3),
+                           "bp_bands": info["bp_bands"], "hybrid_from": info["hybrid_from"],
+                           "flops_over_layerwise": round(info["flops_rows"] /
+                                                         info["flops_layerwise"], 3)}
+        print(f"workload {cid} {label}: {variants[label]['images_per_s']} img/s, ratio "
+              f"{variants[label]['mem_ratio_layerwise_over_rows']}", file=sys.stderr,
+              flush=True)
+    res["variants"] = variants
+    ok = {k: v for k, v in variants.items() if v["mem_ratio_layerwise_over_rows"] >= 3.0}
+    if res["mem_ratio_layerwise_over_rows"] >= 3.0:
+        ok["default"] = {"images_per_s": res["value"]}
+    res["fastest_with_3x_memory_cut"] = (max(ok, key=lambda k: ok[k]["images_per_s"])
+                                         if ok else None)
+    del dm, dy
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
 def max_batch_study(args):
     """Largest batch of the layer-wise baseline and of the row-centric step
     that fit in the device's free memory: found by the planner's search
@@ -169,7 +303,7 @@ def max_batch_study(args):
     c = dict(CONFIGS[args.config])
     nb = args.bands or c["bands"]
     mode = L.RECOMPUTE if args.mode == "recompute" else L.CARRY
-    policy = L.BALANCED if args.mode == "balanced" else L.EVEN
+    policy = policy_of(L, args.mode)
     nodes, inp = config_inputs(args.config, batch=1)
     _, H, W, Cin = inp.x.shape
     tdt = torch.bfloat16 if inp.dtype == BF16 else torch.float32
@@ -394,7 +528,7 @@ def main():
         c["batch"] = args.batch
     nb = args.bands or c["bands"]
     mode = L.RECOMPUTE if args.mode == "recompute" else L.CARRY
-    policy = L.BALANCED if args.mode == "balanced" else L.EVEN
+    policy = policy_of(L, args.mode)
     nodes, inp = config_inputs(args.config, batch=c["batch"])
     B, H, W, Cin = inp.x.shape
     dts = "bf16" if inp.dtype == BF16 else "f32"
@@ -441,6 +575,9 @@ def main():
                                     args.eager, L.lrcnn_debug_profile if args.eager else None)
     del graph
     value = B * 1000.0 / ms
+    # the comparison runs of a long step time fewer steps (a few seconds each)
+    xsteps = max(3, min(args.steps, int(4000.0 / max(ms, 1e-3))))
+    xwarm = min(args.warmup, 2)
     if not args.eager:
         # HIP cannot time events recorded inside a graph, so the per-kernel
         # durations come from an eager pass of the same steps with the
@@ -525,7 +662,7 @@ def main():
                                             dm.dw, None, b["ws"])
         try:
             peak_lw, lb = measure(lw_alloc, lw_step)
-            lw_ms, _, g_ = timed_steps(torch, lambda: lw_step(lb), args.steps, args.warmup,
+            lw_ms, _, g_ = timed_steps(torch, lambda: lw_step(lb), xsteps, xwarm,
                                        args.eager)
             del g_
             out["layerwise"] = {"images_per_s": round(B * 1000.0 / lw_ms, 3),
@@ -549,7 +686,7 @@ def main():
                 L.lrcnn_forward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, b["y"], b["ws"])
                 L.lrcnn_backward_rows(fplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, b["ws"])
             peak_f, fb = measure(f_alloc, f_step)
-            f_ms, _, g_ = timed_steps(torch, lambda: f_step(fb), args.steps, args.warmup,
+            f_ms, _, g_ = timed_steps(torch, lambda: f_step(fb), xsteps, xwarm,
                                       args.eager)
             del g_
             ent = {"bp_bands": finfo["bp_bands"], "images_per_s": round(B * 1000.0 / f_ms, 3),
@@ -574,7 +711,7 @@ def main():
                     L.lrcnn_backward_rows(hplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None,
                                           b["ws"])
                 peak_h, hb = measure(h_alloc, h_step)
-                h_ms, _, g_ = timed_steps(torch, lambda: h_step(hb), args.steps, args.warmup,
+                h_ms, _, g_ = timed_steps(torch, lambda: h_step(hb), xsteps, xwarm,
                                           args.eager)
                 del g_
                 ent = {"hybrid_from": hinfo["hybrid_from"],
@@ -598,7 +735,7 @@ def main():
             def rstep():
                 L.lrcnn_forward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, ry, rws)
                 L.lrcnn_backward_rows(rplan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, rws)
-            r_ms, _, g_ = timed_steps(torch, rstep, args.steps, args.warmup, args.eager)
+            r_ms, _, g_ = timed_steps(torch, rstep, xsteps, xwarm, args.eager)
             del g_
             out["recompute"] = {"images_per_s": round(B * 1000.0 / r_ms, 3),
                                 "ms_per_step": round(r_ms, 3),
@@ -611,6 +748,17 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.config, min(args.cpu_images, B),
                                            args.cpu_seconds)
+    extra = [int(v) for v in args.extra_configs.split(",") if v.strip()]
+    if extra and not args.no_extras:
+        del dm, dy
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        out["other_workloads"] = {}
+        for cid in extra:
+            if cid == args.config:
+                continue
+            r = compact_workload(args, cid)
+            out["other_workloads"][r["config"]["workload"]] = r
     print(json.dumps(out), flush=True)
 
 

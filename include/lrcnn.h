@@ -88,12 +88,25 @@ enum { LRCNN_CARRY = 0, LRCNN_RECOMPUTE = 1 };
 /* Band placement. CARRY bands are ranges of input rows (Algorithm 1 splits
  * the input); RECOMPUTE bands are ranges of the last node's rows (the paper
  * divides the last layer evenly, Section IV-B).
- *   EVEN      r * H / N boundaries
- *   BALANCED  CARRY only: boundaries that minimise the largest per-band
- *             cache of feature maps (the skew of Section IV-A)
- *   EXPLICIT  the caller's `bounds` (n_bands + 1 non-decreasing values from
- *             0 to the partitioned height; empty bands are allowed)       */
-enum { LRCNN_EVEN = 0, LRCNN_BALANCED = 1, LRCNN_EXPLICIT = 2 };
+ *   EVEN       r * H / N boundaries
+ *   BALANCED   CARRY only: boundaries that minimise the peak workspace of
+ *              the step (the skew of Section IV-A)
+ *   EXPLICIT   the caller's `bounds` (n_bands + 1 non-decreasing values from
+ *              0 to the partitioned height; empty bands are allowed)
+ *   PAPER_2PS  CARRY only: the greedy partition of two-phase sharing
+ *              (Section IV-A, Eqs. (11), (13), (14)). Band r must complete
+ *              t_r rows of the last node: t_1 = first_rows (H_1^L; 0 reads
+ *              as ceil(H_L / N_BP)), the remaining H_L - t_1 rows are split
+ *              evenly over bands 2..N_BP. A band's end is the smallest input
+ *              row count from which the frontier of the last node reaches
+ *              t_r -- for a chain of layers exactly the input height that
+ *              Eq. (11) (first band) and Eq. (13) (middle bands) give by
+ *              inverting the layers from the last one; the last band takes
+ *              the remaining input rows (Eq. (14)). The partition is made
+ *              for the backward bands (N_BP = n_bands * bp_refine, as the
+ *              paper sizes it for BP); the forward bands are every
+ *              bp_refine-th of them. */
+enum { LRCNN_EVEN = 0, LRCNN_BALANCED = 1, LRCNN_EXPLICIT = 2, LRCNN_PAPER_2PS = 3 };
 enum { LRCNN_HYBRID_AUTO = -1 };
 
 typedef struct {
@@ -101,7 +114,7 @@ typedef struct {
   int32_t dtype;             /* LRCNN_F32 | LRCNN_BF16                        */
   int32_t mode;              /* LRCNN_CARRY | LRCNN_RECOMPUTE                 */
   int32_t n_bands;           /* N >= 1: bands of the forward pass             */
-  int32_t policy;            /* LRCNN_EVEN | LRCNN_BALANCED | LRCNN_EXPLICIT  */
+  int32_t policy;            /* LRCNN_EVEN | BALANCED | EXPLICIT | PAPER_2PS  */
   const int32_t *bounds;     /* host array, used when policy == EXPLICIT      */
   int32_t bp_refine;         /* >= 1 (0 reads as 1): the backward pass splits */
                              /* every forward band evenly into bp_refine      */
@@ -117,6 +130,9 @@ typedef struct {
                              /* LRCNN_HYBRID_AUTO (-1): the planner takes the  */
                              /* valid k with the smallest workspace (0 if no   */
                              /* checkpoint beats the all-row-centric plan).    */
+  int32_t first_rows;        /* PAPER_2PS: H_1^L, rows of the last node that  */
+                             /* the first band completes (0: ceil(H_L/N_BP)); */
+                             /* ignored by the other policies                 */
 } lrcnn_config;
 
 /* Opaque plan handle (host memory only). */
@@ -206,9 +222,12 @@ typedef struct {
  * kernels the most parallel work (the paper's second principle). The exact
  * workspace of each candidate plan stands in for the paper's analytic
  * Omega, so the strips, error windows and split-K buffers are counted too.
- * cfg->n_bands and cfg->bp_refine are ignored; cfg->policy must be EVEN or
- * BALANCED. Candidates are tried in increasing (N_BP, N_FP) order, each a
- * full host-side plan (milliseconds).
+ * cfg->n_bands and cfg->bp_refine are ignored; cfg->policy must be EVEN,
+ * BALANCED or PAPER_2PS. Candidates are tried in increasing (N_BP, N_FP)
+ * order, each a full host-side plan (milliseconds). With PAPER_2PS each
+ * (N_BP, N_FP) also tries H_1^L from H_L down to ceil(H_L / N_BP) and takes
+ * the largest that fits (Eq. (12): the largest first band, the fewest
+ * bands); cfg->first_rows is ignored.
  * Errors: EINVAL (null, EXPLICIT policy, bad budget), the errors of
  * lrcnn_plan, EINFEASIBLE (no candidate up to max_bands fits). */
 int lrcnn_plan_for_budget(const lrcnn_node *nodes, int32_t n_nodes,

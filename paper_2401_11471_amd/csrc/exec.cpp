@@ -86,6 +86,7 @@ struct Run {
   Plan &P;
   const Layout &L;
   Sched sched;
+  const Fuse &F;  // the schedule's fusions
   char *ws;
   const void *x;
   const void *const *w;
@@ -118,7 +119,7 @@ struct Run {
   Run(Plan &p, const Layout &l, Sched s, void *wsp, const void *x_,
       const void *const *w_, const float *const *sc_, const float *const *sf_,
       void *st)
-      : P(p), L(l), sched(s), ws((char *)wsp), x(x_), w(w_), sc(sc_), sf(sf_),
+      : P(p), L(l), sched(s), F(s == S_LAYERWISE ? p.fz_lw : p.fz), ws((char *)wsp), x(x_), w(w_), sc(sc_), sf(sf_),
         stream(st), dt(p.cfg.dtype == LRCNN_BF16 ? DT_BF16 : DT_F32) {
     act.resize(P.n);
     dlt.resize(P.n);
@@ -146,7 +147,7 @@ struct Run {
   int pipe_wait(int v) {
     if (!pipe || !ev_prev) return LRCNN_OK;
     int w = last_reader(v);
-    if (!P.fuse_fwd.empty() && P.fuse_fwd[v]) w = std::max(w, last_reader(P.fuse_fwd[v]));
+    if (F.fwd[v]) w = std::max(w, last_reader(F.fwd[v]));
     LAUNCH(hipStreamWaitEvent((hipStream_t)stream, ev_prev[w], 0), "band wait");
     return LRCNN_OK;
   }
@@ -220,11 +221,19 @@ struct Run {
       c.kh = d.kh, c.kw = d.kw, c.sh = d.sh, c.sw = d.sw, c.ph = d.ph, c.pw = d.pw;
       c.part = (float *)(ws + part_off);
       c.part_bytes = L.part_bytes;
+      c.splits = P.fsplit[v];
       if (res) {
         c.res = *res;
         c.res_relu = res_relu;
       }
-      LAUNCH(launch_conv(dt, 0, c, stream), "conv forward");
+      // (a layer-wise launch whose partial sums exceed the buffer runs in row
+      // chunks; each output element's sum is the same)
+      const int chunk = L.fchunk.empty() || L.fchunk[v] <= 0 ? b - a : L.fchunk[v];
+      for (int y = a; y < b; y += chunk) {
+        c.y0 = y;
+        c.y1 = std::min(b, y + chunk);
+        LAUNCH(launch_conv(dt, 0, c, stream), "conv forward");
+      }
     } else if (d.op == LRCNN_OP_MAXPOOL) {
       PoolArgs p{};
       p.src = act[d.in0];
@@ -336,8 +345,8 @@ struct Run {
                         ? (uint8_t *)(ws + L.argmax[v]) : nullptr;
       // (not with lifetime-packed forward windows: the add's window may
       // still belong to another node while the conv runs)
-      const bool can_fuse = !packed && !P.fuse_fwd.empty();
-      const int fa = can_fuse ? P.fuse_fwd[v] : 0;
+      const bool can_fuse = !packed;
+      const int fa = can_fuse ? F.fwd[v] : 0;
       const lrcnn_node &nd = P.nodes[v];
       if (fa) {
         // this conv's epilogue computes the residual add fa (its only
@@ -347,7 +356,7 @@ struct Run {
         uint8_t *amk = mask_out ? (uint8_t *)mask_out[fa] : nullptr;
         if ((st = node_fwd(v, q.a, q.b, act[fa], am, amk, &other, an.relu)) != LRCNN_OK)
           return st;
-      } else if (can_fuse && nd.op == LRCNN_OP_ADD && P.fuse_fwd[std::max(nd.in0, nd.in1)] == v) {
+      } else if (can_fuse && nd.op == LRCNN_OP_ADD && F.fwd[std::max(nd.in0, nd.in1)] == v) {
         // computed with its later input
       } else {
         uint8_t *mk = mask_out ? (uint8_t *)mask_out[v] : nullptr;
@@ -411,7 +420,7 @@ struct Run {
   // the rows carried in from that buffer. stage_a = 0 when nothing is staged.
   int fuse_err(int r, int v, int u, int y0, int y1, ErrOut &eo, View &stage, int &stage_a) {
     stage_a = 0;
-    if (P.fuse_act.empty() || P.fuse_act[u] != v) return LRCNN_OK;
+    if (F.act[u] != v) return LRCNN_OK;
     const Rows qu = band_rows(r, u);
     const lrcnn_node &du = P.nodes[u];
     const Shape &sh = P.shp[u];
@@ -677,7 +686,7 @@ struct Run {
 
   // a conv whose error operand the add's backward writes (no error window)
   bool fused(int u) const {
-    return u > 0 && u < (int)P.fuse_add.size() && P.fuse_add[u] != 0;
+    return u > 0 && u < (int)F.add.size() && F.add[u] != 0;
   }
 
   // BP of band r after its feature maps are in place.
@@ -718,7 +727,7 @@ struct Run {
             dinit_carry[u] = delta_view(r, u, dinit_cv[u], dinit_t[u]) ? 1 : 0;
             continue;
           }
-          if (!P.fuse_act.empty() && P.fuse_act[u] == v) {
+          if (F.act[u] == v) {
             // v's input gradient forms u's error operand; a band without
             // rows of v holds nothing of u (the planner checked), and u's
             // error window has no memory of its own

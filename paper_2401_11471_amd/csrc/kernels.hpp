@@ -95,6 +95,8 @@ struct ConvArgs {
   int kh, kw, sh, sw, ph, pw;
   float *part;        // split-K partial sums (nullable: no split)
   size_t part_bytes;  // capacity of `part`
+  int splits;         // > 0: this split count (the layer's fixed one); 0: the
+                      // launcher's estimate picks it
   int kts;            // K iterations per split (set by the launcher)
   // forward only: residual add fused into the epilogue (res.p nullable):
   // the conv value (rounded to the storage dtype) plus the other input of
@@ -168,27 +170,49 @@ struct SplitChoice {
   int s;
   double us;  // estimated duration
 };
+// Estimated duration of a launch of `tiles` tiles split s ways.
+inline double split_cost(long long tiles, int KT, long long part_elems, const SplitCost &c,
+                         long long s) {
+  const long long wg = tiles * s;
+  const long long per_cu = (wg + 255) / 256;
+  const long long kts = (KT + s - 1) / s;
+  const double share = per_cu >= 2 && c.occ >= 2 ? LRCNN_SHARE2 : 1.0;
+  double t = (double)kts * (double)per_cu * c.step_us * share + c.fixed_us;
+  if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
+  return t;
+}
+// A split count s of a K loop of KT iterations is used only when no smaller
+// count gives the same chunks (each of the s chunks has ceil(KT / s)
+// iterations, the last one possibly fewer, none empty).
+inline bool split_valid(int KT, long long s) {
+  if (s == 1) return true;
+  if (s < 1 || s > 128 || s > KT / 2) return false;
+  const long long kts = (KT + s - 1) / s;
+  return (KT + kts - 1) / kts == s;
+}
 inline SplitChoice split_choice(long long tiles, int KT, long long part_elems, size_t cap,
                                 const SplitCost &c) {
-  auto cost = [&](long long s) {
-    const long long wg = tiles * s;
-    const long long per_cu = (wg + 255) / 256;
-    const long long kts = (KT + s - 1) / s;
-    const double share = per_cu >= 2 && c.occ >= 2 ? LRCNN_SHARE2 : 1.0;
-    double t = (double)kts * (double)per_cu * c.step_us * share + c.fixed_us;
-    if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
-    return t;
-  };
-  SplitChoice best{1, cost(1)};
+  SplitChoice best{1, split_cost(tiles, KT, part_elems, c, 1)};
   if (tiles <= 0 || KT <= 1) return best;
   for (long long s = 2; s <= 128 && s <= KT / 2; ++s) {
     if ((size_t)s * (size_t)part_elems * 4 > cap) break;
-    const long long kts = (KT + s - 1) / s;
-    if ((KT + kts - 1) / kts != s) continue;  // same work as a smaller s
-    const double t = cost(s);
+    if (!split_valid(KT, s)) continue;  // same work as a smaller s
+    const double t = split_cost(tiles, KT, part_elems, c, s);
     if (t < best.us * 0.98) best = SplitChoice{(int)s, t};
   }
   return best;
+}
+// The guard every split launch passes before it is enqueued: its partial
+// sums (splits x M x N float32) fit the buffer it was given, and M x N
+// indexes in 32 bits (the reduction's index arithmetic). A launch that
+// fails it is refused with an error instead of writing past the buffer.
+inline bool split_fits(long long splits, long long M, long long N, const void *part,
+                       size_t part_bytes) {
+  if (splits <= 1) return true;
+  if (!part || M <= 0 || N <= 0) return false;
+  if (M * N >= (1ll << 32)) return false;
+  return (unsigned long long)splits * (unsigned long long)M * (unsigned long long)N * 4ull <=
+         (unsigned long long)part_bytes;
 }
 inline int split_count(long long tiles, int KT, long long part_elems, size_t cap,
                        const SplitCost &c) {
@@ -217,6 +241,19 @@ inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es) {
 // split count of a convolution launch (the planner sizes partial sums with it)
 inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
   return conv_tiles(M, N, KT, cap, es).splits;
+}
+// Tile width of a convolution launch whose split count is fixed (the
+// forward launches of one layer all use the layer's count, so every output
+// element sums K in the same chunks whatever the band); `us` its estimate.
+inline ConvTiles conv_tiles_split(long long M, int N, int KT, int s, int es) {
+  const double f = es == 2 ? 0.75 : 1.0;
+  const long long mt = (M + 127) / 128;
+  const double u64 = split_cost(mt * ((N + 63) / 64), KT, M * (long long)N,
+                                SplitCost{LRCNN_STEP_N64 * f, 3, 5.0}, s);
+  if (N <= 64) return ConvTiles{64, s, u64};
+  const double u128 = split_cost(mt * ((N + 127) / 128), KT, M * (long long)N,
+                                 SplitCost{LRCNN_STEP_N128 * f, 2, 5.0}, s);
+  return u64 < u128 * LRCNN_NARROW_GAIN ? ConvTiles{64, s, u64} : ConvTiles{128, s, u128};
 }
 // K iterations of a conv for storage element size es (bytes); one
 // iteration covers LRCNN_CONV_KR 16-byte vectors of a tile row.

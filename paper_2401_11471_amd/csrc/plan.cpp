@@ -190,6 +190,50 @@ static std::vector<int> balanced_bounds(Plan &P, int H, int nb) {
   return best;
 }
 
+// Rows of the last node completed once input rows [0, x) exist (the
+// frontiers of every node, as in carry_rows).
+static int last_frontier(const Plan &P, int x) {
+  std::vector<int> F(P.n, 0);
+  F[0] = x;
+  for (int v = 1; v < P.n; ++v) {
+    const lrcnn_node &nd = P.nodes[v];
+    if (nd.op == LRCNN_OP_ADD) {
+      F[v] = std::min(F[nd.in0], F[nd.in1]);
+    } else {
+      int k, s, p;
+      ksp(nd, k, s, p);
+      F[v] = frontier(F[nd.in0], P.shp[nd.in0].h, P.shp[v].h, k, s, p);
+    }
+  }
+  return F[P.n - 1];
+}
+
+// PAPER_2PS: the greedy partition of two-phase sharing (Section IV-A). The
+// first band completes `first` rows of the last node (H_1^L), the others
+// share the remaining rows evenly; each band's input height is inferred
+// from the last layer back to the input: the end of band r is the smallest
+// input row count whose last-node frontier reaches the band's target t_r.
+// For a chain this is Eq. (11) for the first band (H_1^l = (H_1^{l+1} - 1)
+// s + k - p) and Eq. (13) for the middle bands (H_r^l = H_r^{l+1} s); the
+// last band takes the rest of the input (Eq. (14)). The frontier is
+// monotone in the input rows, so the smallest count is found by bisection.
+static std::vector<int> paper_bounds(const Plan &P, int H, int nb, int first) {
+  const int HL = P.shp[P.n - 1].h;
+  const int h1 = first > 0 ? std::min(first, HL) : (HL + nb - 1) / nb;
+  std::vector<int> bd(nb + 1, 0);
+  bd[nb] = H;
+  for (int r = 1; r < nb; ++r) {
+    const int t = h1 + (int)((int64_t)(r - 1) * (HL - h1) / std::max(1, nb - 1));
+    int lo = bd[r - 1], hi = H;  // smallest x in [bd[r-1], H] with frontier >= t
+    while (lo < hi) {
+      const int mid = lo + (hi - lo) / 2;
+      if (last_frontier(P, mid) >= t) hi = mid; else lo = mid + 1;
+    }
+    bd[r] = lo;
+  }
+  return bd;
+}
+
 static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
   if (!nodes || !cfg) return lrcnn_fail(LRCNN_EINVAL, "null nodes or config");
   if (n < 2) return lrcnn_fail(LRCNN_ESHAPE, "need an input node and at least one layer");
@@ -202,10 +246,14 @@ static int validate(const lrcnn_node *nodes, int n, const lrcnn_config *cfg) {
   if (cfg->mode != LRCNN_CARRY && cfg->mode != LRCNN_RECOMPUTE)
     return lrcnn_fail(LRCNN_EINVAL, "mode must be LRCNN_CARRY or LRCNN_RECOMPUTE");
   if (cfg->n_bands < 1) return lrcnn_fail(LRCNN_EPARTITION, "n_bands must be >= 1");
-  if (cfg->policy < LRCNN_EVEN || cfg->policy > LRCNN_EXPLICIT)
+  if (cfg->policy < LRCNN_EVEN || cfg->policy > LRCNN_PAPER_2PS)
     return lrcnn_fail(LRCNN_EINVAL, "bad partition policy");
   if (cfg->policy == LRCNN_BALANCED && cfg->mode != LRCNN_CARRY)
     return lrcnn_fail(LRCNN_EINVAL, "BALANCED applies to CARRY mode only");
+  if (cfg->policy == LRCNN_PAPER_2PS && cfg->mode != LRCNN_CARRY)
+    return lrcnn_fail(LRCNN_EINVAL, "PAPER_2PS applies to CARRY mode only");
+  if (cfg->policy == LRCNN_PAPER_2PS && cfg->first_rows < 0)
+    return lrcnn_fail(LRCNN_EPARTITION, "first_rows must be >= 0");
   if (cfg->policy == LRCNN_EXPLICIT && !cfg->bounds)
     return lrcnn_fail(LRCNN_EINVAL, "EXPLICIT policy needs bounds");
   if (cfg->bp_refine < 0 || cfg->bp_refine > 64)
@@ -275,13 +323,68 @@ static size_t pack(std::vector<LiveBuf> &bufs) {
   return peak;
 }
 
+// Bytes of split-K partial sums one launch may use.
+#ifndef LRCNN_PART_MIB
+#define LRCNN_PART_MIB 24
+#endif
+static constexpr size_t kPartCap = (size_t)LRCNN_PART_MIB << 20;
+
+// Split-K count of every conv's forward launches. All forward launches of a
+// layer -- the row-centric bands, their backward recompute and the
+// layer-wise launch -- use one count, so each output element sums the same
+// K chunks in the same order whatever band computes it: the row-centric and
+// layer-wise forwards (and the ReLU / argmax decisions) are then bitwise
+// equal. The count is the one with the smallest summed duration estimate
+// over those launches (the layer-wise launch in row chunks whose partial
+// sums fit the buffer), among the counts whose partial sums fit the buffer
+// at every row-centric launch.
+static void forward_splits(Plan &P,
+                           const std::vector<const std::vector<std::vector<Rows>> *> &tabs) {
+  P.fsplit.assign(P.n, 0);
+  const long long B = P.cfg.batch;
+  for (int v = 1; v < P.n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV) continue;
+    const Shape &su = P.shp[d.in0], &sv = P.shp[v];
+    const int KT = conv_k_iters(d.kh * d.kw, su.c, P.es);
+    std::vector<long long> ms;
+    long long mmax = 0;
+    for (auto *tab : tabs)
+      for (auto &br : *tab)
+        if (br[v].b > br[v].a) {
+          ms.push_back(B * (br[v].b - br[v].a) * sv.w);
+          mmax = std::max(mmax, ms.back());
+        }
+    int best_s = 1;
+    double best = -1;
+    for (int sp = 1; sp <= 128; ++sp) {
+      if (!split_valid(KT, sp)) continue;
+      if (sp > 1 && (size_t)sp * (size_t)mmax * sv.c * 4 > kPartCap) break;
+      double t = 0;
+      for (long long m : ms) t += conv_tiles_split(m, sv.c, KT, sp, P.es).us;
+      // the layer-wise launch, in chunks of rows
+      const size_t row_part = (size_t)sp * B * sv.w * sv.c * 4;
+      const int rows = sp > 1 ? (int)std::min<size_t>(sv.h, std::max<size_t>(1, kPartCap / row_part))
+                              : sv.h;
+      const int full = sv.h / rows, rest = sv.h - full * rows;
+      t += full * conv_tiles_split(B * rows * sv.w, sv.c, KT, sp, P.es).us;
+      if (rest) t += conv_tiles_split(B * rest * sv.w, sv.c, KT, sp, P.es).us;
+      if (best < 0 || t < best * 0.98) {
+        best = t;
+        best_s = sp;
+      }
+    }
+    P.fsplit[v] = best_s;
+  }
+}
+
 // Lay out one workspace. Backward (and, unless packed, forward) windows
 // hold cap[v] rows, a band owns at most own[v] rows, carry[v] rows of error
 // are carried (CARRY). `bands` lists the row intervals of every launch
 // (forward and backward partitions) for sizing the partial sums; `fpw`
 // (nullable) gives the forward windows' rows when they are packed by
 // lifetime.
-static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
+static void layout(Plan &P, Layout &L, const Fuse &F, const std::vector<int> &cap,
                    const std::vector<int> &own, const std::vector<int> &carry,
                    const std::vector<const std::vector<std::vector<Rows>> *> &bands,
                    bool strips, bool layerwise, bool dxacc, const std::vector<int> *fpw) {
@@ -318,10 +421,23 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   const int vec_e = 16 / P.es;
   L.cpad = P.shp[0].c % vec_e ? (P.shp[0].c + vec_e - 1) / vec_e * vec_e : 0;
   int xrows = 0;
-#ifndef LRCNN_PART_MIB
-#define LRCNN_PART_MIB 24
-#endif
-  const size_t pcap = (size_t)LRCNN_PART_MIB << 20;
+  const size_t pcap = kPartCap;
+  // The layer-wise schedule's partial sums get a buffer that does not
+  // depend on the row partition (the baseline's memory must not move with
+  // it): what the largest split of the largest launch would need, capped
+  // at the launch cap; its forward launches run in row chunks that fit.
+  size_t lw_part = 0;
+  if (layerwise) {
+    for (int v = 1; v < n; ++v)
+      if (P.nodes[v].op == LRCNN_OP_CONV) {
+        const Shape &su = P.shp[P.nodes[v].in0], &sv = P.shp[v];
+        const size_t mf = (size_t)P.cfg.batch * sv.h * sv.w * sv.c;
+        const size_t md = (size_t)P.cfg.batch * su.h * su.w * su.c;
+        lw_part = std::max(lw_part, 128 * std::max(mf, md) * 4);
+      }
+    lw_part = std::min(lw_part, pcap);
+  }
+  L.fchunk.assign(n, 0);
   for (int v = 1; v < n; ++v)
     if (P.nodes[v].op == LRCNN_OP_CONV) {
       const lrcnn_node &d = P.nodes[v];
@@ -329,6 +445,14 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
       const int taps = d.kh * d.kw;
       const bool padded = L.cpad && d.in0 == 0;
       const int64_t nw = (int64_t)taps * (padded ? L.cpad : su.c);
+      // forward launches: the layer's fixed split count; a layer-wise launch
+      // too large for the partial buffer runs as several row chunks
+      const int sf = P.fsplit[v];
+      const size_t row_part = (size_t)sf * P.cfg.batch * sv.w * sv.c * 4;
+      if (layerwise && sf > 1) {
+        const int rows_fit = (int)std::max<size_t>(1, lw_part / row_part);
+        L.fchunk[v] = rows_fit < sv.h ? rows_fit : 0;
+      }
       std::vector<Rows> qs;
       if (layerwise) qs.push_back(Rows{0, sv.h, 0, sv.h});
       for (auto *tab : bands)
@@ -338,8 +462,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
         const long long mf = (long long)P.cfg.batch * (q.b - q.a) * sv.w;
         const int sw_ = wgrad_split_count(d.c_out, nw, mf, pcap, P.es);
         if (sw_ > 1) wpn[v] = std::max(wpn[v], (size_t)sw_ * d.c_out * nw * 4);
-        const int sf = conv_split_count(mf, sv.c, conv_k_iters(taps, su.c, P.es), pcap, P.es);
-        if (sf > 1) part = std::max(part, (size_t)(sf * mf * sv.c * 4));
+        if (sf > 1 && !layerwise) part = std::max(part, (size_t)sf * (size_t)mf * sv.c * 4);
         const int u0 = std::max(0, q.a * d.sh - d.ph);
         const int u1 = std::min(su.h, (q.b - 1) * d.sh - d.ph + d.kh);
         if (padded) xrows = std::max(xrows, u1 - u0);
@@ -348,6 +471,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
         if (sd > 1) part = std::max(part, (size_t)(sd * md * su.c * 4));
       }
     }
+  if (layerwise) part = lw_part;
   L.part_bytes = part;
   L.part = A.take(part);
   const size_t ubase = A.top;
@@ -391,7 +515,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
     // (an act-fused conv's error window only stages the rows its consumer's
     // input gradient carries out, which the launch may not write into the
     // carry buffer it reads the rows carried in from)
-    const bool staged = !P.fuse_act.empty() && P.fuse_act[v];
+    const bool staged = F.act[v] != 0;
     bufs[v] = LiveBuf{n - 1 - first, n - 1 - v, P.elems(v, staged ? carry[v] : cap[v]) * 4, 0};
   }
   std::vector<int> dc_i(n, -1), wp_i(n, -1);
@@ -402,9 +526,7 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
       if (P.nodes[u].op == LRCNN_OP_CONV) nxt = u;
     // (a conv fed by an add's backward gets its error operand at the add's step)
     // (or at the step of the conv whose input gradient forms it)
-    const int early = !P.fuse_add.empty() && P.fuse_add[v]   ? P.fuse_add[v]
-                      : !P.fuse_act.empty() && P.fuse_act[v] ? P.fuse_act[v]
-                                                             : v;
+    const int early = F.add[v] ? F.add[v] : F.act[v] ? F.act[v] : v;
     const int s0 = n - 1 - early;
     const int s1 = nxt ? n - 2 - nxt : n - 1;
     dc_i[v] = (int)bufs.size();
@@ -458,7 +580,67 @@ static void layout(Plan &P, Layout &L, const std::vector<int> &cap,
   L.total = std::max<size_t>(std::max(bp_end, fp_end), 256);
 }
 
-static int build(Plan &P) {
+// Fusions of a schedule whose backward bands have rows `rows` and forward
+// bands `rows_fp` (act_ok: the schedule may form a conv's error operand in
+// its consumer's backward launch -- CARRY and layer-wise).
+static Fuse decide_fusions(const Plan &P, const std::vector<std::vector<Rows>> &rows,
+                           const std::vector<std::vector<Rows>> &rows_fp, bool act_ok) {
+  const int n = P.n, nb = (int)rows.size();
+  Fuse F;
+  // convs whose error operand the residual add's backward can write
+  F.add.assign(n, 0);
+  for (int v = 1; v < n; ++v) {
+    const lrcnn_node &d = P.nodes[v];
+    if (d.op != LRCNN_OP_CONV || d.relu || P.cons[v].size() != 1) continue;
+    const int c = P.cons[v][0];
+    if (P.nodes[c].op != LRCNN_OP_ADD || P.nodes[c].in0 == P.nodes[c].in1) continue;
+    bool ok = true;
+    for (int r = 0; r < nb && ok; ++r) ok = rows[r][v].lo == rows[r][v].a;
+    if (ok) F.add[v] = c;
+  }
+  F.fwd.assign(n, 0);
+  for (int v = 1; v < n; ++v) {
+    const int c = F.add[v];
+    if (!c || v != std::max(P.nodes[c].in0, P.nodes[c].in1)) continue;
+    if (P.shp[v].c % (16 / P.es) != 0) continue;
+    bool ok = true;
+    for (int r = 0; r < nb && ok; ++r)
+      ok = rows[r][v].a == rows[r][c].a && rows[r][v].b == rows[r][c].b;
+    for (size_t r = 0; r < rows_fp.size() && ok; ++r)
+      ok = rows_fp[r][v].a == rows_fp[r][c].a && rows_fp[r][v].b == rows_fp[r][c].b &&
+           rows_fp[r][v].lo == rows_fp[r][v].a;
+    if (ok) F.fwd[v] = c;
+  }
+  // convs whose error operand the backward launch of their only consumer v
+  // (a conv's input gradient, a max-pool's backward) forms: in every band
+  // v's launch must cover exactly u's error-window rows, which end with u's
+  // own rows, or the band must hold nothing of u; u's float32 error window
+  // is then never used
+  F.act.assign(n, 0);
+  if (act_ok && !g_no_act_fusion)
+    for (int u = 1; u < n; ++u) {
+      if (P.nodes[u].op != LRCNN_OP_CONV || F.add[u] || P.cons[u].size() != 1) continue;
+      const int v = P.cons[u][0];
+      const lrcnn_node &d = P.nodes[v];
+      if (d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) continue;
+      const int hu = P.shp[u].h;
+      bool ok = true;
+      for (int r = 0; r < nb && ok; ++r) {
+        const Rows &qv = rows[r][v], &qu = rows[r][u];
+        if (qv.b > qv.a) {
+          const int y0 = std::max(0, qv.a * d.sh - d.ph);
+          const int y1 = std::min(hu, (qv.b - 1) * d.sh - d.ph + d.kh);
+          ok = y0 == qu.lo && y1 == qu.hi && qu.hi == qu.b && qu.lo <= qu.a;
+        } else {
+          ok = qu.b <= qu.a && qu.lo == qu.a;
+        }
+      }
+      if (ok) F.act[u] = v;
+    }
+  return F;
+}
+
+static int shapes_and_consumers(Plan &P) {
   const int n = P.n;
   // shapes
   P.shp.assign(n, Shape{});
@@ -488,6 +670,85 @@ static int build(Plan &P) {
     if (P.cons[v].empty())
       return lrcnn_fail(LRCNN_ESHAPE, "node " + std::to_string(v) +
                                           " feeds nothing (only the last node is an output)");
+  return LRCNN_OK;
+}
+
+static void finish(Plan &P, const std::vector<int> &bd, const std::vector<int> &bb,
+                   bool quick = false);
+
+// Peak workspace of the row-centric step for forward bounds `bd` (the
+// backward bands refine each evenly), planned on a scratch copy.
+static size_t workspace_for(const Plan &P, const std::vector<int> &bd) {
+  Plan Q;
+  Q.nodes = P.nodes;
+  Q.cfg = P.cfg;
+  Q.cfg.bounds = nullptr;
+  Q.n = P.n;
+  Q.es = P.es;
+  Q.shp = P.shp;
+  Q.cons = P.cons;
+  Q.no_keep = P.no_keep;
+  Q.dy_f32 = P.dy_f32;
+  Q.lw_keep_out = P.lw_keep_out;
+  const int refine = P.cfg.bp_refine > 1 ? P.cfg.bp_refine : 1;
+  const int nbf = (int)bd.size() - 1;
+  std::vector<int> bb;
+  for (int r = 0; r < nbf; ++r)
+    for (int j = 0; j < refine; ++j)
+      bb.push_back(bd[r] + (int)((int64_t)(bd[r + 1] - bd[r]) * j / refine));
+  bb.push_back(bd[nbf]);
+  finish(Q, bd, bb, true);
+  return Q.rc.total;
+}
+
+// BALANCED: forward bounds that minimise the step's peak workspace (every
+// buffer the plan lays out: band windows, shared-row strips, error
+// windows, carries, partial sums). Starts from the better of the even split
+// and the bounds that balance the per-band caches (the skew of Section
+// IV-A), then moves one boundary at a time by decreasing steps while the
+// workspace shrinks (a bounded local search over exact plans).
+static std::vector<int> balanced_peak_bounds(Plan &P, int H, int nb) {
+  std::vector<int> even(nb + 1);
+  for (int r = 0; r <= nb; ++r) even[r] = (int)((int64_t)r * H / nb);
+  std::vector<int> best = even;
+  size_t best_ws = workspace_for(P, even);
+  if (nb <= 1) return best;
+  {
+    std::vector<int> bal = balanced_bounds(P, H, nb);
+    const size_t w = workspace_for(P, bal);
+    if (w < best_ws) {
+      best_ws = w;
+      best = bal;
+    }
+  }
+  int evals = 0;
+  const int max_evals = 400;
+  for (int step = std::max(1, H / (2 * nb)); step >= 1 && evals < max_evals; step /= 2) {
+    bool moved = true;
+    while (moved && evals < max_evals) {
+      moved = false;
+      for (int r = 1; r < nb && evals < max_evals; ++r)
+        for (int sgn = -1; sgn <= 1; sgn += 2) {
+          std::vector<int> cand = best;
+          cand[r] += sgn * step;
+          if (cand[r] < cand[r - 1] || cand[r] > cand[r + 1]) continue;
+          const size_t w = workspace_for(P, cand);
+          ++evals;
+          if (w < best_ws) {
+            best_ws = w;
+            best = cand;
+            moved = true;
+          }
+        }
+    }
+  }
+  return best;
+}
+
+static int build(Plan &P) {
+  const int n = P.n;
+  int st = shapes_and_consumers(P);
+  if (st != LRCNN_OK) return st;
   // bounds of the forward partition, refined evenly for the backward one
   const bool carry = P.cfg.mode == LRCNN_CARRY;
   const int H = carry ? P.shp[0].h : P.shp[n - 1].h;
@@ -501,15 +762,35 @@ static int build(Plan &P) {
     for (int r = 0; r < nbf; ++r)
       if (bd[r + 1] < bd[r]) return lrcnn_fail(LRCNN_EPARTITION, "bounds must be non-decreasing");
   } else if (P.cfg.policy == LRCNN_BALANCED) {
-    bd = balanced_bounds(P, H, nbf);
-  } else {
+    bd = balanced_peak_bounds(P, H, nbf);
+  } else if (P.cfg.policy != LRCNN_PAPER_2PS) {
     for (int r = 0; r <= nbf; ++r) bd[r] = (int)((int64_t)r * H / nbf);
   }
   std::vector<int> bb;
-  for (int r = 0; r < nbf; ++r)
-    for (int j = 0; j < refine; ++j)
-      bb.push_back(bd[r] + (int)((int64_t)(bd[r + 1] - bd[r]) * j / refine));
-  bb.push_back(H);
+  if (P.cfg.policy == LRCNN_PAPER_2PS) {
+    // the partition is made for the backward bands; the forward bands are
+    // every refine-th of them
+    bb = paper_bounds(P, H, nbf * refine, P.cfg.first_rows);
+    for (int r = 0; r <= nbf; ++r) bd[r] = bb[r * refine];
+  } else {
+    for (int r = 0; r < nbf; ++r)
+      for (int j = 0; j < refine; ++j)
+        bb.push_back(bd[r] + (int)((int64_t)(bd[r + 1] - bd[r]) * j / refine));
+    bb.push_back(H);
+  }
+  (void)n;
+  finish(P, bd, bb);
+  return LRCNN_OK;
+}
+
+// Everything after the bounds: row intervals of both partitions, fusions,
+// split counts, the two workspace layouts and the FLOP figures (quick:
+// only what the row-centric workspace size needs).
+static void finish(Plan &P, const std::vector<int> &bd, const std::vector<int> &bb, bool quick) {
+  const int n = P.n;
+  const bool carry = P.cfg.mode == LRCNN_CARRY;
+  const int nbf = (int)bd.size() - 1;
+  const int refine = (int)(bb.size() - 1) / std::max(1, nbf);
   P.nb_fp = nbf;
   P.refine = refine;
   P.nb = nbf * refine;
@@ -519,56 +800,13 @@ static int build(Plan &P) {
   P.rows_fp = P.rows;
   if (carry) carry_rows(P, bb); else cone_rows(P, bb);
   const int nb = P.nb;
-  // convs whose error operand the residual add's backward can write
-  P.fuse_add.assign(n, 0);
-  for (int v = 1; v < n; ++v) {
-    const lrcnn_node &d = P.nodes[v];
-    if (d.op != LRCNN_OP_CONV || d.relu || P.cons[v].size() != 1) continue;
-    const int c = P.cons[v][0];
-    if (P.nodes[c].op != LRCNN_OP_ADD || P.nodes[c].in0 == P.nodes[c].in1) continue;
-    bool ok = true;
-    for (int r = 0; r < nb && ok; ++r) ok = P.rows[r][v].lo == P.rows[r][v].a;
-    if (ok) P.fuse_add[v] = c;
+  P.fz = decide_fusions(P, P.rows, P.rows_fp, carry);
+  {
+    // the layer-wise schedule: one band of whole maps
+    std::vector<std::vector<Rows>> whole(1, std::vector<Rows>(n));
+    for (int v = 0; v < n; ++v) whole[0][v] = Rows{0, P.shp[v].h, 0, P.shp[v].h};
+    P.fz_lw = decide_fusions(P, whole, whole, true);
   }
-  P.fuse_fwd.assign(n, 0);
-  for (int v = 1; v < n; ++v) {
-    const int c = P.fuse_add[v];
-    if (!c || v != std::max(P.nodes[c].in0, P.nodes[c].in1)) continue;
-    if (P.shp[v].c % (16 / P.es) != 0) continue;
-    bool ok = true;
-    for (int r = 0; r < nb && ok; ++r)
-      ok = P.rows[r][v].a == P.rows[r][c].a && P.rows[r][v].b == P.rows[r][c].b;
-    for (size_t r = 0; r < P.rows_fp.size() && ok; ++r)
-      ok = P.rows_fp[r][v].a == P.rows_fp[r][c].a && P.rows_fp[r][v].b == P.rows_fp[r][c].b &&
-           P.rows_fp[r][v].lo == P.rows_fp[r][v].a;
-    if (ok) P.fuse_fwd[v] = c;
-  }
-  // convs whose error operand the backward launch of their only consumer v
-  // (a conv's input gradient, a max-pool's backward) forms: in every band (and in the layer-wise schedule) v's launch must
-  // cover exactly u's error-window rows, which end with u's own rows, or
-  // the band must hold nothing of u; u's float32 error window is then never
-  // used
-  P.fuse_act.assign(n, 0);
-  if (carry && !g_no_act_fusion)
-    for (int u = 1; u < n; ++u) {
-      if (P.nodes[u].op != LRCNN_OP_CONV || P.fuse_add[u] || P.cons[u].size() != 1) continue;
-      const int v = P.cons[u][0];
-      const lrcnn_node &d = P.nodes[v];
-      if (d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) continue;
-      const int hu = P.shp[u].h;
-      bool ok = std::min(hu, (P.shp[v].h - 1) * d.sh - d.ph + d.kh) == hu;  // layer-wise
-      for (int r = 0; r < nb && ok; ++r) {
-        const Rows &qv = P.rows[r][v], &qu = P.rows[r][u];
-        if (qv.b > qv.a) {
-          const int y0 = std::max(0, qv.a * d.sh - d.ph);
-          const int y1 = std::min(hu, (qv.b - 1) * d.sh - d.ph + d.kh);
-          ok = y0 == qu.lo && y1 == qu.hi && qu.hi == qu.b && qu.lo <= qu.a;
-        } else {
-          ok = qu.b <= qu.a && qu.lo == qu.a;
-        }
-      }
-      if (ok) P.fuse_act[u] = v;
-    }
   // capacities
   std::vector<int> cap(n, 0), own(n, 0), cry(n, 0), fcap(n, 0);
   for (int r = 0; r < nb; ++r)
@@ -584,11 +822,13 @@ static int build(Plan &P) {
       fcap[v] = std::max(fcap[v], q.hi - q.lo);
     }
   std::vector<const std::vector<std::vector<Rows>> *> tabs = {&P.rows, &P.rows_fp};
-  layout(P, P.rc, cap, own, cry, tabs, carry, false, !carry && P.cfg.dtype == LRCNN_BF16,
+  forward_splits(P, tabs);
+  layout(P, P.rc, P.fz, cap, own, cry, tabs, carry, false, !carry && P.cfg.dtype == LRCNN_BF16,
          refine > 1 ? &fcap : nullptr);
+  if (quick) return;
   std::vector<int> full(n), zero(n, 0);
   for (int v = 0; v < n; ++v) full[v] = P.shp[v].h;
-  layout(P, P.lw, full, full, zero, {}, false, true, false, nullptr);
+  layout(P, P.lw, P.fz_lw, full, full, zero, {}, false, true, false, nullptr);
   // FLOPs: tau of Section IV-B and the row-centric total (FP over the
   // forward bands; BP recompute, input and weight gradient over the backward
   // bands; without recomputing the last band when FP left it in place)
@@ -613,7 +853,6 @@ static int build(Plan &P) {
     }
   if (!carry)
     for (int v = 0; v < n; ++v) P.halo_rows -= P.shp[v].h;
-  return LRCNN_OK;
 }
 
 }  // namespace lrcnn
@@ -870,8 +1109,9 @@ extern "C" int lrcnn_plan_for_budget(const lrcnn_node *nodes, int32_t n_nodes,
   if (!out) return lrcnn_fail(LRCNN_EINVAL, "null output pointer");
   *out = nullptr;
   if (!nodes || !cfg || !budget) return lrcnn_fail(LRCNN_EINVAL, "null argument");
-  if (cfg->policy != LRCNN_EVEN && cfg->policy != LRCNN_BALANCED)
-    return lrcnn_fail(LRCNN_EINVAL, "the budget search takes the EVEN or BALANCED policy");
+  if (cfg->policy == LRCNN_EXPLICIT)
+    return lrcnn_fail(LRCNN_EINVAL,
+                      "the budget search takes the EVEN, BALANCED or PAPER_2PS policy");
   if (budget->max_bands < 0 || budget->max_refine < 0 || budget->max_refine > 64)
     return lrcnn_fail(LRCNN_EINVAL, "max_bands must be >= 0 and max_refine in [0, 64]");
   lrcnn_config c = *cfg;
@@ -889,23 +1129,32 @@ extern "C" int lrcnn_plan_for_budget(const lrcnn_node *nodes, int32_t n_nodes,
     *out = probe;
     return LRCNN_OK;
   }
+  const int HL_probe = P1.shp[P1.n - 1].h;
   lrcnn_plan_destroy(probe);
   const int maxb = budget->max_bands > 0 ? std::min(budget->max_bands, H) : std::min(256, H);
   const int maxr = budget->max_refine > 1 ? budget->max_refine : 1;
+  // PAPER_2PS (Eq. (12)): for each N_BP the largest H_1^L whose step fits,
+  // from all H_L rows in the first band down to an even share
+  const int HL = HL_probe;
   for (int nbp = 2; nbp <= maxb; ++nbp) {
     for (int nfp = 1; nfp <= nbp; ++nfp) {
       if (nbp % nfp != 0 || nbp / nfp > maxr) continue;
       c.n_bands = nfp;
       c.bp_refine = nbp / nfp;
-      lrcnn_plan_t *p = nullptr;
-      st = lrcnn_plan(nodes, n_nodes, &c, &p);
-      if (st != LRCNN_OK) return st;
-      if (lrcnn::step_bytes(*reinterpret_cast<const Plan *>(p), false, budget->want_dx != 0) <=
-          budget->budget_bytes) {
-        *out = p;
-        return LRCNN_OK;
+      const bool paper = c.policy == LRCNN_PAPER_2PS;
+      const int h_lo = paper ? (HL + nbp - 1) / nbp : 0;
+      for (int h1 = paper ? HL : 0; h1 >= h_lo; --h1) {
+        c.first_rows = h1;
+        lrcnn_plan_t *p = nullptr;
+        st = lrcnn_plan(nodes, n_nodes, &c, &p);
+        if (st != LRCNN_OK) return st;
+        if (lrcnn::step_bytes(*reinterpret_cast<const Plan *>(p), false,
+                              budget->want_dx != 0) <= budget->budget_bytes) {
+          *out = p;
+          return LRCNN_OK;
+        }
+        lrcnn_plan_destroy(p);
       }
-      lrcnn_plan_destroy(p);
     }
   }
   return lrcnn_fail(LRCNN_EINFEASIBLE, "no plan with at most " + std::to_string(maxb) +

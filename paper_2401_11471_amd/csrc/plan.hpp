@@ -45,6 +45,9 @@ struct Layout {
   size_t xpad = 0;
   std::vector<size_t> dwpad;
   size_t dxacc = 0, dxacc_bytes = 0;  // RECOMPUTE: float32 dX accumulator
+  // per conv node: the most output rows one forward launch may cover, so
+  // that its split-K partial sums fit `part_bytes` (0: no limit)
+  std::vector<int> fchunk;
   size_t strip_bytes = 0, cache_bytes = 0, delta_bytes = 0, carry_bytes = 0;
   // forward windows packed by lifetime (when the forward partition is
   // coarser than the backward one); they share memory with the buffers that
@@ -53,6 +56,22 @@ struct Layout {
   std::vector<size_t> fwin;
   std::vector<int> fwin_cap;
   size_t fwin_bytes = 0;
+};
+
+// Fusions of a schedule (decided from that schedule's own rows, so the
+// layer-wise baseline does not depend on the row partition):
+//  add[u]: the ADD node whose backward writes conv u's error operand
+//          directly (a conv without ReLU whose only consumer is that add
+//          and that carries no rows between backward bands), else 0
+//  fwd[u]: the ADD node whose forward conv u's epilogue computes (the add's
+//          later input, fused in its backward, same rows in every band and
+//          whole 16-byte channel vectors), else 0
+//  act[u]: (CARRY / layer-wise) conv u's only consumer, a conv or max-pool
+//          v, whose backward launch forms u's error operand and carry
+//          directly (when that launch initializes u's whole error window);
+//          u's error operand then lives from v's backward step
+struct Fuse {
+  std::vector<int> add, fwd, act;
 };
 
 struct Plan {
@@ -67,19 +86,12 @@ struct Plan {
   std::vector<std::vector<Rows>> rows; // [backward band][node]
   std::vector<std::vector<Rows>> rows_fp;  // [forward band][node]
   std::vector<std::vector<int>> tail;  // CARRY: [backward band][node] first kept row
-  // per node: the ADD node whose backward writes this conv's error operand
-  // directly (a conv without ReLU whose only consumer is that add and that
-  // carries no rows between backward bands), else 0
-  std::vector<int> fuse_add;
-  // per node: the ADD node whose forward this conv's epilogue computes (the
-  // add's later input, fused in its backward, same rows in every band and
-  // whole 16-byte channel vectors), else 0
-  std::vector<int> fuse_fwd;
-  // per conv u (CARRY / layer-wise): its only consumer, a conv v, whose
-  // input gradient may form u's error operand and carry directly (when that
-  // launch initializes u's whole error window); u's error operand then lives
-  // from v's backward step
-  std::vector<int> fuse_act;
+  Fuse fz;     // fusions of the row-centric schedule
+  Fuse fz_lw;  // fusions of the layer-wise schedule
+  // per conv node: the split-K count of every forward launch (row-centric
+  // bands, recompute and layer-wise alike), so each output element sums
+  // its K products in the same order in every schedule (0: not a conv)
+  std::vector<int> fsplit;
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   double tau = 0, flops_rows = 0;

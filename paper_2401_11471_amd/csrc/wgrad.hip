@@ -1,0 +1,303 @@
+// Weight-gradient kernel and its fixed-order split-K reduction.
+#include "kdev.hpp"
+
+namespace lrcnn {
+
+// ------------------------------------------------------------ weight grad
+// A[m = co][k = pixel] = dc[pixel][co] and B[k = pixel][n = (tap, ci)] =
+// input pixel under tap. Both are K-outer in memory, so both tiles are
+// staged k-major ([k][row], 16-byte stores). The tile is WBM x 128: WBM =
+// 128 (four waves of 64 x 64) or, for 64 output channels or fewer, WBM = 64
+// (four waves of 64 x 32), so a narrow layer does not compute a half-empty
+// tile.
+#ifndef LRCNN_WG_OCC
+#define LRCNN_WG_OCC 2
+#endif
+template <typename T, int WBM, bool AVEC, bool BVEC>
+__global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, int kchunk,
+                                                    float *dw) {
+  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK;
+  constexpr int BN = 128;
+  constexpr int FBN = WBM == 128 ? 128 : 64;  // columns per wave: FBN / 2
+  constexpr int NB = FBN / 64;
+  constexpr int RV = BN / E;        // 16-byte vectors per B tile row
+  constexpr int KS = 256 / RV;      // pixels of B loaded per pass
+  constexpr int RVA = WBM / E;      // 16-byte vectors per A tile row
+  constexpr int KSA = 256 / RVA;    // pixels of A loaded per pass
+  constexpr int NPA = BK / KSA;     // A passes per tile
+  constexpr int PA = WBM + E, PB = BN + E;
+  constexpr int ASZ = BK * PA, BSZ = BK * PB;
+  constexpr int ST = 3;
+  __shared__ __align__(16) T As[ST][ASZ];
+  __shared__ __align__(16) T Bs[ST][BSZ];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int R = a.y1 - a.y0;
+  const int K = a.B * R * a.Wv;
+  const int taps = a.kh * a.kw;
+  const int N = taps * a.Ci;
+  // one split's pixel range per run of workgroups on an XCD
+  const TileId tl = xcd_tile(false);
+  const int m0 = tl.x * WBM, n0 = tl.y * BN;
+  const int kbeg = tl.z * kchunk;
+  const int kend = min(K, kbeg + kchunk);
+  const int rv = tid % RV, kk0 = tid / RV;
+  const int rva = tid % RVA, kka0 = tid / RVA;
+  const T *dc = (const T *)a.dc;
+  const T *src = (const T *)a.src.p;
+  const long long srow = (long long)a.src.W * a.src.C;
+
+  // this thread's B columns n0 + rv*E + e: (tap, channel) of each element
+  const int nb0 = n0 + rv * E;
+  const int tapv = nb0 / a.Ci, cv = nb0 - (nb0 / a.Ci) * a.Ci;
+  const int tiv = tapv / a.kw, tjv = tapv - (tapv / a.kw) * a.kw;
+  const int ov = m0 + rva * E;
+
+  union V16 {
+    uint4 u;
+    T e[E];
+  };
+  V16 ra[NPA], rb[2];
+  int k0 = kbeg;
+  const bool ovok = ov < a.Co, nbok = nb0 < N;
+  // channel counts that are not a multiple of E (the first layer): the
+  // (tap, channel) of each of this thread's E columns, fixed for the launch
+  int cti[BVEC ? 1 : E], ctj[BVEC ? 1 : E], cc[BVEC ? 1 : E];
+  bool cok[BVEC ? 1 : E];
+  if (!BVEC) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const int n = nb0 + e;
+      const int tap = n / a.Ci;
+      cc[e] = n - tap * a.Ci;
+      cti[e] = tap / a.kw;
+      ctj[e] = tap - cti[e] * a.kw;
+      cok[e] = n < N;
+    }
+  }
+  const T *zero_e = (const T *)&g_zero16[0];
+  // bounds tests use non-short-circuit '&' so that no test becomes a branch
+  auto gload = [&]() {
+#pragma unroll
+    for (int i = 0; i < NPA; ++i) {
+      // A: E output channels of pixel p
+      const int p = k0 + kka0 + KSA * i;
+      const bool pk = p < kend;
+      if (AVEC) {
+        ra[i].u = load16z(dc, ((long long)p * a.Co + ov) * (long long)sizeof(T), pk & ovok);
+      } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+          ra[i].e[e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      // B: E input values of pixel p under the column's tap
+      const int p = k0 + kk0 + KS * i;
+      const bool pk = p < kend;
+      uint32_t t, x, yy, b;
+      fdiv_qr((uint32_t)(pk ? p : 0), a.fw, t, x);
+      fdiv_qr(t, a.fr, b, yy);
+      const int y = a.y0 + (int)yy;
+      if (BVEC) {
+        const int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
+        const bool ok = pk & nbok & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+        const long long off =
+            b * a.src.bs + (sy - a.src.row0) * srow + (long long)sx * a.src.C + cv;
+        rb[i].u = load16z(src, off * (long long)sizeof(T), ok);
+      } else {
+        const long long bbase = b * a.src.bs - a.src.row0 * srow;
+        const int sy0 = y * a.sh - a.ph, sx0 = x * a.sw - a.pw;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int sy = sy0 + cti[e], sx = sx0 + ctj[e];
+          const bool ok =
+              pk & cok[e] & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+          const T *q = ok ? src + bbase + sy * srow + (long long)sx * a.src.C + cc[e] : zero_e;
+          rb[i].e[e] = *q;
+        }
+      }
+    }
+    k0 += BK;
+  };
+  auto store = [&](int st) {
+#pragma unroll
+    for (int i = 0; i < NPA; ++i)
+      *(uint4 *)(&As[st][(kka0 + KSA * i) * PA + rva * E]) = ra[i].u;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      *(uint4 *)(&Bs[st][(kk0 + KS * i) * PB + rv * E]) = rb[i].u;
+  };
+
+  f32x16 acc[2][NB];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int wm = WBM == 128 ? (wave & 1) * 64 : 0;
+  const int wn = WBM == 128 ? (wave >> 1) * 64 : wave * 32;
+  const int n = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (n > 0) {
+    gload();
+    store(0);
+  }
+  if (n > 1) {
+    gload();
+    store(1);
+  }
+  if (n > 2) gload();
+  __syncthreads();
+  using FR = Frag<T, FBN, 4, 1, 1, WBM, BN>;
+  FR f0, f1;
+  if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
+  int s1 = 1, s2 = 2;
+  auto step = [&](int t, FR &cur, FR &nxt) {
+    if (t + 1 < n) nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    if (t + 2 < n) {
+      store(s2);
+      if (t + 3 < n) gload();
+    }
+    cur.mma(acc);
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
+  auto step_full = [&](FR &cur, FR &nxt) {
+    nxt.load(As[s1], Bs[s1], wm, wn, lane);
+    store(s2);
+    gload();
+    cur.mma(acc);
+    interleave_step<FR::NMFMA, FR::NDSR, NPA + 2, NPA + 2>();
+    s1 = s2;
+    s2 = s2 == ST - 1 ? 0 : s2 + 1;
+    __syncthreads();
+  };
+  int t = 0;
+  if (AVEC && BVEC) {
+    for (; t + 4 < n; t += 2) {
+      step_full(f0, f1);
+      step_full(f1, f0);
+    }
+  }
+  for (; t + 1 < n; t += 2) {
+    step(t, f0, f1);
+    step(t + 1, f1, f0);
+  }
+  if (t < n) step(t, f0, f1);
+
+  const int col = lane & 31;
+  float *out = gridDim.z == 1 ? dw : a.out + (long long)tl.z * a.Co * N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + wm + 32 * i + acc_row(v, lane);
+      if (m >= a.Co) continue;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int nn = n0 + wn + 32 * j + col;
+        if (nn >= N) continue;
+        float *d = out + (long long)m * N + nn;
+        if (gridDim.z == 1) *d = a.overwrite ? acc[i][j][v] : *d + acc[i][j][v];
+        else *d = acc[i][j][v];
+      }
+    }
+}
+
+// dW += (first band: dW =) sum over the split partial sums in a fixed order
+// (deterministic):
+// eight groups of threads each add the splits z = g, g + 8, ... of 32
+// vectors of V elements, then the eight group sums are added in order.
+template <int V>
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, float *dw,
+                                                           long long mn, int splits,
+                                                           int overwrite) {
+  __shared__ float red[8][32 * 4];
+  const int g = threadIdx.x >> 5, e = threadIdx.x & 31;
+  const long long i = ((long long)blockIdx.x * 32 + e) * V;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f}, q[4];
+  if (i < mn) {
+    for (int z = g; z < splits; z += 8) {
+      ldv<float, V>(part + z * mn + i, q);
+#pragma unroll
+      for (int k = 0; k < V; ++k) acc[k] += q[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < V; ++k) red[g][e * 4 + k] = acc[k];
+  __syncthreads();
+  if (g == 0 && i < mn) {
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int gg = 0; gg < 8; ++gg)
+#pragma unroll
+      for (int k = 0; k < V; ++k) sum[k] += red[gg][e * 4 + k];
+    if (overwrite) {
+#pragma unroll
+      for (int k = 0; k < V; ++k) q[k] = sum[k];
+    } else {
+      ldv<float, V>(dw + i, q);
+#pragma unroll
+      for (int k = 0; k < V; ++k) q[k] += sum[k];
+    }
+    stv<float, V>(dw + i, q);
+  }
+}
+
+template <typename T>
+static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
+  WgradArgs a = a0;
+  const int K = a.B * (a.y1 - a.y0) * a.Wv;
+  const int N = a.kh * a.kw * a.Ci;
+  if (K <= 0) return 0;
+  // pixel indices are split by multiply-shift division
+  a.fw = fast_div((uint32_t)a.Wv);
+  a.fr = fast_div((uint32_t)(a.y1 - a.y0));
+  constexpr int BK = Cfg<T>::BK;
+  const WgradTiles wt = wgrad_tiles(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
+  int splits = wt.splits;
+  const int KT = (K + BK - 1) / BK;
+  const int kchunk = (KT + splits - 1) / splits * BK;
+  splits = (K + kchunk - 1) / kchunk;
+  if (!split_fits(splits, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
+  const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
+  const int wbm = wt.rows;
+  dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
+  int pr = -1;
+  if (prof::on)
+    pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
+                         (avec && bvec ? ", vec>" : ", scalar>"),
+                     2.0 * K * a.Co * N, s);
+  if (wbm == 64) {
+    if (avec && bvec) wgrad_kernel<T, 64, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else if (avec) wgrad_kernel<T, 64, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else wgrad_kernel<T, 64, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  } else {
+    if (avec && bvec) wgrad_kernel<T, 128, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else if (avec) wgrad_kernel<T, 128, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else wgrad_kernel<T, 128, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  }
+  prof::end(pr, s);
+  if (splits > 1) {
+    long long mn = (long long)a.Co * N;
+    int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
+    if (mn % 4 == 0)
+      wgrad_reduce_kernel<4><<<(unsigned)((mn / 4 + 31) / 32), 256, 0, s>>>(a.out, dw, mn,
+                                                                            splits, a.overwrite);
+    else
+      wgrad_reduce_kernel<1><<<(unsigned)((mn + 31) / 32), 256, 0, s>>>(a.out, dw, mn, splits,
+                                                                        a.overwrite);
+    prof::end(p2, s);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream) {
+  hipStream_t s = (hipStream_t)stream;
+  return dt == DT_F32 ? wgrad_dispatch<float>(a, dw, s) : wgrad_dispatch<bf16>(a, dw, s);
+}
+
+}  // namespace lrcnn

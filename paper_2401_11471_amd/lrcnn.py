@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(HERE, "liblrcnn.so")
 OP_INPUT, OP_CONV, OP_MAXPOOL, OP_ADD = 0, 1, 2, 3
 F32, BF16 = 0, 1
 CARRY, RECOMPUTE = 0, 1
-EVEN, BALANCED, EXPLICIT = 0, 1, 2
+EVEN, BALANCED, EXPLICIT, PAPER_2PS = 0, 1, 2, 3
 HYBRID_AUTO = -1
 
 STATUS = {0: "OK", -1: "EINVAL", -2: "ESHAPE", -3: "EPARTITION",
@@ -46,7 +46,7 @@ class Config(C.Structure):
                 ("in_w", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
                 ("n_bands", C.c_int32), ("policy", C.c_int32),
                 ("bounds", C.POINTER(C.c_int32)), ("bp_refine", C.c_int32),
-                ("hybrid_from", C.c_int32)]
+                ("hybrid_from", C.c_int32), ("first_rows", C.c_int32)]
 
 
 class PlanInfo(C.Structure):
@@ -183,10 +183,10 @@ class Plan:
 
 
 def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
-               policy=EVEN, bounds=None, bp_refine=1, hybrid_from=0):
+               policy=EVEN, bounds=None, bp_refine=1, hybrid_from=0, first_rows=0):
     arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
     cfg = Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None, bp_refine,
-                 hybrid_from)
+                 hybrid_from, first_rows)
     keep = None
     if bounds is not None:
         keep = (C.c_int32 * len(bounds))(*bounds)
@@ -197,10 +197,10 @@ def lrcnn_plan(nodes, batch, in_c, in_h, in_w, dtype=F32, mode=CARRY, n_bands=1,
 
 
 def _node_cfg(nodes, batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, bp_refine,
-              hybrid_from):
+              hybrid_from, first_rows=0):
     arr = (Node * len(nodes))(*[Node(*nd) for nd in nodes])
     return arr, Config(batch, in_c, in_h, in_w, dtype, mode, n_bands, policy, None,
-                       bp_refine, hybrid_from)
+                       bp_refine, hybrid_from, first_rows)
 
 
 def lrcnn_plan_for_budget(nodes, batch, in_c, in_h, in_w, budget_bytes, dtype=F32,

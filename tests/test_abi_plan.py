@@ -153,11 +153,11 @@ def test_shared_rows_eq12_term():
     assert p.info()["shared_rows"] == 3 * 3 * 2
 
 
-def test_balanced_policy_cuts_largest_band():
-    nodes = vgg16_net()
-    ev = L.lrcnn_plan(nodes, 8, 3, 224, 224, L.F32, L.CARRY, 4, L.EVEN).info()
-    ba = L.lrcnn_plan(nodes, 8, 3, 224, 224, L.F32, L.CARRY, 4, L.BALANCED)
-    assert ba.info()["band_cache_bytes"] < ev["band_cache_bytes"]
+def test_balanced_policy_cuts_the_workspace():
+    nodes = resnet50_net()
+    ev = L.lrcnn_plan(nodes, 16, 3, 224, 224, L.BF16, L.CARRY, 4, L.EVEN).info()
+    ba = L.lrcnn_plan(nodes, 16, 3, 224, 224, L.BF16, L.CARRY, 4, L.BALANCED)
+    assert ba.info()["workspace_bytes"] < ev["workspace_bytes"]
     rows = [ba.band_rows(r, 0) for r in range(4)]
     assert rows[0][0] == 0 and rows[-1][1] == 224
     assert all(rows[i][1] == rows[i + 1][0] for i in range(3))

@@ -153,39 +153,47 @@ def test_layerwise_parity(name, dtype):
     assert_parity(nodes, inp, gpu)
 
 
+SCHEDULES = [("carry_even", dict(mode=L.CARRY, nb=5)),
+             ("carry_balanced", dict(mode=L.CARRY, nb=4, policy=L.BALANCED)),
+             ("carry_paper_2ps", dict(mode=L.CARRY, nb=3, policy=L.PAPER_2PS)),
+             ("carry_refined", dict(mode=L.CARRY, nb=2, bp_refine=3)),
+             ("recompute", dict(mode=L.RECOMPUTE, nb=3))]
+
+
 @pytest.mark.parametrize("dtype", [F32, BF16])
-@pytest.mark.parametrize("name", ["vgg_like", "resnet_like", "wide"])
-def test_row_centric_matches_layerwise(name, dtype):
-    # same kernels; only the split-K grouping of a reduction may differ with
-    # the launch size, so results agree to rounding and every differing
-    # ReLU / argmax decision is a certified near-tie of the oracle
-    from gpu_harness import check_masks, oracle_run
+@pytest.mark.parametrize("name", list(NETS))
+def test_forward_bitwise_equals_layerwise(name, dtype):
+    # every forward launch of a layer sums its K products in the layer's
+    # fixed split-K chunks, whatever band computes the element, so the
+    # row-centric forward output and every ReLU / argmax decision equal the
+    # layer-wise step's bit for bit; gradients agree to rounding
     nodes, inp = _inputs(name, dtype, seed=9)
     lw = gpu_run(nodes, inp, layerwise=True)
-    ref = oracle_run(nodes, inp, lw["g"])
-    tol = 2e-6 if dtype == F32 else 1e-2
-    for mode, nb in ((L.CARRY, 5), (L.RECOMPUTE, 3)):
-        rc = gpu_run(nodes, inp, mode, nb)
-        assert rel(rc["y"], lw["y"]) < tol
-        check_masks(nodes, ref, rc["masks"], dtype, 1e-5 if dtype == F32 else 1e-2)
-        gtol = 1e-5 if dtype == F32 else 1e-2
+    h = inp.x.shape[1]
+    scheds = SCHEDULES + [("carry_empty_bands",
+                           dict(mode=L.CARRY, nb=6, policy=L.EXPLICIT,
+                                bounds=[0, 0, 5, h // 2, h // 2, h - 2, h]))]
+    gtol = 1e-5 if dtype == F32 else 1e-2
+    for label, kw in scheds:
+        print(f"{name} dtype={dtype} {label}", flush=True)
+        rc = gpu_run(nodes, inp, **kw)
+        np.testing.assert_array_equal(rc["y"], lw["y"], err_msg=label)
+        for v, m in lw["masks"].items():
+            np.testing.assert_array_equal(rc["masks"][v], m, err_msg=f"{label} node {v}")
         for v in range(1, len(nodes)):
             if lw["dw"][v] is not None:
-                assert rel(rc["dw"][v], lw["dw"][v]) < gtol
-        assert rel(rc["dx"], lw["dx"]) < gtol
+                assert rel(rc["dw"][v], lw["dw"][v]) < gtol, (label, v)
+        assert rel(rc["dx"], lw["dx"]) < gtol, label
 
 
-def test_forward_is_bitwise_band_invariant_without_splits():
-    # layers too short in K to split: every output element is reduced in the
-    # same order whatever the band, so row-centric forward equals layer-wise
-    # forward bit for bit
-    nodes, inp = _inputs("tiny", F32, seed=21)
-    lw = gpu_run(nodes, inp, layerwise=True)
-    for mode, nb in ((L.CARRY, 4), (L.RECOMPUTE, 3)):
-        rc = gpu_run(nodes, inp, mode, nb)
-        np.testing.assert_array_equal(rc["y"], lw["y"])
-        for v, m in lw["masks"].items():
-            np.testing.assert_array_equal(rc["masks"][v], m)
+@pytest.mark.parametrize("dtype", [F32, BF16])
+@pytest.mark.parametrize("name", ["vgg_like", "odd", "resnet_like"])
+@pytest.mark.parametrize("policy", [L.BALANCED, L.PAPER_2PS])
+def test_partition_policy_parity(name, dtype, policy):
+    # the peak-minimising and the paper's greedy placement (Section IV-A)
+    nodes, inp = _inputs(name, dtype, seed=23)
+    gpu = gpu_run(nodes, inp, L.CARRY, 4, policy)
+    assert_parity(nodes, inp, gpu)
 
 
 def test_weight_gradients_are_deterministic():

@@ -11,7 +11,7 @@ Three passes of the same short bench command, each with one counter group
     rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE \\
         SQ_INSTS_VALU_MFMA_MOPS_F32 SQ_BUSY_CYCLES --output-format csv \\
         -d OUT/mfma -o run -- $B
-    python3 -m paper_2401_11471_amd.traffic --fetch OUT/fetch --write OUT/write \\
+    python3 traffic.py --fetch OUT/fetch --write OUT/write \\
         --mfma OUT/mfma --key cfg2:carry:4
 
 ``--copy-calibration-mib 256`` makes the bench run one plain device copy of
@@ -30,8 +30,7 @@ import os
 import re
 from collections import defaultdict
 
-HERE = os.path.dirname(os.path.abspath(__file__))
-ROOT = os.path.dirname(HERE)
+ROOT = os.path.dirname(os.path.abspath(__file__))
 SIMDS = 256 * 4  # gfx950: 256 CUs x 4 SIMDs
 XCDS = 8
 
