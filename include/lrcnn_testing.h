@@ -4,7 +4,10 @@
 #ifndef LRCNN_TESTING_H
 #define LRCNN_TESTING_H
 
+#include <stddef.h>
 #include <stdint.h>
+
+#include "lrcnn.h"
 
 #ifdef __cplusplus
 extern "C" {
@@ -56,6 +59,17 @@ int lrcnn_debug_profile_collect(void);
  * algorithmic FLOPs. Returns 0, or -1 if i is out of range. */
 int lrcnn_debug_profile_entry(int32_t i, const char **name, int64_t *launches,
                               double *ms, double *flops);
+
+/* Byte offset in the layer-wise workspace of node `node`'s full feature map
+ * ([B][H][W][C], dense, the plan's storage dtype) as
+ * lrcnn_layerwise_reference_gpu leaves it: its forward, which equals
+ * lrcnn_forward_rows of the same plan bit for bit, keeps every map there
+ * for the backward and the maps are unchanged when the call returns.
+ * Errors: EINVAL for a null argument, a node out of range, the input
+ * (node 0, which is x), the output node (which is y) and a convolution
+ * whose value the residual add's forward consumes directly (never
+ * stored). */
+int lrcnn_debug_layerwise_map(const lrcnn_plan_t *plan, int32_t node, size_t *offset);
 
 #ifdef __cplusplus
 }

@@ -1,37 +1,35 @@
-"""Per-site bounds that certify a differing ReLU or max-pool decision.
+"""Certification of ReLU and max-pool decisions that differ from the oracle's.
 
 TEST INFRASTRUCTURE (see ``oracle/column.py``): only ``tests/`` may use it.
 
-The paper states no precision. The parity protocol compares an
-implementation that stores node outputs in float32, or in bfloat16 rounded
-to nearest even at the oracle's emulated rounding points, and sums each
-convolution's products in float32 in any order, with the float64 oracle.
-Its ReLU and argmax decisions can then legitimately differ from the
-oracle's where the oracle's pre-activation (or the gap between two window
-values) lies within the implementation's possible deviation at that site.
+The paper states no precision. An implementation that stores node outputs
+in float32 (or bfloat16, rounded at the oracle's emulated points) and sums
+each convolution's products in float32 in any order reaches its ReLU and
+argmax decisions from its own stored inputs, which differ from the
+oracle's by rounding; a decision can then legitimately differ from the
+oracle's. Such a decision is certified when it is the one the
+implementation's own stored inputs imply, up to the implementation's own
+accumulation error at that site. The bound follows standard floating-point
+error analysis (Higham, "Accuracy and Stability of Numerical Algorithms",
+2nd ed., Section 3.1: a sum of n terms computed in floating point with unit
+roundoff u, in any order, differs from the exact sum by at most gamma_n
+times the sum of the terms' magnitudes, gamma_n = n u / (1 - n u)):
 
-The bound of one site assumes that the stored values the site reads differ
-from the oracle's by at most kappa units of their storage rounding
-(kappa * u * |value|, u = 2^-24 for float32, 2^-8 for bfloat16); the test
-measures kappa on the network output, the deepest and largest deviation.
-Given that, by standard floating-point error analysis (Higham, "Accuracy
-and Stability of Numerical Algorithms", 2nd ed., Section 3.1: a sum of n
-terms computed in floating point with unit roundoff u, in any order,
-differs from the exact sum by at most gamma_n times the sum of the terms'
-magnitudes, gamma_n = n u / (1 - n u)):
+* convolution site with inputs x'_k (the implementation's stored values)
+  and weights w_k, K = kh * kw * C_in products: the exact sum
+  c = sum_k w_k x'_k is computed here in float64 and the implementation's
+  value lies within gamma_{K+1} * sum_k |w_k| |x'_k| of it (gamma's "+1"
+  covers the rounding of each product); a fixed affine a * c + b in float32
+  adds two roundings;
+* residual add of two stored values: their exact sum has the sign the
+  float32 sum has, so the decision must match it exactly; when one input is
+  a convolution whose value the add consumes without storing it, that
+  value's accumulation error and its storage rounding are added;
+* max-pool compares stored values without arithmetic, so the chosen index
+  must be the first maximum of the implementation's own window.
 
-* convolution site, K = kh * kw * C_in products of weights w_k and inputs
-  x_k: |conv' - conv| <= (kappa u_s + gamma_{K+1}(1 + kappa u_s)) S,
-  S = sum_k |w_k| |x_k| (gamma's "+1" covers the rounding of each product);
-* fixed affine a * c + b in float32: |a| times that, plus two roundings;
-* residual add z_a + z_b in float32: kappa u_s (|z_a| + |z_b|) plus one
-  rounding;
-* max-pool: window values x_i, x_j each within kappa u_s of their own
-  magnitude.
-
-A ReLU decision may differ only where |t| <= E_t; an argmax may differ
-only where the oracle's maximum x_i and the implementation's choice x_j
-satisfy x_i - x_j <= kappa u_s (|x_i| + |x_j|).
+A decision is certified when it equals the sign (ReLU) of the exact value
+from the implementation's inputs or that value lies within the bound.
 """
 from __future__ import annotations
 
@@ -53,71 +51,86 @@ def unit(bf16):
     return UBF16 if bf16 else U32
 
 
-def conv_abs_at(x, w, sh, sw, ph, pw, sites):
-    """S = sum over taps and input channels of |w[o, i, j, c]| * |x[b, y*sh -
-    ph + i, x*sw - pw + j, c]| at the given output sites (rows of
-    (b, y, x, o)); positions outside the image contribute nothing."""
+def _taps_at(x, w, sh, sw, ph, pw, sites, absolute):
     sites = np.asarray(sites).reshape(-1, 4)
-    b_, h, wd, c = x.shape
-    co, kh, kw, ci = w.shape
     out = np.zeros(len(sites))
     if len(sites) == 0:
         return out
+    h, wd = x.shape[1:3]
+    co, kh, kw, ci = w.shape
     b, y, xx, o = (sites[:, k] for k in range(4))
-    aw = np.abs(np.asarray(w, dtype=np.float64))
+    ww = np.asarray(w, dtype=np.float64)
+    if absolute:
+        ww = np.abs(ww)
     for i in range(kh):
         for j in range(kw):
             sy, sx = y * sh - ph + i, xx * sw - pw + j
             ok = (sy >= 0) & (sy < h) & (sx >= 0) & (sx < wd)
-            v = np.abs(x[b, np.clip(sy, 0, h - 1), np.clip(sx, 0, wd - 1), :].astype(np.float64))
-            out += np.where(ok, np.einsum("nc,nc->n", v, aw[o, i, j, :]), 0.0)
+            v = x[b, np.clip(sy, 0, h - 1), np.clip(sx, 0, wd - 1), :].astype(np.float64)
+            if absolute:
+                v = np.abs(v)
+            out += np.where(ok, np.einsum("nc,nc->n", v, ww[o, i, j, :]), 0.0)
     return out
 
 
-def conv_site_bound(S, K, t, scale, shift, o, kappa, bf16):
-    """Bound E_t on |t' - t| at convolution sites with S (conv_abs_at), K
-    products each, pre-activations t and output channels o."""
-    us = unit(bf16)
-    d = (kappa * us + gamma(K + 1) * (1.0 + kappa * us)) * S
-    if scale is None:
-        return d
-    a = np.abs(np.asarray(scale, dtype=np.float64))[o]
-    bb = np.abs(np.asarray(shift, dtype=np.float64))[o]
-    ac = np.abs(t - np.asarray(shift, dtype=np.float64)[o])
-    return a * d + 2.0 * U32 * (ac + a * d + bb)
+def conv_at(x, w, sh, sw, ph, pw, sites):
+    """Exact (float64) sum_{i,j,c} w[o,i,j,c] x[b, y*sh - ph + i, x*sw - pw + j, c]
+    at output sites (rows of (b, y, x, o)); outside the image nothing is
+    added (zero padding)."""
+    return _taps_at(x, w, sh, sw, ph, pw, sites, False)
 
 
-def add_site_bound(za, zb, t, kappa, bf16):
-    """Bound E_t on |t' - t| of a residual add t = z_a + z_b at its sites."""
-    e = kappa * unit(bf16) * (np.abs(za) + np.abs(zb))
-    return e + U32 * (np.abs(t) + e)
+def conv_abs_at(x, w, sh, sw, ph, pw, sites):
+    """The same sum of |w| |x| (the magnitude the accumulation bound scales)."""
+    return _taps_at(x, w, sh, sw, ph, pw, sites, True)
 
 
-def relu_flips(t, gpu_mask):
-    """Sites (b, y, x, c) where the implementation's ReLU decision
-    (gpu_mask != 0) differs from the oracle's (t > 0)."""
-    return np.argwhere((gpu_mask != 0) != (t > 0))
-
-
-def argmax_flips(node, z_in, oracle_idx, gpu_idx, kappa, bf16):
-    """(differing argmax decisions, of which not certified) of a max-pool
-    node: the oracle's maximum x_i and the implementation's choice x_j may
-    differ only where x_i - x_j <= kappa u_s (|x_i| + |x_j|)."""
+def conv_site(x, w, scale, shift, node, sites):
+    """(t, E) at conv sites: t the exact pre-activation from inputs x (the
+    affine applied in float64), E the bound on the implementation's float32
+    accumulation and affine rounding."""
     op, in0, in1, co, kh, kw, sh, sw, ph, pw, aff, rl = node
-    diff = gpu_idx != oracle_idx
-    if not diff.any():
-        return 0, 0
-    h, w = z_in.shape[1:3]
-    bb, yy, xx, cc = np.nonzero(diff)
+    sites = np.asarray(sites).reshape(-1, 4)
+    c = conv_at(x, w, sh, sw, ph, pw, sites)
+    S = conv_abs_at(x, w, sh, sw, ph, pw, sites)
+    E = gamma(kh * kw * x.shape[3] + 1) * S
+    if not aff:
+        return c, E
+    o = sites[:, 3]
+    a = np.asarray(scale, dtype=np.float64)[o]
+    b = np.asarray(shift, dtype=np.float64)[o]
+    t = a * c + b
+    return t, np.abs(a) * E + 2.0 * U32 * (np.abs(a * c) + np.abs(a) * E + np.abs(b))
 
-    def at(idx):
-        iy = yy * sh - ph + idx[bb, yy, xx, cc] // kw
-        ix = xx * sw - pw + idx[bb, yy, xx, cc] % kw
-        ok = (iy >= 0) & (iy < h) & (ix >= 0) & (ix < w)
-        v = z_in[bb, np.clip(iy, 0, h - 1), np.clip(ix, 0, w - 1), cc].astype(np.float64)
-        return np.where(ok, v, -np.inf)
 
-    xi, xj = at(oracle_idx), at(gpu_idx)
-    with np.errstate(invalid="ignore"):
-        bad = ~(xi - xj <= kappa * unit(bf16) * (np.abs(xi) + np.abs(xj)))
-    return int(diff.sum()), int(bad.sum())
+def fused_conv_value_bound(t, E, bf16):
+    """Bound on |r' - t| for the stored (rounded) value r' of a conv whose
+    exact value from the implementation's inputs is t, known within E."""
+    return E + unit(bf16) * (np.abs(t) + E)
+
+
+def relu_certified(t, E, decision):
+    """Decisions (bool) at sites with exact values t and bounds E that are
+    certified: equal to t > 0, or |t| <= E."""
+    return (decision == (t > 0)) | (np.abs(t) <= E)
+
+
+def pool_first_max_violations(node, z, idx):
+    """Number of max-pool outputs whose index (row-major in the window) is
+    not the first maximum of window values z (-inf padding)."""
+    op, in0, in1, co, kh, kw, sh, sw, ph, pw, aff, rl = node
+    b_, ho, wo, c_ = idx.shape
+    h, w = z.shape[1:3]
+    best = np.full(idx.shape, -np.inf)
+    first = np.zeros(idx.shape, np.int64)
+    for i in range(kh):
+        for j in range(kw):
+            yy = np.arange(ho)[None, :, None, None] * sh - ph + i
+            xx = np.arange(wo)[None, None, :, None] * sw - pw + j
+            ok = (yy >= 0) & (yy < h) & (xx >= 0) & (xx < w)
+            v = np.where(ok, z[:, np.clip(yy[0, :, 0, 0], 0, h - 1)][:, :,
+                                np.clip(xx[0, 0, :, 0], 0, w - 1)], -np.inf)
+            better = v > best
+            best = np.where(better, v, best)
+            first = np.where(better, i * kw + j, first)
+    return int((first != idx).sum())

@@ -1057,6 +1057,18 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
   return run.finish_dw(dw);
 }
 
+extern "C" int lrcnn_debug_layerwise_map(const lrcnn_plan_t *plan, int32_t node,
+                                         size_t *offset) {
+  if (!plan || !offset) return lrcnn_fail(LRCNN_EINVAL, "null argument");
+  const Plan &P = *reinterpret_cast<const Plan *>(plan);
+  if (node <= 0 || node >= P.n) return lrcnn_fail(LRCNN_EINVAL, "node out of range or input");
+  if (node == P.n - 1 && !P.lw_keep_out)
+    return lrcnn_fail(LRCNN_EINVAL, "the output node's map is y");
+  if (P.fz_lw.fwd[node]) return lrcnn_fail(LRCNN_EINVAL, "map consumed by a fused add");
+  *offset = P.lw.win[node];
+  return LRCNN_OK;
+}
+
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
 extern "C" void lrcnn_debug_act_fusion(int on) { lrcnn::g_no_act_fusion = on == 0; }
 extern "C" void lrcnn_debug_fp_pipeline(int on) { lrcnn::g_no_fp_pipe = on == 0; }

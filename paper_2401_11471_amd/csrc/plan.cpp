@@ -340,6 +340,10 @@ static constexpr size_t kPartCap = (size_t)LRCNN_PART_MIB << 20;
 // at every row-centric launch.
 static void forward_splits(Plan &P,
                            const std::vector<const std::vector<std::vector<Rows>> *> &tabs) {
+  if ((int)P.fsplit_fixed.size() == P.n) {
+    P.fsplit = P.fsplit_fixed;
+    return;
+  }
   P.fsplit.assign(P.n, 0);
   const long long B = P.cfg.batch;
   for (int v = 1; v < P.n; ++v) {
@@ -892,6 +896,7 @@ static int build_hybrid(Plan &P, bool quiet = false) {
   if (st != LRCNN_OK) return st;
   P.row->no_keep = true;
   P.row->dy_f32 = true;
+  P.row->fsplit_fixed.assign(P.fsplit.begin(), P.fsplit.begin() + k);
   st = build(*P.row);
   P.row->cfg.bounds = nullptr;
   if (st != LRCNN_OK) return st;
@@ -913,6 +918,8 @@ static int build_hybrid(Plan &P, bool quiet = false) {
   }
   if ((st = sub(cn, cc, P.col)) != LRCNN_OK) return st;
   P.col->lw_keep_out = true;
+  P.col->fsplit_fixed.assign(1 + n - k, 0);
+  for (int v = k; v < n; ++v) P.col->fsplit_fixed[v - c] = P.fsplit[v];
   if ((st = build(*P.col)) != LRCNN_OK) return st;
   P.hyb = k;
   P.h_col = P.row->rc.ubase;

@@ -92,6 +92,9 @@ struct Plan {
   // bands, recompute and layer-wise alike), so each output element sums
   // its K products in the same order in every schedule (0: not a conv)
   std::vector<int> fsplit;
+  // hybrid parts: the whole plan's counts for their nodes (so the hybrid's
+  // forward equals the whole plan's layer-wise forward bit for bit)
+  std::vector<int> fsplit_fixed;
   Layout rc;                           // row-centric workspace
   Layout lw;                           // layer-wise workspace
   double tau = 0, flops_rows = 0;

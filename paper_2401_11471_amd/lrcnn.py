@@ -115,6 +115,8 @@ def _load():
                                               C.POINTER(C.c_int64),
                                               C.POINTER(C.c_double), C.POINTER(C.c_double)]
     lib.lrcnn_debug_profile_entry.restype = C.c_int
+    lib.lrcnn_debug_layerwise_map.argtypes = [vp, i32, C.POINTER(sz)]
+    lib.lrcnn_debug_layerwise_map.restype = C.c_int
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
               "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
               "lrcnn_layerwise_reference_gpu", "lrcnn_plan_step_bytes",
@@ -135,7 +137,8 @@ EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_debug_dry_run", "lrcnn_debug_fp_pipeline", "lrcnn_debug_act_fusion",
            "lrcnn_debug_dgrad_phases",
            "lrcnn_debug_profile",
-           "lrcnn_debug_profile_collect", "lrcnn_debug_profile_entry")
+           "lrcnn_debug_profile_collect", "lrcnn_debug_profile_entry",
+           "lrcnn_debug_layerwise_map")
 
 
 def _check(code):
@@ -334,3 +337,11 @@ def lrcnn_debug_profile_collect():
         LIB.lrcnn_debug_profile_entry(i, C.byref(nm), C.byref(la), C.byref(ms), C.byref(fl))
         out[nm.value.decode()] = (la.value, ms.value, fl.value)
     return out
+
+
+def lrcnn_debug_layerwise_map(plan, node):
+    """Test hook: byte offset of node's full map in the layer-wise workspace,
+    or None where the map is not stored there (input, output, fused conv)."""
+    out = C.c_size_t()
+    code = LIB.lrcnn_debug_layerwise_map(plan.handle, node, C.byref(out))
+    return out.value if code == 0 else None

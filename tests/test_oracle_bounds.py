@@ -1,16 +1,17 @@
-"""Pins of ``oracle/bounds.py``, the per-site bounds that certify a
-differing ReLU / argmax decision.
+"""Pins of ``oracle/bounds.py``, the certification of a ReLU / argmax
+decision from an implementation's own stored inputs.
 
-* ``conv_abs_at`` equals the oracle convolution of |x| with |w| at every
-  site (brute-force agreement with ``column.conv_fwd``).
-* The bounds hold for float32 implementations written here independently
-  of the oracle: one convolution layer computed by torch's CPU float32
-  convolution (its own summation order) and by a float32 tap loop in
-  reverse tap order, on inputs perturbed by up to kappa units of their
-  storage rounding, stays within E_t of the float64 pre-activation at
-  every site; so does a float32 residual add; every ReLU or argmax
-  decision such an implementation flips is certified.
-* A planted mistake (one weight off by 2%) breaks the bound.
+* ``conv_at`` and ``conv_abs_at`` equal the oracle convolution of x with w
+  and of |x| with |w| at every site.
+* Float32 implementations written here independently of the oracle --
+  torch's CPU float32 convolution (its own summation order) and a float32
+  tap loop in reverse tap order -- stay within the accumulation bound E of
+  the exact pre-activation from the same inputs at every site, in float32
+  and bfloat16 storage; every decision they reach is certified. A planted
+  mistake (one weight off by 2%) breaks the bound.
+* A bfloat16-stored convolution value added to another stored value stays
+  within the fused-value bound.
+* The max-pool check accepts exactly the first maximum of the window.
 """
 import numpy as np
 import pytest
@@ -21,11 +22,6 @@ from oracle import bounds as OB, column as C
 from oracle.bf16 import round_bf16
 
 rng = np.random.default_rng(42)
-
-
-def perturb(x, kappa, bf16):
-    u = OB.unit(bf16)
-    return x * (1 + rng.uniform(-kappa * u, kappa * u, x.shape))
 
 
 def conv32(x, w, s, p, kind):
@@ -51,81 +47,76 @@ def all_sites(shape):
     return np.argwhere(np.ones(shape, bool))
 
 
-def test_conv_abs_at_matches_convolution_of_magnitudes():
+def test_site_sums_match_convolutions():
     x, w = rng.standard_normal((2, 9, 7, 5)), rng.standard_normal((4, 3, 3, 5))
+    ref = C.conv_fwd(x, w, 2, 2, 1, 1)
+    sites = all_sites(ref.shape)
+    np.testing.assert_allclose(OB.conv_at(x, w, 2, 2, 1, 1, sites).reshape(ref.shape), ref,
+                               rtol=1e-12, atol=1e-12)
     ref = C.conv_fwd(np.abs(x), np.abs(w), 2, 2, 1, 1)
-    got = OB.conv_abs_at(x, w, 2, 2, 1, 1, all_sites(ref.shape)).reshape(ref.shape)
-    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(OB.conv_abs_at(x, w, 2, 2, 1, 1, sites).reshape(ref.shape),
+                               ref, rtol=1e-13, atol=0)
 
 
 @pytest.mark.parametrize("bf16", [False, True])
 @pytest.mark.parametrize("kind", ["torch", "taps_reversed"])
-@pytest.mark.parametrize("kappa", [1, 4])
-def test_conv_site_bound_holds_for_float32_layers(bf16, kind, kappa):
-    x = rng.standard_normal((2, 11, 9, 24))
-    w = rng.standard_normal((16, 3, 3, 24)) * np.sqrt(2 / 216)
+@pytest.mark.parametrize("aff", [0, 1])
+def test_float32_layers_stay_within_the_accumulation_bound(bf16, kind, aff):
+    x = rng.standard_normal((2, 11, 9, 24)).astype(np.float32).astype(np.float64)
+    w = (rng.standard_normal((16, 3, 3, 24)) * np.sqrt(2 / 216)).astype(np.float32)
+    w = w.astype(np.float64)
     if bf16:
         x, w = round_bf16(x), round_bf16(w)
-    scale, shift = rng.uniform(0.5, 1, 16), rng.uniform(-0.1, 0.1, 16)
-    t = C.conv_fwd(x, w, 1, 1, 1, 1) * scale + shift
-    xp = perturb(x, kappa, bf16)
-    t32 = (conv32(xp, w, 1, 1, kind) * scale.astype(np.float32)
-           + shift.astype(np.float32)).astype(np.float32)
-    sites = all_sites(t.shape)
-    S = OB.conv_abs_at(x, w, 1, 1, 1, 1, sites).reshape(t.shape)
-    o = np.broadcast_to(np.arange(16), t.shape)
-    # (the float32 copy of a perturbed input adds one more rounding)
-    Et = OB.conv_site_bound(S, 216, t, scale, shift, o, kappa + 1, bf16)
-    assert (np.abs(t32 - t) <= Et).all()
-    flips = OB.relu_flips(t, (t32 > 0).astype(np.uint8))
-    for b, y, xx, c in flips:
-        assert abs(t[b, y, xx, c]) <= Et[b, y, xx, c]
-    # not vacuous: the bound is a small part of the values' spread
-    assert np.median(Et) < 0.2 * np.std(t)
+    scale = rng.uniform(0.5, 1, 16).astype(np.float32) if aff else None
+    shift = rng.uniform(-0.1, 0.1, 16).astype(np.float32) if aff else None
+    node = (1, 0, -1, 16, 3, 3, 1, 1, 1, 1, aff, 1)
+    out = conv32(x, w, 1, 1, kind)
+    if aff:
+        out = (out * scale + shift).astype(np.float32)
+    sites = all_sites(out.shape)
+    t, E = OB.conv_site(x, w, scale, shift, node, sites)
+    t, E = t.reshape(out.shape), E.reshape(out.shape)
+    assert (np.abs(out.astype(np.float64) - t) <= E).all()
+    assert OB.relu_certified(t, E, out > 0).all()
+    assert np.median(E) < 1e-3 * np.std(t)  # the bound is tight enough to matter
 
 
-def test_planted_mistake_breaks_the_conv_bound():
-    x = rng.standard_normal((1, 8, 8, 16))
-    w = rng.standard_normal((8, 3, 3, 16)) * np.sqrt(2 / 144)
-    t = C.conv_fwd(x, w, 1, 1, 1, 1)
+def test_planted_mistake_breaks_the_bound():
+    x = rng.standard_normal((1, 8, 8, 16)).astype(np.float32).astype(np.float64)
+    w = (rng.standard_normal((8, 3, 3, 16)) * np.sqrt(2 / 144)).astype(np.float32)
+    w = w.astype(np.float64)
     wbad = w.copy()
     wbad[0, 1, 1, 0] *= 1.02
-    t32 = conv32(x, wbad, 1, 1, "torch")
-    S = OB.conv_abs_at(x, w, 1, 1, 1, 1, all_sites(t.shape)).reshape(t.shape)
-    o = np.broadcast_to(np.arange(8), t.shape)
-    Et = OB.conv_site_bound(S, 144, t, None, None, o, 1, False)
-    assert (np.abs(t32 - t) > Et).any()
+    out = conv32(x, wbad, 1, 1, "torch")
+    node = (1, 0, -1, 8, 3, 3, 1, 1, 1, 1, 0, 1)
+    t, E = OB.conv_site(x, w, None, None, node, all_sites(out.shape))
+    assert (np.abs(out.ravel().astype(np.float64) - t) > E).any()
 
 
-@pytest.mark.parametrize("bf16", [False, True])
-def test_add_site_bound_holds(bf16):
-    za, zb = rng.standard_normal((3, 50)), rng.standard_normal((3, 50))
-    if bf16:
-        za, zb = round_bf16(za), round_bf16(zb)
-    t = za + zb
-    t32 = (perturb(za, 2, bf16).astype(np.float32) + perturb(zb, 2, bf16).astype(np.float32))
-    # perturbed by 2 units, plus the float32 copy's rounding
-    assert (np.abs(t32 - t) <= OB.add_site_bound(za, zb, t, 3, bf16)).all()
+def test_fused_conv_value_plus_stored_input():
+    x = round_bf16(rng.standard_normal((2, 6, 5, 32)))
+    w = round_bf16(rng.standard_normal((16, 1, 1, 32)) * 0.25)
+    zb = round_bf16(rng.standard_normal((2, 6, 5, 16)))
+    scale = rng.uniform(0.5, 1, 16).astype(np.float32)
+    shift = rng.uniform(-0.1, 0.1, 16).astype(np.float32)
+    node = (1, 0, -1, 16, 1, 1, 1, 1, 0, 0, 1, 0)
+    c32 = (conv32(x, w, 1, 0, "torch") * scale + shift).astype(np.float32)
+    stored = round_bf16(c32.astype(np.float64))
+    t_impl = (stored.astype(np.float32) + zb.astype(np.float32)).astype(np.float64)
+    sites = all_sites(c32.shape)
+    t, E = OB.conv_site(x, w, scale, shift, node, sites)
+    e = OB.fused_conv_value_bound(t, E, True).reshape(c32.shape)
+    t = t.reshape(c32.shape)
+    tot = t + zb
+    assert (np.abs(t_impl - tot) <= e + OB.U32 * (np.abs(tot) + e)).all()
 
 
-def test_argmax_certification():
-    node = (2, 0, -1, 0, 2, 2, 2, 2, 0, 0, 0, 0)
-    z = np.array([[[[1.0], [1.0 + 1e-6]], [[0.0], [0.5]]]])  # one 2x2 window
-    oracle_idx = np.array([[[[1]]]], np.uint8)
-    assert OB.argmax_flips(node, z, oracle_idx, np.array([[[[0]]]], np.uint8), 1, False) == (1, 1)
-    assert OB.argmax_flips(node, z, oracle_idx, np.array([[[[0]]]], np.uint8), 1, True) == (1, 0)
-    assert OB.argmax_flips(node, z, oracle_idx, np.array([[[[3]]]], np.uint8), 4, True) == (1, 1)
-    assert OB.argmax_flips(node, z, oracle_idx, oracle_idx, 1, True) == (0, 0)
-
-
-@pytest.mark.parametrize("bf16", [False, True])
-def test_pool_flips_of_perturbed_values_are_certified(bf16):
+def test_pool_first_maximum():
     node = (2, 0, -1, 0, 3, 3, 2, 2, 1, 1, 0, 0)
     z = rng.standard_normal((2, 15, 13, 8))
-    z = np.where(rng.random(z.shape) < 0.3, 0.0, z)  # ReLU-like zeros tie
-    if bf16:
-        z = round_bf16(z)
-    _, oi = C.maxpool_fwd(z, 3, 3, 2, 2, 1, 1)
-    _, gi = C.maxpool_fwd(perturb(z, 2, bf16), 3, 3, 2, 2, 1, 1)
-    n, bad = OB.argmax_flips(node, z, oi, gi, 2, bf16)
-    assert bad == 0
+    z = np.where(rng.random(z.shape) < 0.4, 0.0, z)  # ties between zeros
+    _, idx = C.maxpool_fwd(z, 3, 3, 2, 2, 1, 1)
+    assert OB.pool_first_max_violations(node, z, idx) == 0
+    bad = idx.copy()
+    bad[1, 2, 3, 4] = (bad[1, 2, 3, 4] + 1) % 9
+    assert OB.pool_first_max_violations(node, z, bad) == 1
