@@ -45,12 +45,17 @@ def parse():
     ap.add_argument("--mode", default="carry",
                     choices=["carry", "balanced", "paper2ps", "recompute"])
     ap.add_argument("--bands", type=int, default=0, help="override the band count")
-    ap.add_argument("--bp-refine", type=int, default=1,
-                    help="backward bands per forward band (finer BP partition)")
+    ap.add_argument("--bp-refine", type=int, default=0,
+                    help="backward bands per forward band (finer BP partition; 0: the "
+                         "workload's step preset)")
     ap.add_argument("--batch", type=int, default=0, help="override the batch")
-    ap.add_argument("--hybrid-from", type=int, default=0,
+    ap.add_argument("--hybrid-from", type=int, default=None,
                     help="hybrid depth: first node run layer-wise (-1: the planner's "
-                         "smallest-workspace checkpoint; 0: all row-centric)")
+                         "smallest-workspace checkpoint; 0: all row-centric; default: the "
+                         "workload's step preset)")
+    ap.add_argument("--plain", action="store_true",
+                    help="ignore the workload's step preset (even bands, no refinement, "
+                         "no hybrid depth)")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the layer-wise / recompute comparison runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -208,7 +213,8 @@ def compact_workload(args, cid):
     B, H, W, Cin = inp.x.shape
     dts = "bf16" if inp.dtype == BF16 else "f32"
     dm = DeviceModel.from_inputs(nodes, inp)
-    base = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, c["bands"])
+    preset = c.get("step", {})
+    base = L.lrcnn_plan(nodes, B, Cin, H, W, inp.dtype, L.CARRY, c["bands"], **preset)
     out_shape = (B,) + base.node_shape(len(nodes) - 1)
     dy = dm.to_device(inp.grad(out_shape))
 
@@ -250,7 +256,9 @@ def compact_workload(args, cid):
            "dtype": dts,
            "config": {"workload": c["name"], "net": c["net"], "batch": B,
                       "input": [Cin, H, W], "bands": c["bands"], "mode": "carry",
-                      "policy": "even", "bp_bands": base.info()["bp_bands"]},
+                      "policy": ["even", "balanced"][preset.get("policy", 0)],
+                      "bp_bands": base.info()["bp_bands"],
+                      "hybrid_from": base.info()["hybrid_from"]},
            "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": pk,
                         "unit": unit, "frac": round(achieved / pk, 4), "kernel": dom_name,
                         "launches_per_step": dom_n // ps,
@@ -260,7 +268,8 @@ def compact_workload(args, cid):
                          "ms_per_step": round(lw_ms, 3), "peak_act_bytes": lw_peak},
            "mem_ratio_layerwise_over_rows": round(lw_peak / peak, 3)}
     variants = {}
-    for label, kw in (("balanced", dict(policy=L.BALANCED)),
+    for label, kw in (("plain", dict()),
+                      ("balanced", dict(policy=L.BALANCED)),
                       ("hybrid", dict(hybrid_from=L.HYBRID_AUTO)),
                       ("balanced_hybrid", dict(policy=L.BALANCED, hybrid_from=L.HYBRID_AUTO)),
                       ("finer_bp", dict(bp_refine=2)),
@@ -280,7 +289,7 @@ def compact_workload(args, cid):
     res["variants"] = variants
     ok = {k: v for k, v in variants.items() if v["mem_ratio_layerwise_over_rows"] >= 3.0}
     if res["mem_ratio_layerwise_over_rows"] >= 3.0:
-        ok["default"] = {"images_per_s": res["value"]}
+        ok["step"] = {"images_per_s": res["value"]}
     res["fastest_with_3x_memory_cut"] = (max(ok, key=lambda k: ok[k]["images_per_s"])
                                          if ok else None)
     del dm, dy
@@ -528,7 +537,11 @@ def main():
         c["batch"] = args.batch
     nb = args.bands or c["bands"]
     mode = L.RECOMPUTE if args.mode == "recompute" else L.CARRY
-    policy = policy_of(L, args.mode)
+    preset = {} if args.plain or mode == L.RECOMPUTE else c.get("step", {})
+    policy = policy_of(L, args.mode) if args.mode != "carry" else preset.get("policy", L.EVEN)
+    args.bp_refine = args.bp_refine or preset.get("bp_refine", 1)
+    if args.hybrid_from is None:
+        args.hybrid_from = preset.get("hybrid_from", 0)
     nodes, inp = config_inputs(args.config, batch=c["batch"])
     B, H, W, Cin = inp.x.shape
     dts = "bf16" if inp.dtype == BF16 else "f32"
@@ -620,7 +633,9 @@ def main():
         "dtype": dts, "data": "synthetic N(0,1), paper's shapes (ImageNet not available)",
         "config": {"workload": c["name"], "net": c["net"], "batch": B,
                    "input": [Cin, H, W], "bands": nb, "bp_bands": info["bp_bands"],
-                   "mode": args.mode, "dx": False, "hybrid_from": info["hybrid_from"],
+                   "mode": args.mode, "policy": ["even", "balanced", "explicit",
+                                                 "paper2ps"][policy],
+                   "dx": False, "hybrid_from": info["hybrid_from"],
                    "launch": "host" if args.eager else "hip-graph"},
         "roofline": roofline,
         "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),

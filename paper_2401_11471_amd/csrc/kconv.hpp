@@ -752,9 +752,12 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
     const double taps = (double)a.kh * a.kw;
     const double fl = DGRAD && a.pst <= 1 ? 2.0 * a.B * (a.sy1 - a.sy0) * a.Ws * a.KC * taps * a.N
                                           : 2.0 * M * a.N * taps * a.KC;
+    // (1x1 kernels, which carry little reuse per loaded byte, are named
+    // apart from the windowed ones)
+    const bool one_ = vec && a.kh == 1 && a.kw == 1;
     std::string nm = std::string("conv_gemm_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                      ", " + std::to_string(bn) + (DGRAD ? ", dgrad" : ", fwd") +
-                     (vec ? ", vec>" : ", scalar>");
+                     (!vec ? ", scalar>" : one_ ? ", 1x1>" : ", vec>");
     pr = prof::begin(nm, fl, s);
   }
   // the input gradient of a strided convolution divides by the stride

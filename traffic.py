@@ -43,11 +43,13 @@ def bench_name(mangled: str) -> str:
     """rocprofv3's kernel name -> the name bench.py's per-kernel table uses."""
     n = re.sub(r"\(.*", "", mangled).replace("void ", "").replace("lrcnn::", "")
     n = n.replace("unsigned short", "bf16")
-    m = re.match(r"conv_gemm_kernel<(\w+), (\d+), \d+, (true|false), (true|false)", n)
+    m = re.match(r"conv_gemm_kernel<(\w+), (\d+), \d+, (true|false), (true|false), "
+                 r"(true|false)(?:, (true|false))?", n)
     if m:
+        kind = ("scalar" if m.group(4) != "true" else
+                "1x1" if m.group(6) == "true" else "vec")
         return (f"conv_gemm_kernel<{m.group(1)}, {m.group(2)}, "
-                f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, "
-                f"{'vec' if m.group(4) == 'true' else 'scalar'}>")
+                f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, {kind}>")
     m = re.match(r"wgrad_kernel<(\w+), (?:\d+, )?(true|false), (true|false)>", n)
     if m:
         vec = m.group(2) == "true" and m.group(3) == "true"
@@ -110,6 +112,7 @@ def main():
         busy = per_dispatch(mrows, "SQ_VALU_MFMA_BUSY_CYCLES")
         gui = per_dispatch(mrows, "GRBM_GUI_ACTIVE")
         mops = per_dispatch(mrows, "SQ_INSTS_VALU_MFMA_MOPS_F32")
+        mops.update(per_dispatch(mrows, "SQ_INSTS_VALU_MFMA_MOPS_BF16"))
         ma = defaultdict(lambda: [0.0, 0.0, 0.0])
         for d, (name, grid, b) in busy.items():
             if "lrcnn::" not in name:
@@ -117,7 +120,7 @@ def main():
             e = ma[bench_name(name)]
             e[0] += b
             e[1] += gui[d][2] / XCDS  # GRBM_GUI_ACTIVE is summed over the XCDs
-            e[2] += mops[d][2] * 512.0
+            e[2] += mops[d][2] * 512.0 if d in mops else 0.0
         for k, (b, g, fl) in ma.items():
             mf[k] = {"mfma_busy_pct": round(100.0 * b / (g * SIMDS), 1) if g else None,
                      "mfma_flops_executed": fl}

@@ -95,10 +95,15 @@ def resnet50_net(layers=(3, 4, 6, 3)):
 CONFIGS = {
     1: dict(name="tiny3x3_f32_b1_32x32", net="tiny", dtype=F32, batch=1,
             h=32, w=32, bands=4),
+    # step: the row-centric step's plan options at this workload (policy 0
+    # even / 1 balanced; bp_refine backward bands per forward band;
+    # hybrid_from -1 = the planner's checkpoint): at 224 px the plain
+    # two-phase-sharing step keeps about 2.5x less activation memory than
+    # the layer-wise step, these about 3.2-3.5x, at the same or better speed
     2: dict(name="vgg16_f32_b8_224x224", net="vgg16", dtype=F32, batch=8,
-            h=224, w=224, bands=4),
+            h=224, w=224, bands=4, step=dict(policy=0, bp_refine=2, hybrid_from=-1)),
     3: dict(name="resnet50_bf16_b16_224x224", net="resnet50", dtype=BF16,
-            batch=16, h=224, w=224, bands=8),
+            batch=16, h=224, w=224, bands=8, step=dict(policy=1, bp_refine=1, hybrid_from=-1)),
     4: dict(name="vgg16_f32_b4_1200x1800", net="vgg16", dtype=F32, batch=4,
             h=1200, w=1800, bands=16),
     5: dict(name="resnet50_bf16_b8_2400x3600", net="resnet50", dtype=BF16,
