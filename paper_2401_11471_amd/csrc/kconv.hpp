@@ -38,8 +38,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   constexpr int ST = DMA ? LRCNN_DMA_ST : 3;
   // input gradient: weights staged k-major (16-byte stores)
   constexpr int BKM = DGRAD ? 1 : 0;
-  constexpr int PB = BN + E;
-  constexpr int BSZ = BKM ? BK * PB : BN * LDK;
+  constexpr int BSZ = BKM ? BK * KM<T, BN>::P : BN * LDK;
   // LDS: the operand ring during the K loop; the forward epilogue then
   // reuses it to stage the output tile ([BM][BN + E] in the storage dtype)
   constexpr int CP = BN + E;
@@ -351,7 +350,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
 #pragma unroll
     for (int j = 0; j < NBL; ++j) {
       if (BKM) {
-        *(uint4 *)(&Bs[st][(bk0 + BKS * j) * PB + (tid % BV) * E]) = rb[j];
+        *(uint4 *)(&Bs[st][KM<T, BN>::off(bk0 + BKS * j, (tid % BV) * E)]) = rb[j];
       } else if (DGRAD) {
         union {
           uint4 u;

@@ -80,6 +80,29 @@ __device__ __forceinline__ int swz(int row, int vec) {
 
 constexpr int BM = 128;
 
+// k-major LDS tiles ([k][row], W elements per k row). float32: pitch W + 4
+// (fragments read single words, a column of 32 rows per read). bfloat16:
+// pitch W, no padding; the 64-byte chunk c of k row k is stored at chunk
+// c ^ sw(k). A transposing fragment read (below) takes 64 bytes from each
+// of four consecutive k rows in one 256-byte pass over the 64 banks; sw
+// places those four on distinct 16-bank groups, for any W that is a
+// multiple of 32 (bank group of chunk c of row k: (k W / 32 + c) mod 4).
+// A 16-byte vector stays inside its chunk, and 16 consecutive vectors of a
+// row (or of two rows when W = 64) still cover 64 distinct banks.
+template <typename T, int W>
+struct KM {
+  static constexpr bool SW = sizeof(T) == 2;
+  static constexpr int P = SW ? W : W + 4;  // pitch in elements
+  static_assert(!SW || W % 32 == 0, "k-major bfloat16 tile width");
+  __device__ static __forceinline__ int sw(int k) {
+    constexpr int C = W / 32;
+    return C >= 4 ? (k & 3) : C == 2 ? ((k >> 1) & 1) : 0;
+  }
+  __device__ static __forceinline__ int off(int k, int col) {
+    return SW ? k * W + (col ^ (sw(k) << 5)) : k * P + col;
+  }
+};
+
 // ------------------------------------------------------------------ MFMA
 // Operand fragments of one 128 x BN tile step. Wave w owns rows
 // [wm, wm+64) and columns [wn, wn+BN/2); lane l feeds row/column (l & 31) of
@@ -88,13 +111,13 @@ constexpr int BM = 128;
 // matching K indices; the order in which K is summed is the same for every
 // output element and every band.
 // AKM / BKM select the LDS layout of an operand: 0 = [row][k] (pitch
-// LDK), fragments read as 16-byte vectors; 1 = [k][row] (pitch rows + 4),
-// fragments read as 4-byte words. k-major staging lets operands whose global
-// layout is K-outer (the input gradient's weights, both weight-gradient
-// operands) be stored with 16-byte writes; it is used for float32, where
-// one element feeds one MFMA.
-// TA / TB: rows of the A tile and columns of the B tile in LDS (the pitch
-// of a k-major operand); NB = BN / 64 column blocks per wave.
+// LDK), fragments read as 16-byte vectors; 1 = [k][row] (layout KM),
+// fragments read as 4-byte words (float32) or with transposing reads
+// (bfloat16). k-major staging lets operands whose global layout is K-outer
+// (the input gradient's weights, both weight-gradient operands) be stored
+// with 16-byte writes.
+// TA / TB: rows of the A tile and columns of the B tile in LDS (the row
+// width of a k-major operand); NB = BN / 64 column blocks per wave.
 template <typename T, int BN, int KR, int AKM = 0, int BKM = 0, int TA = BM, int TB = BN>
 struct Frag;
 
@@ -102,7 +125,7 @@ template <int BN, int KR, int AKM, int BKM, int TA, int TB>
 struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
   static constexpr int LDK = Cfg<float, KR>::LDK, NB = BN / 64, NV = KR / 2;
   static constexpr int S = 4 * NV;            // K elements per lane group
-  static constexpr int PA = TA + 4, PB = TB + 4;
+  static constexpr int PA = KM<float, TA>::P, PB = KM<float, TB>::P;
   // instructions per tile step: MFMAs and LDS reads of one fragment load
   static constexpr int NMFMA = S * 2 * NB;
   static constexpr int NDSR = (AKM ? 2 * S : 2 * NV) + (BKM ? NB * S : NB * NV);
@@ -155,7 +178,7 @@ struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
 // bfloat16: one MFMA slice s (16 K values) gives lane half g = l >> 5 the
 // K values 16*g + 8*s + [0, 8) of row / column l & 31 of its 32x32 block.
 // [row][k] operands are read as one 16-byte vector per slice. k-major
-// operands ([k][row], pitch rows + 8) are read with two transposing LDS
+// operands ([k][row], layout KM) are read with two transposing LDS
 // reads (ds_read_b64_tr_b16): within each 16-lane group, lane i receives
 // element i mod 4 of the 8-byte runs addressed by lanes 4*k' + i/4,
 // k' = 0..3, so lane 16*G + 4*k' + q addresses K row
@@ -164,11 +187,12 @@ struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
 // read. Both layouts therefore sum K in the same order.
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-__device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int pitch, int base, int s, int lane) {
+template <int W>
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int base, int s, int lane) {
   const int G = lane >> 4, sl = lane & 15;
   const int k = 16 * (G >> 1) + 8 * s + (sl >> 2);
   const int col = base + 16 * (G & 1) + 4 * (sl & 3);
-  const bf16 *p0 = T + k * pitch + col, *p1 = T + (k + 4) * pitch + col;
+  const bf16 *p0 = T + KM<bf16, W>::off(k, col), *p1 = T + KM<bf16, W>::off(k + 4, col);
   const bf16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
       (lds_bf16x4 *)((__attribute__((address_space(3))) char *)(char *)p0));
   const bf16x4 r1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
@@ -179,7 +203,6 @@ __device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int pitch, int base, int
 template <int BN, int KR, int AKM, int BKM, int TA, int TB>
 struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
   static constexpr int LDK = Cfg<bf16, KR>::LDK, NB = BN / 64, NV = KR / 2;
-  static constexpr int PA = TA + 8, PB = TB + 8;
   static constexpr int NMFMA = NV * 2 * NB;
   static constexpr int NDSR = (AKM ? 4 * NV : 2 * NV) + (BKM ? 2 * NB * NV : NB * NV);
   bf16x8 a[2][NV], b[NB][NV];
@@ -190,7 +213,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
     for (int i = 0; i < 2; ++i) {
       if (AKM) {
 #pragma unroll
-        for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8(As, PA, wm + 32 * i, q, lane);
+        for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8<TA>(As, wm + 32 * i, q, lane);
       } else {
         const int row = wm + 32 * i + r;
         const bf16x8 *p = (const bf16x8 *)(As + row * LDK);
@@ -202,7 +225,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
     for (int j = 0; j < NB; ++j) {
       if (BKM) {
 #pragma unroll
-        for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8(Bs, PB, wn + 32 * j, q, lane);
+        for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8<TB>(Bs, wn + 32 * j, q, lane);
       } else {
         const int row = wn + 32 * j + r;
         const bf16x8 *p = (const bf16x8 *)(Bs + row * LDK);

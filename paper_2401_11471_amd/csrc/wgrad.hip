@@ -25,8 +25,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   constexpr int RVA = WBM / E;      // 16-byte vectors per A tile row
   constexpr int KSA = 256 / RVA;    // pixels of A loaded per pass
   constexpr int NPA = BK / KSA;     // A passes per tile
-  constexpr int PA = WBM + E, PB = BN + E;
-  constexpr int ASZ = BK * PA, BSZ = BK * PB;
+  constexpr int ASZ = BK * KM<T, WBM>::P, BSZ = BK * KM<T, BN>::P;
   constexpr int ST = 3;
   __shared__ __align__(16) T As[ST][ASZ];
   __shared__ __align__(16) T Bs[ST][BSZ];
@@ -123,10 +122,10 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   auto store = [&](int st) {
 #pragma unroll
     for (int i = 0; i < NPA; ++i)
-      *(uint4 *)(&As[st][(kka0 + KSA * i) * PA + rva * E]) = ra[i].u;
+      *(uint4 *)(&As[st][KM<T, WBM>::off(kka0 + KSA * i, rva * E)]) = ra[i].u;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
-      *(uint4 *)(&Bs[st][(kk0 + KS * i) * PB + rv * E]) = rb[i].u;
+      *(uint4 *)(&Bs[st][KM<T, BN>::off(kk0 + KS * i, rv * E)]) = rb[i].u;
   };
 
   f32x16 acc[2][NB];

@@ -17,7 +17,8 @@ import os
 import torch  # noqa: F401
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liblrcnn.so")
+# (LRCNN_LIB_PATH: another build of the library, e.g. a variant under test)
+LIB_PATH = os.environ.get("LRCNN_LIB_PATH") or os.path.join(HERE, "liblrcnn.so")
 
 OP_INPUT, OP_CONV, OP_MAXPOOL, OP_ADD = 0, 1, 2, 3
 F32, BF16 = 0, 1
