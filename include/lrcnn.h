@@ -261,6 +261,28 @@ int lrcnn_forward_rows(lrcnn_plan_t *plan, const void *x,
                        void *y, void *workspace, size_t ws_bytes,
                        void *const *mask_out, void *stream);
 
+/* Allocation-free lrcnn_forward_rows, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). The workspace is the library's own
+ * static device array of LRCNN_STATIC_WORKSPACE_BYTES (64 MiB), one per
+ * device, held from the library's load until the process ends; its device
+ * address is looked up once per device on the first call there. The call
+ * allocates no device memory; the caller still owns x, w, aff_*, y and
+ * mask_out, with the meaning, layout and results of lrcnn_forward_rows.
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents (the forward initialises every row it reads): calls that
+ * overlap on one device (several streams or threads) race. A later
+ * lrcnn_backward_rows cannot use this forward's shared rows (ESTATE).
+ * Errors: as lrcnn_forward_rows; EWORKSPACE when the plan's workspace_bytes
+ * exceed LRCNN_STATIC_WORKSPACE_BYTES; EHIP when the array's device address
+ * cannot be obtained. */
+#define LRCNN_STATIC_WORKSPACE_BYTES (64u << 20)
+int lrcnn_forward_rows_static(lrcnn_plan_t *plan, const void *x,
+                              const void *const *w,
+                              const float *const *aff_scale,
+                              const float *const *aff_shift, void *y,
+                              void *const *mask_out, void *stream);
+
 /* Row-centric BP (Algorithm 1, BP loop), bands in reverse: recompute each
  * band, propagate the error dy = dL/dy, overwrite dw[node] (float32,
  * [C_out][kh][kw][C_in]) with the weight gradient of every conv node and,

@@ -10,7 +10,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblrcnn.so")
 SOURCES = ["plan.cpp", "exec.cpp", "kernels.hip", "conv_f32_fwd.hip", "conv_f32_dgrad.hip",
-           "conv_bf16_fwd.hip", "conv_bf16_dgrad.hip", "wgrad.hip", "head.hip"]
+           "conv_bf16_fwd.hip", "conv_bf16_dgrad.hip", "wgrad.hip", "head.hip",
+           "static_ws.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -94,6 +94,7 @@ def _load():
                                     C.POINTER(Budget), C.POINTER(i32)]
     lib.lrcnn_plan_destroy.restype = None
     lib.lrcnn_forward_rows.argtypes = [vp, vp, pp, pp, pp, vp, vp, sz, pp, vp]
+    lib.lrcnn_forward_rows_static.argtypes = [vp, vp, pp, pp, pp, vp, pp, vp]
     lib.lrcnn_backward_rows.argtypes = [vp, vp, pp, pp, pp, vp, pp, vp, vp, sz, vp]
     lib.lrcnn_layerwise_reference_gpu.argtypes = [vp, vp, pp, pp, pp, vp, vp, pp, vp,
                                                   vp, sz, pp, vp]
@@ -119,7 +120,8 @@ def _load():
     lib.lrcnn_debug_layerwise_map.argtypes = [vp, i32, C.POINTER(sz)]
     lib.lrcnn_debug_layerwise_map.restype = C.c_int
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
-              "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_backward_rows",
+              "lrcnn_plan_band_rows", "lrcnn_forward_rows", "lrcnn_forward_rows_static",
+              "lrcnn_backward_rows",
               "lrcnn_layerwise_reference_gpu", "lrcnn_plan_step_bytes",
               "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_head_workspace_bytes",
               "lrcnn_head_loss", "lrcnn_sgd_update"):
@@ -134,6 +136,7 @@ EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_plan_band_rows", "lrcnn_plan_destroy", "lrcnn_plan_step_bytes",
            "lrcnn_plan_for_budget", "lrcnn_max_batch", "lrcnn_head_workspace_bytes",
            "lrcnn_head_loss", "lrcnn_sgd_update", "lrcnn_forward_rows",
+           "lrcnn_forward_rows_static",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
            "lrcnn_debug_dry_run", "lrcnn_debug_fp_pipeline", "lrcnn_debug_act_fusion",
            "lrcnn_debug_dgrad_phases",
@@ -255,6 +258,18 @@ def lrcnn_forward_rows(plan, x, weights, scales, shifts, y, workspace, masks=Non
         plan.handle, _ptr(x), _ptr_array(weights), _ptr_array(scales),
         _ptr_array(shifts), _ptr(y), _ptr(workspace), workspace.numel(),
         _ptr_array(masks) if masks is not None else None, _stream(stream)))
+
+
+def lrcnn_forward_rows_static(plan, x, weights, scales, shifts, y, masks=None, stream=None):
+    """lrcnn_forward_rows on the library's static device workspace (no
+    workspace argument; the call allocates nothing)."""
+    _check(LIB.lrcnn_forward_rows_static(
+        plan.handle, _ptr(x), _ptr_array(weights), _ptr_array(scales),
+        _ptr_array(shifts), _ptr(y),
+        _ptr_array(masks) if masks is not None else None, _stream(stream)))
+
+
+STATIC_WORKSPACE_BYTES = 64 << 20
 
 
 def lrcnn_backward_rows(plan, x, weights, scales, shifts, dy, dws, dx, workspace,
