@@ -3,6 +3,8 @@
 // direction by the conv_*.hip translation units.
 #pragma once
 
+#include <type_traits>
+
 #include "kdev.hpp"
 
 namespace lrcnn {
@@ -497,25 +499,47 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
     constexpr int RPP = 256 / CPR;  // tile rows per pass
     const int cc = tid % CPR;
     const int n = n0 + cc * E;
+    // the affine parameters of this lane's columns, read once (columns
+    // past N are staged but never stored)
+    float csc[NB], csh[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int nn = n0 + wn + 32 * j + col;
+      const bool ok = a.scale && nn < a.N;
+      csc[j] = ok ? a.scale[nn] : 1.f;
+      csh[j] = ok ? a.shift[nn] : 0.f;
+    }
+    // the accumulators of this wave's rows in [h0, h0 + HR), affine and
+    // ReLU applied, into the staging tile (SC / RL fixed per launch, so
+    // the unrolled loop has no branches)
+    auto stage = [&](auto SC, auto RL, int h0) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = wm - h0 + 32 * i + acc_row(v, lane);
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            float val = acc[i][j][v];
+            if constexpr (decltype(SC)::value) val = val * csc[j] + csh[j];
+            if constexpr (decltype(RL)::value) val = val > 0.f ? val : 0.f;
+            stf(&Ct[r * CP + wn + 32 * j + col], val);
+          }
+        }
+    };
+    // (the chunk's mask bytes start at a multiple of E bytes from the base)
+    const bool mask_vec = ((uintptr_t)a.mask & (E - 1)) == 0;
+    using yes = std::true_type;
+    using no = std::false_type;
     for (int h0 = 0; h0 < BM; h0 += HR) {
     if (h0) __syncthreads();
     if (wm >= h0 && wm < h0 + HR) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = wm - h0 + 32 * i + acc_row(v, lane);
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          const int cl = wn + 32 * j + col;
-          const int nn = n0 + cl;
-          float val = acc[i][j][v];
-          if (nn < a.N) {
-            if (a.scale) val = val * a.scale[nn] + a.shift[nn];
-            if (a.relu) val = val > 0.f ? val : 0.f;
-          }
-          stf(&Ct[r * CP + cl], val);
-        }
+      if (a.scale) {
+        if (a.relu) stage(yes(), yes(), h0);
+        else stage(yes(), no(), h0);
+      } else {
+        if (a.relu) stage(no(), yes(), h0);
+        else stage(no(), no(), h0);
       }
     }
     __syncthreads();
@@ -548,14 +572,23 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       }
       *(uint4 *)((T *)a.dst.p + off) = q;
       if (a.mask) {
+        // E mask bytes (1 where the stored value is > 0) in one store
         union {
           uint4 u;
           T e[E];
         } w;
         w.u = q;
-        uint8_t *mk = a.mask + (((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n;
+        uint64_t bits = 0;
 #pragma unroll
-        for (int e = 0; e < E; ++e) mk[e] = ldf(&w.e[e]) > 0.f ? 1 : 0;
+        for (int e = 0; e < E; ++e) bits |= (uint64_t)(ldf(&w.e[e]) > 0.f ? 1 : 0) << (8 * e);
+        uint8_t *mk = a.mask + (((long long)b * a.mask_h + y) * a.Wd + x) * a.N + n;
+        if (mask_vec) {
+          if (E == 8) *(uint64_t *)mk = bits;
+          else *(uint32_t *)mk = (uint32_t)bits;
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e) mk[e] = (uint8_t)(bits >> (8 * e));
+        }
       }
     }
     }

@@ -36,13 +36,13 @@ __device__ __forceinline__ float ldf(const float *p) { return *p; }
 __device__ __forceinline__ float ldf(const bf16 *p) {
   return __uint_as_float((uint32_t)(*p) << 16);
 }
-// float32 -> bfloat16, round to nearest, ties to even (NaN kept quiet).
+// float32 -> bfloat16, round to nearest, ties to even (NaN stays NaN):
+// the gfx950 conversion instruction (v_cvt_pk_bf16_f32), which gives the
+// same bits as the integer rounding u + 0x7fff + ((u >> 16) & 1) for every
+// non-NaN float32 input, denormals included (checked over all 2^32 bit
+// patterns on the device).
 __device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu))
-    return (bf16)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
+  return __builtin_bit_cast(bf16, (__bf16)f);
 }
 __device__ __forceinline__ void stf(float *p, float v) { *p = v; }
 __device__ __forceinline__ void stf(bf16 *p, float v) { *p = f2bf(v); }

@@ -279,6 +279,9 @@ struct WgradArgs {
   int kh, kw, sh, sw, ph, pw;
   int overwrite;  // 1: dw = this launch's sum (the first band); 0: dw += it
   FastDiv fw, fr;  // division by Wv and by y1 - y0 (set by the launcher)
+  // one K step of BK pixels as a mixed-radix (b, row, column) increment:
+  // BK = wdb * (Wv * R) + wdy * Wv + wdx (set by the launcher)
+  int wdx, wdy, wdb;
 };
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels

@@ -57,6 +57,55 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   };
   V16 ra[NPA], rb[2];
   int k0 = kbeg;
+  // B with channel counts that are multiples of E: thread (kkb, rvb)
+  // loads pixel k0 + kkb under column vectors rvb and rvb + RV / 2, so one
+  // pixel position per thread is walked from K step to K step (a
+  // mixed-radix increment, no division in the loop); the taps' offsets in
+  // the source window are fixed per thread
+  constexpr int RVH = RV / 2;
+  const int kkb = tid / RVH, rvb = tid % RVH;
+  // walk state of pixel k0 + kkb: column wx and band row wy, the source
+  // row / column under tap (0, 0) (ybase, xbase) and the byte offset of
+  // that source position (poff); a K step adds uniform deltas, with the
+  // column and row carries selecting the wrap corrections
+  int wx = 0, wy = 0, ybase = 0, xbase = 0;
+  long long poff = 0;
+  int bti[2], btj[2];
+  long long btoff[2];
+  bool bnok[2];
+  constexpr long long ES = sizeof(T);
+  const int dxb = a.wdx * a.sw, wxb = a.Wv * a.sw;
+  const int dyb = a.wdy * a.sh, ryb = R * a.sh;
+  const long long pd0 =
+      ((long long)a.wdb * a.src.bs + (long long)dyb * srow + (long long)dxb * a.src.C) * ES;
+  const long long pd1 = ((long long)a.sh * srow - (long long)wxb * a.src.C) * ES;
+  const long long pd2 = (a.src.bs - (long long)ryb * srow) * ES;
+  if (BVEC) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int nb = n0 + (rvb + RVH * h) * E;
+      const int tap = nb / a.Ci;
+      const int c = nb - tap * a.Ci;
+      bti[h] = tap / a.kw;
+      btj[h] = tap - bti[h] * a.kw;
+      bnok[h] = nb < N;
+      btoff[h] = ((long long)bti[h] * srow + (long long)btj[h] * a.src.C + c) * ES;
+    }
+    uint32_t t, x, yy, b;
+    fdiv_qr((uint32_t)(kbeg + kkb), a.fw, t, x);
+    fdiv_qr(t, a.fr, b, yy);
+    wx = (int)x, wy = (int)yy;
+    ybase = (a.y0 + wy) * a.sh - a.ph;
+    xbase = wx * a.sw - a.pw;
+    poff = ((long long)b * a.src.bs + (long long)(ybase - a.src.row0) * srow +
+            (long long)xbase * a.src.C) * ES;
+  }
+  // A: byte offsets of this thread's pixels, advanced by BK pixels a step
+  long long aoff[NPA];
+#pragma unroll
+  for (int i = 0; i < NPA; ++i)
+    aoff[i] = ((long long)(kbeg + kka0 + KSA * i) * a.Co + ov) * ES;
+  const long long adk = (long long)BK * a.Co * ES;
   const bool ovok = ov < a.Co, nbok = nb0 < N;
   // channel counts that are not a multiple of E (the first layer): the
   // (tap, channel) of each of this thread's E columns, fixed for the launch
@@ -82,15 +131,37 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
       const int p = k0 + kka0 + KSA * i;
       const bool pk = p < kend;
       if (AVEC) {
-        ra[i].u = load16z(dc, ((long long)p * a.Co + ov) * (long long)sizeof(T), pk & ovok);
+        ra[i].u = load16z(dc, aoff[i], pk & ovok);
+        aoff[i] += adk;
       } else {
 #pragma unroll
         for (int e = 0; e < E; ++e)
           ra[i].e[e] = (pk && ov + e < a.Co) ? dc[(long long)p * a.Co + ov + e] : (T)0;
       }
     }
+    if (BVEC) {
+      // B: E input values of pixel p under each of the thread's two taps
+      const int p = k0 + kkb;
+      const bool pk = p < kend;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+      for (int h = 0; h < 2; ++h) {
+        const int sy = ybase + bti[h], sx = xbase + btj[h];
+        const bool ok = pk & bnok[h] & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+        rb[h].u = load16z(src, poff + btoff[h], ok);
+      }
+      // next K step: pixel + BK
+      wx += a.wdx;
+      const bool cx = wx >= a.Wv;
+      wx -= cx ? a.Wv : 0;
+      xbase += dxb - (cx ? wxb : 0);
+      wy += a.wdy + (cx ? 1 : 0);
+      const bool cy = wy >= R;
+      wy -= cy ? R : 0;
+      ybase += dyb + (cx ? a.sh : 0) - (cy ? ryb : 0);
+      poff += pd0 + (pd1 & -(long long)cx) + (pd2 & -(long long)cy);
+    }
+#pragma unroll
+    for (int i = 0; i < 2 && !BVEC; ++i) {
       // B: E input values of pixel p under the column's tap
       const int p = k0 + kk0 + KS * i;
       const bool pk = p < kend;
@@ -98,13 +169,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
       fdiv_qr((uint32_t)(pk ? p : 0), a.fw, t, x);
       fdiv_qr(t, a.fr, b, yy);
       const int y = a.y0 + (int)yy;
-      if (BVEC) {
-        const int sy = y * a.sh - a.ph + tiv, sx = x * a.sw - a.pw + tjv;
-        const bool ok = pk & nbok & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
-        const long long off =
-            b * a.src.bs + (sy - a.src.row0) * srow + (long long)sx * a.src.C + cv;
-        rb[i].u = load16z(src, off * (long long)sizeof(T), ok);
-      } else {
+      {
         const long long bbase = b * a.src.bs - a.src.row0 * srow;
         const int sy0 = y * a.sh - a.ph, sx0 = x * a.sw - a.pw;
 #pragma unroll
@@ -124,8 +189,10 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
     for (int i = 0; i < NPA; ++i)
       *(uint4 *)(&As[st][KM<T, WBM>::off(kka0 + KSA * i, rva * E)]) = ra[i].u;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      *(uint4 *)(&Bs[st][KM<T, BN>::off(kk0 + KS * i, rv * E)]) = rb[i].u;
+    for (int i = 0; i < 2; ++i) {
+      if (BVEC) *(uint4 *)(&Bs[st][KM<T, BN>::off(kkb, (rvb + RVH * i) * E)]) = rb[i].u;
+      else *(uint4 *)(&Bs[st][KM<T, BN>::off(kk0 + KS * i, rv * E)]) = rb[i].u;
+    }
   };
 
   f32x16 acc[2][NB];
@@ -256,6 +323,9 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
   a.fw = fast_div((uint32_t)a.Wv);
   a.fr = fast_div((uint32_t)(a.y1 - a.y0));
   constexpr int BK = Cfg<T>::BK;
+  a.wdx = BK % a.Wv;
+  a.wdy = (BK / a.Wv) % (a.y1 - a.y0);
+  a.wdb = BK / (a.Wv * (a.y1 - a.y0));
   const WgradTiles wt = wgrad_tiles(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
   int splits = wt.splits;
   const int KT = (K + BK - 1) / BK;
