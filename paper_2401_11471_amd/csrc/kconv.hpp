@@ -688,7 +688,18 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
   const long long idx = ((long long)blockIdx.x * epb + e) * V;
   float val[4] = {0.f, 0.f, 0.f, 0.f};
   if (idx < MN) {
-    for (int z = g; z < splits; z += G) {
+    // four loads in flight, added in split order
+    int z = g;
+    for (; z + 3 * G < splits; z += 4 * G) {
+      float q4[4][4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ldv<float, V>(a.part + (z + G * u) * MN + idx, q4[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int k = 0; k < V; ++k) val[k] += q4[u][k];
+    }
+    for (; z < splits; z += G) {
       float q[4];
       ldv<float, V>(a.part + z * MN + idx, q);
 #pragma unroll

@@ -176,21 +176,22 @@ struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
 };
 
 // bfloat16: one MFMA slice s (16 K values) gives lane half g = l >> 5 the
-// K values 16*g + 8*s + [0, 8) of row / column l & 31 of its 32x32 block.
+// K values 8*NV*g + 8*s + [0, 8) of row / column l & 31 of its 32x32 block
+// (NV = KR / 2 slices per K tile row).
 // [row][k] operands are read as one 16-byte vector per slice. k-major
 // operands ([k][row], layout KM) are read with two transposing LDS
 // reads (ds_read_b64_tr_b16): within each 16-lane group, lane i receives
 // element i mod 4 of the 8-byte runs addressed by lanes 4*k' + i/4,
 // k' = 0..3, so lane 16*G + 4*k' + q addresses K row
-// 16*(G >> 1) + 8*s + 4*t + k' at column 16*(G & 1) + 4*q (t = 0, 1 for the
-// two reads), which hands every lane the same K values as the [row][k]
-// read. Both layouts therefore sum K in the same order.
+// 8*NV*(G >> 1) + 8*s + 4*t + k' at column 16*(G & 1) + 4*q (t = 0, 1 for
+// the two reads), which hands every lane the same K values as the
+// [row][k] read. Both layouts therefore sum K in the same order.
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-template <int W>
+template <int W, int NV>
 __device__ __forceinline__ bf16x8 ld_tr8(const bf16 *T, int base, int s, int lane) {
   const int G = lane >> 4, sl = lane & 15;
-  const int k = 16 * (G >> 1) + 8 * s + (sl >> 2);
+  const int k = 8 * NV * (G >> 1) + 8 * s + (sl >> 2);
   const int col = base + 16 * (G & 1) + 4 * (sl & 3);
   const bf16 *p0 = T + KM<bf16, W>::off(k, col), *p1 = T + KM<bf16, W>::off(k + 4, col);
   const bf16x4 r0 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
@@ -213,7 +214,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
     for (int i = 0; i < 2; ++i) {
       if (AKM) {
 #pragma unroll
-        for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8<TA>(As, wm + 32 * i, q, lane);
+        for (int q = 0; q < NV; ++q) a[i][q] = ld_tr8<TA, NV>(As, wm + 32 * i, q, lane);
       } else {
         const int row = wm + 32 * i + r;
         const bf16x8 *p = (const bf16x8 *)(As + row * LDK);
@@ -225,7 +226,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
     for (int j = 0; j < NB; ++j) {
       if (BKM) {
 #pragma unroll
-        for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8<TB>(Bs, wn + 32 * j, q, lane);
+        for (int q = 0; q < NV; ++q) b[j][q] = ld_tr8<TB, NV>(Bs, wn + 32 * j, q, lane);
       } else {
         const int row = wn + 32 * j + r;
         const bf16x8 *p = (const bf16x8 *)(Bs + row * LDK);

@@ -13,10 +13,17 @@ namespace lrcnn {
 #ifndef LRCNN_WG_OCC
 #define LRCNN_WG_OCC 2
 #endif
-template <typename T, int WBM, bool AVEC, bool BVEC>
+// K steps of KRW 16-byte vectors per tile row (BK = KRW * E pixels): 4, or
+// 8 for bfloat16 tiles with vector channel counts (twice the MFMAs per
+// barrier and per fragment prefetch).
+#ifndef LRCNN_WG_KR
+#define LRCNN_WG_KR 4
+#endif
+template <typename T, int WBM, bool AVEC, bool BVEC, int KRW = 4>
 __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, int kchunk,
                                                     float *dw) {
-  constexpr int E = Cfg<T>::E, BK = Cfg<T>::BK;
+  static_assert(KRW == 4 || (KRW == 8 && BVEC && AVEC), "K step");
+  constexpr int E = Cfg<T>::E, BK = KRW * E;
   constexpr int BN = 128;
   constexpr int FBN = WBM == 128 ? 128 : 64;  // columns per wave: FBN / 2
   constexpr int NB = FBN / 64;
@@ -55,21 +62,22 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
     uint4 u;
     T e[E];
   };
-  V16 ra[NPA], rb[2];
+  constexpr int RVH = RV / 2;
+  constexpr int NPB = BVEC ? BK / (256 / RVH) : 1;  // B pixel passes (vector path)
+  V16 ra[NPA], rb[2 * NPB];
   int k0 = kbeg;
   // B with channel counts that are multiples of E: thread (kkb, rvb)
   // loads pixel k0 + kkb under column vectors rvb and rvb + RV / 2, so one
   // pixel position per thread is walked from K step to K step (a
   // mixed-radix increment, no division in the loop); the taps' offsets in
   // the source window are fixed per thread
-  constexpr int RVH = RV / 2;
   const int kkb = tid / RVH, rvb = tid % RVH;
-  // walk state of pixel k0 + kkb: column wx and band row wy, the source
-  // row / column under tap (0, 0) (ybase, xbase) and the byte offset of
-  // that source position (poff); a K step adds uniform deltas, with the
-  // column and row carries selecting the wrap corrections
-  int wx = 0, wy = 0, ybase = 0, xbase = 0;
-  long long poff = 0;
+  // walk state of pixels k0 + kkb + (256 / RVH) * i: column wx and band row
+  // wy, the source row / column under tap (0, 0) (ybase, xbase) and the
+  // byte offset of that source position (poff); a K step adds uniform
+  // deltas, with the column and row carries selecting the wrap corrections
+  int wx[NPB], wy[NPB], ybase[NPB], xbase[NPB];
+  long long poff[NPB];
   int bti[2], btj[2];
   long long btoff[2];
   bool bnok[2];
@@ -91,14 +99,17 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
       bnok[h] = nb < N;
       btoff[h] = ((long long)bti[h] * srow + (long long)btj[h] * a.src.C + c) * ES;
     }
-    uint32_t t, x, yy, b;
-    fdiv_qr((uint32_t)(kbeg + kkb), a.fw, t, x);
-    fdiv_qr(t, a.fr, b, yy);
-    wx = (int)x, wy = (int)yy;
-    ybase = (a.y0 + wy) * a.sh - a.ph;
-    xbase = wx * a.sw - a.pw;
-    poff = ((long long)b * a.src.bs + (long long)(ybase - a.src.row0) * srow +
-            (long long)xbase * a.src.C) * ES;
+#pragma unroll
+    for (int i = 0; i < NPB; ++i) {
+      uint32_t t, x, yy, b;
+      fdiv_qr((uint32_t)(kbeg + kkb + (256 / RVH) * i), a.fw, t, x);
+      fdiv_qr(t, a.fr, b, yy);
+      wx[i] = (int)x, wy[i] = (int)yy;
+      ybase[i] = (a.y0 + wy[i]) * a.sh - a.ph;
+      xbase[i] = wx[i] * a.sw - a.pw;
+      poff[i] = ((long long)b * a.src.bs + (long long)(ybase[i] - a.src.row0) * srow +
+                 (long long)xbase[i] * a.src.C) * ES;
+    }
   }
   // A: byte offsets of this thread's pixels, advanced by BK pixels a step
   long long aoff[NPA];
@@ -140,25 +151,28 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
       }
     }
     if (BVEC) {
-      // B: E input values of pixel p under each of the thread's two taps
-      const int p = k0 + kkb;
-      const bool pk = p < kend;
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int sy = ybase + bti[h], sx = xbase + btj[h];
-        const bool ok = pk & bnok[h] & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
-        rb[h].u = load16z(src, poff + btoff[h], ok);
+      for (int i = 0; i < NPB; ++i) {
+        // B: E input values of pixel p under each of the thread's two taps
+        const int p = k0 + kkb + (256 / RVH) * i;
+        const bool pk = p < kend;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int sy = ybase[i] + bti[h], sx = xbase[i] + btj[h];
+          const bool ok = pk & bnok[h] & (sy >= 0) & (sy < a.Hs) & (sx >= 0) & (sx < a.Ws);
+          rb[2 * i + h].u = load16z(src, poff[i] + btoff[h], ok);
+        }
+        // next K step: pixel + BK
+        wx[i] += a.wdx;
+        const bool cx = wx[i] >= a.Wv;
+        wx[i] -= cx ? a.Wv : 0;
+        xbase[i] += dxb - (cx ? wxb : 0);
+        wy[i] += a.wdy + (cx ? 1 : 0);
+        const bool cy = wy[i] >= R;
+        wy[i] -= cy ? R : 0;
+        ybase[i] += dyb + (cx ? a.sh : 0) - (cy ? ryb : 0);
+        poff[i] += pd0 + (pd1 & -(long long)cx) + (pd2 & -(long long)cy);
       }
-      // next K step: pixel + BK
-      wx += a.wdx;
-      const bool cx = wx >= a.Wv;
-      wx -= cx ? a.Wv : 0;
-      xbase += dxb - (cx ? wxb : 0);
-      wy += a.wdy + (cx ? 1 : 0);
-      const bool cy = wy >= R;
-      wy -= cy ? R : 0;
-      ybase += dyb + (cx ? a.sh : 0) - (cy ? ryb : 0);
-      poff += pd0 + (pd1 & -(long long)cx) + (pd2 & -(long long)cy);
     }
 #pragma unroll
     for (int i = 0; i < 2 && !BVEC; ++i) {
@@ -188,10 +202,17 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
 #pragma unroll
     for (int i = 0; i < NPA; ++i)
       *(uint4 *)(&As[st][KM<T, WBM>::off(kka0 + KSA * i, rva * E)]) = ra[i].u;
+    if (BVEC) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      if (BVEC) *(uint4 *)(&Bs[st][KM<T, BN>::off(kkb, (rvb + RVH * i) * E)]) = rb[i].u;
-      else *(uint4 *)(&Bs[st][KM<T, BN>::off(kk0 + KS * i, rv * E)]) = rb[i].u;
+      for (int i = 0; i < NPB; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          *(uint4 *)(&Bs[st][KM<T, BN>::off(kkb + (256 / RVH) * i, (rvb + RVH * h) * E)]) =
+              rb[2 * i + h].u;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        *(uint4 *)(&Bs[st][KM<T, BN>::off(kk0 + KS * i, rv * E)]) = rb[i].u;
     }
   };
 
@@ -216,7 +237,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   }
   if (n > 2) gload();
   __syncthreads();
-  using FR = Frag<T, FBN, 4, 1, 1, WBM, BN>;
+  using FR = Frag<T, FBN, KRW, 1, 1, WBM, BN>;
   FR f0, f1;
   if (n > 0) f0.load(As[0], Bs[0], wm, wn, lane);
   int s1 = 1, s2 = 2;
@@ -236,7 +257,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
     store(s2);
     gload();
     cur.mma(acc);
-    interleave_step<FR::NMFMA, FR::NDSR, NPA + 2, NPA + 2>();
+    interleave_step<FR::NMFMA, FR::NDSR, NPA + 2 * NPB, NPA + 2 * NPB>();
     s1 = s2;
     s2 = s2 == ST - 1 ? 0 : s2 + 1;
     __syncthreads();
@@ -286,7 +307,18 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *part, fl
   const long long i = ((long long)blockIdx.x * 32 + e) * V;
   float acc[4] = {0.f, 0.f, 0.f, 0.f}, q[4];
   if (i < mn) {
-    for (int z = g; z < splits; z += 8) {
+    // four loads in flight, added in split order
+    int z = g;
+    for (; z + 24 < splits; z += 32) {
+      float q4[4][4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ldv<float, V>(part + (z + 8 * u) * mn + i, q4[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int k = 0; k < V; ++k) acc[k] += q4[u][k];
+    }
+    for (; z < splits; z += 8) {
       ldv<float, V>(part + z * mn + i, q);
 #pragma unroll
       for (int k = 0; k < V; ++k) acc[k] += q[k];
@@ -323,16 +355,21 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
   a.fw = fast_div((uint32_t)a.Wv);
   a.fr = fast_div((uint32_t)(a.y1 - a.y0));
   constexpr int BK = Cfg<T>::BK;
-  a.wdx = BK % a.Wv;
-  a.wdy = (BK / a.Wv) % (a.y1 - a.y0);
-  a.wdb = BK / (a.Wv * (a.y1 - a.y0));
+  const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
+  // (the split count is chosen in units of BK pixels, as the planner sizes
+  // the partial sums; a wide K step rounds each chunk up to its own width,
+  // which never adds splits)
+  const bool wide = LRCNN_WG_KR == 8 && sizeof(T) == 2 && avec && bvec;
+  const int BKL = wide ? 8 * Cfg<T>::E : BK;
+  a.wdx = BKL % a.Wv;
+  a.wdy = (BKL / a.Wv) % (a.y1 - a.y0);
+  a.wdb = BKL / (a.Wv * (a.y1 - a.y0));
   const WgradTiles wt = wgrad_tiles(a.Co, N, K, a.out ? a.part_bytes : 0, (int)sizeof(T));
   int splits = wt.splits;
   const int KT = (K + BK - 1) / BK;
-  const int kchunk = (KT + splits - 1) / splits * BK;
+  const int kchunk = ((KT + splits - 1) / splits * BK + BKL - 1) / BKL * BKL;
   splits = (K + kchunk - 1) / kchunk;
   if (!split_fits(splits, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
-  const bool avec = (a.Co % Cfg<T>::E) == 0, bvec = (a.Ci % Cfg<T>::E) == 0;
   const int wbm = wt.rows;
   dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
   int pr = -1;
@@ -340,7 +377,10 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
     pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                          (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
-  if (wbm == 64) {
+  if (wide) {
+    if (wbm == 64) wgrad_kernel<T, 64, true, true, 8><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    else wgrad_kernel<T, 128, true, true, 8><<<grid, 256, 0, s>>>(a, kchunk, dw);
+  } else if (wbm == 64) {
     if (avec && bvec) wgrad_kernel<T, 64, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
     else if (avec) wgrad_kernel<T, 64, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
     else wgrad_kernel<T, 64, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
