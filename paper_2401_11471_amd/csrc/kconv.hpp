@@ -809,38 +809,36 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   const bool one = vec && s1 && a.kh == 1 && a.kw == 1;
   if (bn == 64) {
     if (!s1) {
-      if (vec) conv_gemm_kernel<T, 64, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
-      else conv_gemm_kernel<T, 64, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+      if (vec) launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, true, false>, grid, s, pr, a);
+      else launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, false, false>, grid, s, pr, a);
     } else if (one) {
-      conv_gemm_kernel<T, 64, KR, DGRAD, true, true, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, true, true, true>, grid, s, pr, a);
     } else if (vec) {
-      conv_gemm_kernel<T, 64, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, true, true>, grid, s, pr, a);
     } else {
-      conv_gemm_kernel<T, 64, KR, DGRAD, false, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, false, true>, grid, s, pr, a);
     }
   } else {
     if (!s1) {
-      if (vec) conv_gemm_kernel<T, 128, KR, DGRAD, true, false><<<grid, 256, 0, s>>>(a);
-      else conv_gemm_kernel<T, 128, KR, DGRAD, false, false><<<grid, 256, 0, s>>>(a);
+      if (vec) launch_timed(conv_gemm_kernel<T, 128, KR, DGRAD, true, false>, grid, s, pr, a);
+      else launch_timed(conv_gemm_kernel<T, 128, KR, DGRAD, false, false>, grid, s, pr, a);
     } else if (one) {
-      conv_gemm_kernel<T, 128, KR, DGRAD, true, true, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 128, KR, DGRAD, true, true, true>, grid, s, pr, a);
     } else if (vec) {
-      conv_gemm_kernel<T, 128, KR, DGRAD, true, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 128, KR, DGRAD, true, true>, grid, s, pr, a);
     } else {
-      conv_gemm_kernel<T, 128, KR, DGRAD, false, true><<<grid, 256, 0, s>>>(a);
+      launch_timed(conv_gemm_kernel<T, 128, KR, DGRAD, false, true>, grid, s, pr, a);
     }
   }
-  prof::end(pr, s);
   if (splits > 1) {
     int p2 = prof::begin("conv_split_epilogue", 0.0, s);
     const int G = splits >= 8 ? 8 : splits >= 4 ? 4 : 2;
     const long long vecs = a.N % 4 == 0 ? (long long)M * a.N / 4 : (long long)M * a.N;
     const unsigned blocks = (unsigned)((vecs + 256 / G - 1) / (256 / G));
     if (a.N % 4 == 0)
-      conv_split_epilogue<T, DGRAD, 4><<<blocks, 256, 0, s>>>(a, splits, G);
+      launch_timed(conv_split_epilogue<T, DGRAD, 4>, dim3(blocks), s, p2, a, splits, G);
     else
-      conv_split_epilogue<T, DGRAD, 1><<<blocks, 256, 0, s>>>(a, splits, G);
-    prof::end(p2, s);
+      launch_timed(conv_split_epilogue<T, DGRAD, 1>, dim3(blocks), s, p2, a, splits, G);
   }
   return (int)hipGetLastError();
 }

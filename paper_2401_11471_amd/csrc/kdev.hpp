@@ -5,6 +5,7 @@
 // index arithmetic of band windows.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -14,12 +15,28 @@
 
 namespace lrcnn {
 
-// Launch timing of the matrix-core kernels (test hook; kernels.hip).
+// Launch timing of the matrix-core kernels (test hook; kernels.hip):
+// begin() registers a launch and returns its index (-1 when profiling is
+// off); the launch carries the index's start and stop events.
 namespace prof {
 extern bool on;
 int begin(const std::string &name, double flops, hipStream_t s);
-void end(int i, hipStream_t s);
+hipEvent_t start(int i);
+hipEvent_t stop(int i);
 }  // namespace prof
+
+// Launch of a kernel that may be profiled: with profiling on (pr >= 0) the
+// start and stop events are attached to the dispatch itself
+// (hipExtLaunchKernelGGL), so their interval is the kernel's execution
+// and not the queue time around it; otherwise a plain launch.
+template <typename F, typename... Args>
+inline void launch_timed(F kernel, dim3 grid, hipStream_t s, int pr, Args... args) {
+  if (pr >= 0)
+    hipExtLaunchKernelGGL(kernel, grid, dim3(256), 0, s, prof::start(pr), prof::stop(pr), 0,
+                          args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, dim3(256), 0, s, args...);
+}
 
 // Convolution launchers, one translation unit per storage type and
 // direction (conv_*.hip).

@@ -54,17 +54,15 @@ static hipEvent_t take() {
   }
   return pool[used++];
 }
-int begin(const std::string &name, double flops, hipStream_t s) {
+int begin(const std::string &name, double flops, hipStream_t) {
   if (!on) return -1;
   hipEvent_t a = take(), b = take();
   if (!a || !b) return -1;
-  hipEventRecord(a, s);
   recs.push_back(Rec{name, a, b, flops});
   return (int)recs.size() - 1;
 }
-void end(int i, hipStream_t s) {
-  if (i >= 0) hipEventRecord(recs[i].b, s);
-}
+hipEvent_t start(int i) { return recs[i].a; }
+hipEvent_t stop(int i) { return recs[i].b; }
 struct Agg {
   int64_t launches = 0;
   double ms = 0, flops = 0;

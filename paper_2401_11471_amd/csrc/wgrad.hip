@@ -378,28 +378,26 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
                          (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
   if (wide) {
-    if (wbm == 64) wgrad_kernel<T, 64, true, true, 8><<<grid, 256, 0, s>>>(a, kchunk, dw);
-    else wgrad_kernel<T, 128, true, true, 8><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    if (wbm == 64) launch_timed(wgrad_kernel<T, 64, true, true, 8>, grid, s, pr, a, kchunk, dw);
+    else launch_timed(wgrad_kernel<T, 128, true, true, 8>, grid, s, pr, a, kchunk, dw);
   } else if (wbm == 64) {
-    if (avec && bvec) wgrad_kernel<T, 64, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
-    else if (avec) wgrad_kernel<T, 64, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
-    else wgrad_kernel<T, 64, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    if (avec && bvec) launch_timed(wgrad_kernel<T, 64, true, true>, grid, s, pr, a, kchunk, dw);
+    else if (avec) launch_timed(wgrad_kernel<T, 64, true, false>, grid, s, pr, a, kchunk, dw);
+    else launch_timed(wgrad_kernel<T, 64, false, false>, grid, s, pr, a, kchunk, dw);
   } else {
-    if (avec && bvec) wgrad_kernel<T, 128, true, true><<<grid, 256, 0, s>>>(a, kchunk, dw);
-    else if (avec) wgrad_kernel<T, 128, true, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
-    else wgrad_kernel<T, 128, false, false><<<grid, 256, 0, s>>>(a, kchunk, dw);
+    if (avec && bvec) launch_timed(wgrad_kernel<T, 128, true, true>, grid, s, pr, a, kchunk, dw);
+    else if (avec) launch_timed(wgrad_kernel<T, 128, true, false>, grid, s, pr, a, kchunk, dw);
+    else launch_timed(wgrad_kernel<T, 128, false, false>, grid, s, pr, a, kchunk, dw);
   }
-  prof::end(pr, s);
   if (splits > 1) {
     long long mn = (long long)a.Co * N;
     int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
     if (mn % 4 == 0)
-      wgrad_reduce_kernel<4><<<(unsigned)((mn / 4 + 31) / 32), 256, 0, s>>>(a.out, dw, mn,
-                                                                            splits, a.overwrite);
+      launch_timed(wgrad_reduce_kernel<4>, dim3((unsigned)((mn / 4 + 31) / 32)), s, p2,
+                   (const float *)a.out, dw, mn, splits, a.overwrite);
     else
-      wgrad_reduce_kernel<1><<<(unsigned)((mn + 31) / 32), 256, 0, s>>>(a.out, dw, mn, splits,
-                                                                        a.overwrite);
-    prof::end(p2, s);
+      launch_timed(wgrad_reduce_kernel<1>, dim3((unsigned)((mn + 31) / 32)), s, p2,
+                   (const float *)a.out, dw, mn, splits, a.overwrite);
   }
   return (int)hipGetLastError();
 }

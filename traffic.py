@@ -50,7 +50,7 @@ def bench_name(mangled: str) -> str:
                 "1x1" if m.group(6) == "true" else "vec")
         return (f"conv_gemm_kernel<{m.group(1)}, {m.group(2)}, "
                 f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, {kind}>")
-    m = re.match(r"wgrad_kernel<(\w+), (?:\d+, )?(true|false), (true|false)>", n)
+    m = re.match(r"wgrad_kernel<(\w+), (?:\d+, )?(true|false), (true|false)(?:, \d+)?>", n)
     if m:
         vec = m.group(2) == "true" and m.group(3) == "true"
         return f"wgrad_kernel<{m.group(1)}, {'vec' if vec else 'scalar'}>"
