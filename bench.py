@@ -594,7 +594,7 @@ def main():
     if not args.eager:
         # HIP cannot time events recorded inside a graph, so the per-kernel
         # durations come from an eager pass of the same steps with the
-        # library's events around every matrix-core launch
+        # library's events attached to every matrix-core dispatch
         _, psteps, _ = timed_steps(torch, lambda: rc_step(bufs), args.steps, 0, True,
                                    L.lrcnn_debug_profile)
     kern = L.lrcnn_debug_profile_collect()

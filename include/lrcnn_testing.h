@@ -43,10 +43,13 @@ void lrcnn_debug_fp_pipeline(int on);
  * taps (default), 1 = always, 2 = never. Results agree to rounding. */
 void lrcnn_debug_dgrad_phases(int mode);
 
-/* on != 0: clear and start recording two events on the launch stream around
- * every matrix-core kernel launch (convolution forward, input gradient,
- * weight gradient), with each launch's algorithmic FLOPs; on == 0 stops
- * recording. Timing only: results are unchanged. */
+/* on != 0: clear and start timing every matrix-core kernel launch
+ * (convolution forward, input gradient, weight gradient) and split
+ * reduction: the launch goes through hipExtLaunchKernelGGL with a start and
+ * a stop event attached to the dispatch, so the interval is the kernel's
+ * execution; each launch's algorithmic FLOPs are recorded with it. on == 0
+ * stops. Timing only: results are unchanged. Launches made while timing is
+ * on cannot be captured in a graph (the events belong to the dispatch). */
 void lrcnn_debug_profile(int on);
 
 /* After the recorded streams are synchronised: aggregate the records per
