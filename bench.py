@@ -641,6 +641,13 @@ def main():
                    "launch": "host" if args.eager else "hip-graph"},
         "roofline": roofline,
         "tflops_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12, 2),
+        # the whole step against the matrix-core peak: all of the method's
+        # FLOPs (FP, recompute, both gradients), and the useful work of the
+        # layer-wise step, 3 tau (the recompute's share made visible)
+        "step_roofline": {
+            "frac_algorithmic": round(info["flops_rows"] / (ms * 1e-3) / 1e12 / peak, 4),
+            "tflops_useful_3tau": round(3 * info["flops_tau"] / (ms * 1e-3) / 1e12, 2),
+            "frac_useful_3tau": round(3 * info["flops_tau"] / (ms * 1e-3) / 1e12 / peak, 4)},
         "mfma_kernels": {"ms_per_step": round(all_mfma_ms, 3),
                          "tflops": round(all_mfma_fl / (all_mfma_ms * 1e-3) / 1e12, 2),
                          "per_kernel": {k: {"launches": v[0] // psteps,
