@@ -159,7 +159,7 @@ void set_dgrad_phases(int mode);
 #define LRCNN_STEP_N128 1.35  // one K iteration of a lone 128 x 128 tile (fp32)
 #endif
 #ifndef LRCNN_NARROW_GAIN
-#define LRCNN_NARROW_GAIN 1.0  // narrow tiles must beat wide ones by this factor
+#define LRCNN_NARROW_GAIN 1.5  // narrow tiles are taken unless wide ones are 1.5x faster
 #endif
 struct SplitCost {
   double step_us;   // one K iteration of a lone workgroup
