@@ -33,7 +33,11 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // swizzled LDS slot is lane & 3: each wave's rows fill 1 KiB of LDS in
   // lane order, the layout of a direct copy.
   constexpr bool LANE_SLOT = KR == 4 && LRCNN_SWZ;
-  constexpr bool DMA = LRCNN_LDS_DMA && LANE_SLOT && !DGRAD && VEC;
+  // Input gradient, stride 1, bfloat16: the same, with the weights' k-major
+  // tile copied in lane order too (k rows of BN unpadded elements; a
+  // thread's column vector is the one its lane's swizzled slot holds).
+  constexpr bool DMA = LRCNN_LDS_DMA && LANE_SLOT && VEC &&
+                       (!DGRAD || (LRCNN_DG_DMA && S1 && !ONE && sizeof(T) == 2));
   // LDS stages. Register staging: while tile t is multiplied, the
   // fragments of t+1 are read, tile t+2 is written and tile t+3 is fetched
   // from global memory. Direct copies: tiles t+2 .. t+ST-1 are in flight.
@@ -118,7 +122,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // taps mirrored, sy = by - ti and sx = bx - tj, operands staged through
   // registers)
   constexpr bool TMASK = DMA && !ONE;
-  constexpr bool RMASK = DGRAD && S1 && VEC && !ONE;
+  constexpr bool RMASK = DGRAD && S1 && VEC && !ONE && !DMA;
   constexpr bool MASK = TMASK || RMASK;
   uint64_t tmask[MASK ? NA : 1];
   const char *rp[DMA || RMASK ? NA : 1];
@@ -142,7 +146,8 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   bool bvld[NBL];
 #pragma unroll
   for (int j = 0; j < NBL; ++j) {
-    bn[j] = DGRAD ? n0 + (tid % BV) * E : n0 + tid / KR + RS * j;
+    bn[j] = DGRAD ? n0 + E * (DMA ? (tid % BV) ^ (KM<T, BN>::sw(tid / BV) << 2) : tid % BV)
+                  : n0 + tid / KR + RS * j;
     bvld[j] = bn[j] < a.N;
   }
   const int bk0 = tid / BV;
@@ -263,9 +268,18 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         load16_lds_a(rp[i] + ub, ((uint32_t)(tmask[i] >> tap) & 1u) & cok,
                      lds_a + st * ASB + (wrow + RS * i) * LDK * (uint32_t)sizeof(T), zblk);
 #pragma unroll
-      for (int j = 0; j < NBL; ++j)
-        load16_lds_a(wp[j] + wb, bvld[j] & cok,
-                     lds_b + st * BSB + (wrow + RS * j) * LDK * (uint32_t)sizeof(T), zblk);
+      for (int j = 0; j < NBL; ++j) {
+        if (DGRAD) {
+          // k rows (wave * 64) / BV + BKS * j + lane / BV of the k-major tile
+          load16_lds_a(wp[j] + wb, bvld[j] & (cb + bk0 + BKS * j < a.KC),
+                       lds_b + st * BSB +
+                           (uint32_t)((wave * 64) / BV + BKS * j) * BN * (uint32_t)sizeof(T),
+                       zblk);
+        } else {
+          load16_lds_a(wp[j] + wb, bvld[j] & cok,
+                       lds_b + st * BSB + (wrow + RS * j) * LDK * (uint32_t)sizeof(T), zblk);
+        }
+      }
     } else {
 #pragma unroll
     for (int i = 0; i < NA; ++i) {

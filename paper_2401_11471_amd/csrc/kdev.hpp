@@ -77,6 +77,10 @@ __device__ __forceinline__ int fdiv(int a, int b) {
 #ifndef LRCNN_LDS_DMA
 #define LRCNN_LDS_DMA 1
 #endif
+// input-gradient operands (stride 1, bfloat16) copied the same way
+#ifndef LRCNN_DG_DMA
+#define LRCNN_DG_DMA 1
+#endif
 // LDS stages of the direct-copy ring (3 or 4)
 #ifndef LRCNN_DMA_ST
 #define LRCNN_DMA_ST 3

@@ -165,6 +165,8 @@ struct SplitCost {
   double step_us;   // one K iteration of a lone workgroup
   int occ;          // workgroups one CU holds (LDS bound)
   double fixed_us;  // per-launch fixed cost
+  int max_s = 128;  // largest split count considered
+  double share = LRCNN_SHARE2;  // time factor of a workgroup sharing its CU
 };
 struct SplitChoice {
   int s;
@@ -176,7 +178,7 @@ inline double split_cost(long long tiles, int KT, long long part_elems, const Sp
   const long long wg = tiles * s;
   const long long per_cu = (wg + 255) / 256;
   const long long kts = (KT + s - 1) / s;
-  const double share = per_cu >= 2 && c.occ >= 2 ? LRCNN_SHARE2 : 1.0;
+  const double share = per_cu >= 2 && c.occ >= 2 ? c.share : 1.0;
   double t = (double)kts * (double)per_cu * c.step_us * share + c.fixed_us;
   if (s > 1) t += 6.0 + (double)s * (double)part_elems * 8.0 / 1.5e7;
   return t;
@@ -184,9 +186,9 @@ inline double split_cost(long long tiles, int KT, long long part_elems, const Sp
 // A split count s of a K loop of KT iterations is used only when no smaller
 // count gives the same chunks (each of the s chunks has ceil(KT / s)
 // iterations, the last one possibly fewer, none empty).
-inline bool split_valid(int KT, long long s) {
+inline bool split_valid(int KT, long long s, int max_s = 128) {
   if (s == 1) return true;
-  if (s < 1 || s > 128 || s > KT / 2) return false;
+  if (s < 1 || s > max_s || s > KT / 2) return false;
   const long long kts = (KT + s - 1) / s;
   return (KT + kts - 1) / kts == s;
 }
@@ -194,9 +196,9 @@ inline SplitChoice split_choice(long long tiles, int KT, long long part_elems, s
                                 const SplitCost &c) {
   SplitChoice best{1, split_cost(tiles, KT, part_elems, c, 1)};
   if (tiles <= 0 || KT <= 1) return best;
-  for (long long s = 2; s <= 128 && s <= KT / 2; ++s) {
+  for (long long s = 2; s <= c.max_s && s <= KT / 2; ++s) {
     if ((size_t)s * (size_t)part_elems * 4 > cap) break;
-    if (!split_valid(KT, s)) continue;  // same work as a smaller s
+    if (!split_valid(KT, s, c.max_s)) continue;  // same work as a smaller s
     const double t = split_cost(tiles, KT, part_elems, c, s);
     if (t < best.us * 0.98) best = SplitChoice{(int)s, t};
   }
@@ -295,6 +297,15 @@ inline int wgrad_k_iters(long long K, int es) { return (int)((K + 64 / es - 1) /
 #ifndef LRCNN_WG_NARROW
 #define LRCNN_WG_NARROW 1
 #endif
+// Split counts up to LRCNN_WG_MAXS are considered for the weight gradient
+// (its launches have few output tiles and long K loops); LRCNN_WG_SHARE is
+// its time factor for a workgroup that shares the CU.
+#ifndef LRCNN_WG_MAXS
+#define LRCNN_WG_MAXS 128
+#endif
+#ifndef LRCNN_WG_SHARE
+#define LRCNN_WG_SHARE LRCNN_SHARE2
+#endif
 struct WgradTiles {
   int rows, splits;
 };
@@ -303,10 +314,10 @@ inline WgradTiles wgrad_tiles(int Co, long long N, long long K, size_t cap, int 
   const int KT = wgrad_k_iters(K, es);
   const long long nt = (N + 127) / 128;
   const SplitChoice r64 = split_choice(((Co + 63) / 64) * nt, KT, (long long)Co * N, cap,
-                                       SplitCost{f * 0.55, 3, 12.0});
+                                       SplitCost{f * 0.55, 3, 12.0, LRCNN_WG_MAXS, LRCNN_WG_SHARE});
   if (Co <= 64) return WgradTiles{64, r64.s};
   const SplitChoice r128 = split_choice(((Co + 127) / 128) * nt, KT, (long long)Co * N, cap,
-                                        SplitCost{f, 3, 12.0});
+                                        SplitCost{f, 3, 12.0, LRCNN_WG_MAXS, LRCNN_WG_SHARE});
   if (LRCNN_WG_NARROW && es == 2 && r64.us < r128.us) return WgradTiles{64, r64.s};
   return WgradTiles{128, r128.s};
 }

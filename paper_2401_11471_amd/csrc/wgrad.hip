@@ -19,6 +19,32 @@ namespace lrcnn {
 #ifndef LRCNN_WG_KR
 #define LRCNN_WG_KR 4
 #endif
+// Epilogue of a weight-gradient tile: the wave's 64 x 32 NB accumulators
+// (rows m0 + [0, 64), columns n0 + [0, 32 NB)) go to dW (one split: dW =
+// or += the sum) or to the split's partial-sum slice.
+template <int NB>
+__device__ __forceinline__ void wgrad_store(const WgradArgs &a, float *dw,
+                                            const f32x16 (&acc)[2][NB], int m0, int n0,
+                                            int N, int z, int lane) {
+  const int col = lane & 31;
+  float *out = gridDim.z == 1 ? dw : a.out + (long long)z * a.Co * N;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int m = m0 + 32 * i + acc_row(v, lane);
+      if (m >= a.Co) continue;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int nn = n0 + 32 * j + col;
+        if (nn >= N) continue;
+        float *d = out + (long long)m * N + nn;
+        if (gridDim.z == 1) *d = a.overwrite ? acc[i][j][v] : *d + acc[i][j][v];
+        else *d = acc[i][j][v];
+      }
+    }
+}
+
 template <typename T, int WBM, bool AVEC, bool BVEC, int KRW = 4>
 __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, int kchunk,
                                                     float *dw) {
@@ -275,23 +301,195 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
   }
   if (t < n) step(t, f0, f1);
 
-  const int col = lane & 31;
-  float *out = gridDim.z == 1 ? dw : a.out + (long long)tl.z * a.Co * N;
+  wgrad_store<NB>(a, dw, acc, m0 + wm, n0 + wn, N, tl.z, lane);
+}
+
+// bfloat16 with channel counts that are multiples of 8: both operands are
+// copied from global memory straight into the LDS ring
+// (global_load_lds_dwordx4), so the tiles t+2 .. t+ST-1 are in flight while
+// tile t is multiplied, no wave writes LDS and no registers stage the
+// operands. A copy instruction of a wave fills 1 KiB of one k-major tile in
+// lane order: 1024 / (2 W) k rows of a W-wide tile, lane l writing the
+// 16-byte slot l mod (W / 8) of its row. That slot holds the vector
+// slot ^ 4 sw(k) of the row (the chunk swizzle of the k-major layout); since
+// every copy starts at a k row that is a multiple of 4 (W = 128) or 8
+// (W = 64), sw(k) depends on the lane alone, and so does the vector a
+// thread fetches: one output-channel vector of A and one (tap, channel)
+// vector of B per thread, over two or one A rows and two B rows per tile.
+#ifndef LRCNN_WG_DMA
+#define LRCNN_WG_DMA 1
+#endif
+#ifndef LRCNN_WG_DMA_ST
+#define LRCNN_WG_DMA_ST 3
+#endif
+#ifndef LRCNN_WG_DMA_OCC
+#define LRCNN_WG_DMA_OCC 2
+#endif
+template <int WBM>
+__global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_dma_kernel(WgradArgs a,
+                                                                          int kchunk,
+                                                                          float *dw) {
+  using T = bf16;
+  constexpr int E = 8, BK = 32, BN = 128, ST = LRCNN_WG_DMA_ST;
+  static_assert(ST == 3 || ST == 4, "ring depth");
+  constexpr int FBN = WBM == 128 ? 128 : 64, NB = FBN / 64;
+  constexpr int VA = WBM / E, RA = 64 / VA;  // vectors per A row, A rows per copy
+  constexpr int NIA = BK / RA / 4;           // A copies per wave per tile
+  constexpr int VB = BN / E, RB = 64 / VB;   // the same for B
+  constexpr int NIB = BK / RB / 4;
+  constexpr int LD = NIA + NIB;              // copies per thread per tile
+  constexpr uint32_t ASB = BK * WBM * 2, BSB = BK * BN * 2;  // stage bytes
+  static_assert(4 * NIA * 1024 == ASB && 4 * NIB * 1024 == BSB, "copy cover");
+  __shared__ __align__(16) char smem[ST * (ASB + BSB)];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int R = a.y1 - a.y0;
+  const int K = a.B * R * a.Wv;
+  const int N = a.kh * a.kw * a.Ci;
+  const TileId tl = xcd_tile(false);
+  const int m0 = tl.x * WBM, n0 = tl.y * BN;
+  const int kbeg = tl.z * kchunk;
+  const int kend = min(K, kbeg + kchunk);
+  const char *dc = (const char *)a.dc;
+  const char *src = (const char *)a.src.p;
+  const long long srow = (long long)a.src.W * a.src.C;
+  constexpr long long ES = 2;
+
+  // A: k row lane / VA of each copy, output-channel vector fixed per thread
+  const int ka = lane / VA;
+  const int ova = m0 + E * ((lane % VA) ^ (KM<T, WBM>::sw(ka) << 2));
+  const bool ovok = ova < a.Co;
+  long long aoff[NIA];
+  int kar[NIA];
+#pragma unroll
+  for (int j = 0; j < NIA; ++j) {
+    kar[j] = (wave * NIA + j) * RA + ka;
+    aoff[j] = ((long long)(kbeg + kar[j]) * a.Co + ova) * ES;
+  }
+  const long long adk = (long long)BK * a.Co * ES;
+  // B: (tap, channel) vector fixed per thread, two pixels walked per step
+  const int kb = lane / VB;
+  const int nb = n0 + E * ((lane % VB) ^ (KM<T, BN>::sw(kb) << 2));
+  const int tap = nb / a.Ci;
+  const int bti = tap / a.kw, btj = tap - (tap / a.kw) * a.kw;
+  const bool bnok = nb < N;
+  const long long btoff =
+      ((long long)bti * srow + (long long)btj * a.src.C + (nb - tap * a.Ci)) * ES;
+  const int dxb = a.wdx * a.sw, wxb = a.Wv * a.sw;
+  const int dyb = a.wdy * a.sh, ryb = R * a.sh;
+  const long long pd0 =
+      ((long long)a.wdb * a.src.bs + (long long)dyb * srow + (long long)dxb * a.src.C) * ES;
+  const long long pd1 = ((long long)a.sh * srow - (long long)wxb * a.src.C) * ES;
+  const long long pd2 = (a.src.bs - (long long)ryb * srow) * ES;
+  int wx[NIB], wy[NIB], ybase[NIB], xbase[NIB], kbr[NIB];
+  long long poff[NIB];
+#pragma unroll
+  for (int j = 0; j < NIB; ++j) {
+    kbr[j] = (wave * NIB + j) * RB + kb;
+    uint32_t t, x, yy, b;
+    fdiv_qr((uint32_t)(kbeg + kbr[j]), a.fw, t, x);
+    fdiv_qr(t, a.fr, b, yy);
+    wx[j] = (int)x, wy[j] = (int)yy;
+    ybase[j] = (a.y0 + wy[j]) * a.sh - a.ph + bti;
+    xbase[j] = wx[j] * a.sw - a.pw + btj;
+    poff[j] = ((long long)b * a.src.bs + (long long)(ybase[j] - bti - a.src.row0) * srow +
+               (long long)(xbase[j] - btj) * a.src.C) * ES + btoff;
+  }
+  const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+  const uint32_t lds_b = lds_a + ST * ASB;
+  const void *zblk = &g_zero16[0];
+  asm volatile("" : "+s"(zblk));
+  int k0 = kbeg;
+  // copies of the tile at pixels [k0, k0 + BK) into stage st
+  auto gload = [&](int st) {
+#pragma unroll
+    for (int j = 0; j < NIA; ++j) {
+      load16_lds_a(dc + aoff[j], (k0 + kar[j] < kend) & ovok,
+                   lds_a + st * ASB + (uint32_t)(wave * NIA + j) * 1024u, zblk);
+      aoff[j] += adk;
+    }
+#pragma unroll
+    for (int j = 0; j < NIB; ++j) {
+      const bool ok = (k0 + kbr[j] < kend) & bnok & (ybase[j] >= 0) & (ybase[j] < a.Hs) &
+                      (xbase[j] >= 0) & (xbase[j] < a.Ws);
+      load16_lds_a(src + poff[j], ok, lds_b + st * BSB + (uint32_t)(wave * NIB + j) * 1024u,
+                   zblk);
+      // next K step: pixel + BK (column and row carries select the wraps)
+      wx[j] += a.wdx;
+      const bool cx = wx[j] >= a.Wv;
+      wx[j] -= cx ? a.Wv : 0;
+      xbase[j] += dxb - (cx ? wxb : 0);
+      wy[j] += a.wdy + (cx ? 1 : 0);
+      const bool cy = wy[j] >= R;
+      wy[j] -= cy ? R : 0;
+      ybase[j] += dyb + (cx ? a.sh : 0) - (cy ? ryb : 0);
+      poff[j] += pd0 + (pd1 & -(long long)cx) + (pd2 & -(long long)cy);
+    }
+    k0 += BK;
+  };
+  auto As = [&](int st) { return (const T *)(smem + st * ASB); };
+  auto Bs = [&](int st) { return (const T *)(smem + ST * ASB + st * BSB); };
+
+  f32x16 acc[2][NB];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int m = m0 + wm + 32 * i + acc_row(v, lane);
-      if (m >= a.Co) continue;
+    for (int j = 0; j < NB; ++j)
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int nn = n0 + wn + 32 * j + col;
-        if (nn >= N) continue;
-        float *d = out + (long long)m * N + nn;
-        if (gridDim.z == 1) *d = a.overwrite ? acc[i][j][v] : *d + acc[i][j][v];
-        else *d = acc[i][j][v];
-      }
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const int wm = WBM == 128 ? (wave & 1) * 64 : 0;
+  const int wn = WBM == 128 ? (wave >> 1) * 64 : wave * 32;
+  const int n = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  using FR = Frag<T, FBN, 4, 1, 1, WBM, BN>;
+  FR f0, f1;
+  // Tile t+ST is copied into the stage of tile t once every wave has read
+  // tile t; a step waits only for tile t+1, so a copy has ST-1 steps to
+  // arrive. wait_tiles(k) leaves the copies of the k most recent tiles in
+  // flight.
+  auto wait_tiles = [](int k) {
+    if (ST > 3 && k >= 2) wait_vmcnt<(ST > 3 ? 2 : 0) * LD>();
+    else if (k == 1) wait_vmcnt<LD>();
+    else wait_vmcnt<0>();
+  };
+#pragma unroll
+  for (int i = 0; i < ST; ++i)
+    if (i < n) gload(i);
+  wait_tiles(min(n, ST) - 1);
+  __syncthreads();
+  if (n > 0) f0.load(As(0), Bs(0), wm, wn, lane);
+  int sc = 0;  // stage of tile t
+  auto dstep = [&](int t, FR &cur, FR &nxt) {
+    const int s1 = sc == ST - 1 ? 0 : sc + 1;
+    if (t + 1 < n) {
+      wait_tiles(min(n - 1, t + ST - 1) - t - 1);
+      __syncthreads();
+      nxt.load(As(s1), Bs(s1), wm, wn, lane);
+      if (t + ST < n) gload(sc);
     }
+    cur.mma(acc);
+    sc = s1;
+  };
+  auto dstep_full = [&](FR &cur, FR &nxt) {
+    const int s1 = sc == ST - 1 ? 0 : sc + 1;
+    wait_vmcnt<(ST - 2) * LD>();
+    __syncthreads();
+    nxt.load(As(s1), Bs(s1), wm, wn, lane);
+    gload(sc);
+    cur.mma(acc);
+    interleave_step<FR::NMFMA, FR::NDSR, 0, LD>();
+    sc = s1;
+  };
+  int t = 0;
+  for (; t + ST + 1 < n; t += 2) {
+    dstep_full(f0, f1);
+    dstep_full(f1, f0);
+  }
+  for (; t + 1 < n; t += 2) {
+    dstep(t, f0, f1);
+    dstep(t + 1, f1, f0);
+  }
+  if (t < n) dstep(t, f0, f1);
+  wgrad_store<NB>(a, dw, acc, m0 + wm, n0 + wn, N, tl.z, lane);
 }
 
 // dW += (first band: dW =) sum over the split partial sums in a fixed order
@@ -377,7 +575,10 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
     pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                          (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
-  if (wide) {
+  if (LRCNN_WG_DMA && sizeof(T) == 2 && avec && bvec && !wide) {
+    if (wbm == 64) launch_timed(wgrad_dma_kernel<64>, grid, s, pr, a, kchunk, dw);
+    else launch_timed(wgrad_dma_kernel<128>, grid, s, pr, a, kchunk, dw);
+  } else if (wide) {
     if (wbm == 64) launch_timed(wgrad_kernel<T, 64, true, true, 8>, grid, s, pr, a, kchunk, dw);
     else launch_timed(wgrad_kernel<T, 128, true, true, 8>, grid, s, pr, a, kchunk, dw);
   } else if (wbm == 64) {
