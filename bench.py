@@ -598,10 +598,22 @@ def main():
         _, psteps, _ = timed_steps(torch, lambda: rc_step(bufs), args.steps, 0, True,
                                    L.lrcnn_debug_profile)
     kern = L.lrcnn_debug_profile_collect()
+    # the same eager steps with the weight gradients on the caller's stream:
+    # every kernel then has the GPU to itself (the default schedule overlaps
+    # each weight gradient with an input gradient, and their event times
+    # include that sharing)
+    L.lrcnn_debug_serial_wgrad(True)
+    try:
+        ms_serial, psteps_s, _ = timed_steps(torch, lambda: rc_step(bufs), args.steps, 1, True,
+                                             L.lrcnn_debug_profile)
+    finally:
+        L.lrcnn_debug_serial_wgrad(False)
+    kern_serial = L.lrcnn_debug_profile_collect()
 
     # dominant kernel: the largest share of the algorithmic FLOPs (the
-    # forward convolution: it runs in FP and in the recompute, where no
-    # other kernel overlaps it, so its event times are its own)
+    # weight gradient at the ResNet-50 workloads, whose event times in the
+    # default schedule include sharing the GPU with an input gradient; the
+    # serial pass above times it alone)
     dom_name, (dom_n, dom_ms, dom_fl) = max(kern.items(), key=lambda kv: kv[1][2])
     bound, peak, unit = PEAK[dts]
     achieved = dom_fl / (dom_ms * 1e-3) / 1e12
@@ -624,6 +636,15 @@ def main():
                             "in an eager pass of the same steps after the timed graph "
                             "replays")),
                 "avg_launch_ms": round(dom_ms / dom_n, 4)}
+    if dom_name in kern_serial:
+        sn, sms, sfl = kern_serial[dom_name]
+        iso = sfl / (sms * 1e-3) / 1e12
+        roofline["alone"] = {
+            "achieved": round(iso, 2), "frac": round(iso / peak, 4),
+            "avg_launch_ms": round(sms / sn, 4),
+            "step_ms": round(ms_serial, 3),
+            "timing": "eager steps with the weight gradients on the caller's stream "
+                      "(no kernel overlaps another)"}
     all_mfma_ms = sum(v[1] for k, v in kern.items() if "reduce" not in k) / psteps
     all_mfma_fl = sum(v[2] for v in kern.values()) / psteps
 
@@ -653,7 +674,9 @@ def main():
                          "per_kernel": {k: {"launches": v[0] // psteps,
                                             "ms": round(v[1] / psteps, 3),
                                             "tflops": round(v[2] / max(v[1], 1e-9) / 1e9, 2)}
-                                        for k, v in sorted(kern.items())}},
+                                        for k, v in sorted(kern.items())},
+                         "alone_ms_per_step": {k: round(v[1] / psteps_s, 3)
+                                               for k, v in sorted(kern_serial.items())}},
         "peak_act_bytes": int(peak_rc),
         "analytic": {k: info[k] for k in ("workspace_bytes", "layerwise_workspace_bytes",
                                           "strip_bytes", "band_cache_bytes",

@@ -36,6 +36,13 @@ void lrcnn_debug_act_fusion(int on);
  * caller's stream. Results are bitwise equal. */
 void lrcnn_debug_fp_pipeline(int on);
 
+/* on != 0: on the calling thread, the backward launches every weight
+ * gradient on the caller's stream, just before the input gradient it would
+ * otherwise overlap, so that a profile times each kernel with the GPU to
+ * itself; on == 0 (default) the weight gradients run on the plan's side
+ * stream. Results are bitwise equal. */
+void lrcnn_debug_serial_wgrad(int on);
+
 /* On the calling thread, the input gradient of a strided convolution
  * (stride s in both directions) is computed as s^2 launches, one per phase
  * of producer rows and columns ((y + pad) mod s), each with only the taps

@@ -24,6 +24,7 @@ thread_local bool g_dry = false;
 // ResNet-50 bfloat16 graph-captured run with it ended in an abort whose
 // cause is not yet known)
 thread_local bool g_no_fp_pipe = true;
+thread_local bool g_serial_wg = false;
 
 #define LAUNCH(call, what)                                                 \
   do {                                                                     \
@@ -907,7 +908,7 @@ int hybrid_backward(Plan &P, const void *x, const void *const *w, const float *c
   Run run(C, C.lw, S_LAYERWISE, ws + P.h_col, ws + P.h_ck, w + c, sc ? sc + c : nullptr,
           sf ? sf + c : nullptr, stream);
   run.dx_f32 = true;
-  if (!g_dry && ensure_side(C)) run.side = (hipStream_t)C.side_stream;
+  if (!g_dry && !g_serial_wg && ensure_side(C)) run.side = (hipStream_t)C.side_stream;
   int st;
   if ((st = run.band_fwd(0, nullptr, nullptr, true, false, true)) != LRCNN_OK) return st;
   if ((st = run.begin_dw()) != LRCNN_OK) return st;
@@ -1002,7 +1003,7 @@ extern "C" int lrcnn_backward_rows(lrcnn_plan_t *plan, const void *x, const void
     return lrcnn_fail(LRCNN_ESTATE,
                       "CARRY backward needs a preceding lrcnn_forward_rows on this plan and workspace");
   Run run(P, P.rc, carry ? S_CARRY : S_RECOMPUTE, workspace, x, w, aff_scale, aff_shift, stream);
-  if (!g_dry && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
+  if (!g_dry && !g_serial_wg && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
   if ((st = run.begin_dw()) != LRCNN_OK) return st;
   float *dxacc = nullptr;
   if (!carry && dx) {
@@ -1048,7 +1049,7 @@ extern "C" int lrcnn_layerwise_reference_gpu(lrcnn_plan_t *plan, const void *x,
   if ((st = check_dw(P, dw)) != LRCNN_OK) return st;
   if ((st = check_ws(P.lw, workspace, ws_bytes)) != LRCNN_OK) return st;
   Run run(P, P.lw, S_LAYERWISE, workspace, x, w, aff_scale, aff_shift, stream);
-  if (!g_dry && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
+  if (!g_dry && !g_serial_wg && ensure_side(P)) run.side = (hipStream_t)P.side_stream;
   // FP keeps every node's full map; BP reads them without recomputing.
   // The pool argmax is produced in FP (bp = true selects its buffer).
   if ((st = run.band_fwd(0, y, mask_out, true)) != LRCNN_OK) return st;
@@ -1072,6 +1073,7 @@ extern "C" int lrcnn_debug_layerwise_map(const lrcnn_plan_t *plan, int32_t node,
 extern "C" void lrcnn_debug_dry_run(int on) { lrcnn::g_dry = on != 0; }
 extern "C" void lrcnn_debug_act_fusion(int on) { lrcnn::g_no_act_fusion = on == 0; }
 extern "C" void lrcnn_debug_fp_pipeline(int on) { lrcnn::g_no_fp_pipe = on == 0; }
+extern "C" void lrcnn_debug_serial_wgrad(int on) { lrcnn::g_serial_wg = on != 0; }
 extern "C" void lrcnn_debug_dgrad_phases(int mode) { lrcnn::set_dgrad_phases(mode); }
 
 extern "C" void lrcnn_debug_profile(int on) { lrcnn::profile_enable(on); }

@@ -282,8 +282,12 @@ struct WgradArgs {
   int overwrite;  // 1: dw = this launch's sum (the first band); 0: dw += it
   FastDiv fw, fr;  // division by Wv and by y1 - y0 (set by the launcher)
   // one K step of BK pixels as a mixed-radix (b, row, column) increment:
-  // BK = wdb * (Wv * R) + wdy * Wv + wdx (set by the launcher)
+  // BK = wdb * (Wv * R) + wdy * Wv + wdx (set by the launcher; with Wp
+  // columns per row for the row-group kernel)
   int wdx, wdy, wdb;
+  // row-group kernel: rows padded to Wp = Wv rounded up to 8 columns, so an
+  // aligned group of 8 pixels never spans two rows (set by the launcher)
+  int Wp;
 };
 int launch_wgrad(int dt, const WgradArgs &a, float *dw, void *stream);
 // K iterations of a weight-gradient launch over K pixels

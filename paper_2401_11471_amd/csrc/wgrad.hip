@@ -315,7 +315,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
 // every copy starts at a k row that is a multiple of 4 (W = 128) or 8
 // (W = 64), sw(k) depends on the lane alone, and so does the vector a
 // thread fetches: one output-channel vector of A and one (tap, channel)
-// vector of B per thread, over two or one A rows and two B rows per tile.
+// vector of B per thread.
 #ifndef LRCNN_WG_DMA
 #define LRCNN_WG_DMA 1
 #endif
@@ -325,26 +325,33 @@ __global__ __launch_bounds__(256, LRCNN_WG_OCC) void wgrad_kernel(WgradArgs a, i
 #ifndef LRCNN_WG_DMA_OCC
 #define LRCNN_WG_DMA_OCC 2
 #endif
+// The K index runs over padded pixels q = (b, y, x) with x in [0, Wp),
+// Wp = Wv rounded up to a multiple of 8; columns x >= Wv read zeros. A K step's 32 pixels are four
+// aligned groups of 8, one per wave, and such a group lies in one row: the
+// wave walks its group's (b, y, x) and base offsets with scalar
+// instructions, and a lane only adds a constant of its own (its pixel's
+// place in the group, its channel vector, its tap) and tests its bounds
+// against scalar limits. Wave w's A copies fill tile rows 8w .. 8w+7 and
+// so do its B copies, so both operands of a tile row hold the same pixel.
 template <int WBM>
-__global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_dma_kernel(WgradArgs a,
-                                                                          int kchunk,
-                                                                          float *dw) {
+__global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_rowg_kernel(WgradArgs a,
+                                                                           int kchunk,
+                                                                           float *dw) {
   using T = bf16;
   constexpr int E = 8, BK = 32, BN = 128, ST = LRCNN_WG_DMA_ST;
   static_assert(ST == 3 || ST == 4, "ring depth");
   constexpr int FBN = WBM == 128 ? 128 : 64, NB = FBN / 64;
   constexpr int VA = WBM / E, RA = 64 / VA;  // vectors per A row, A rows per copy
-  constexpr int NIA = BK / RA / 4;           // A copies per wave per tile
-  constexpr int VB = BN / E, RB = 64 / VB;   // the same for B
-  constexpr int NIB = BK / RB / 4;
-  constexpr int LD = NIA + NIB;              // copies per thread per tile
-  constexpr uint32_t ASB = BK * WBM * 2, BSB = BK * BN * 2;  // stage bytes
+  constexpr int NIA = 8 / RA;                // A copies per wave per tile
+  constexpr int NIB = 2;                     // B copies per wave per tile (4 rows each)
+  constexpr int LD = NIA + NIB;
+  constexpr uint32_t ASB = BK * WBM * 2, BSB = BK * BN * 2;
   static_assert(4 * NIA * 1024 == ASB && 4 * NIB * 1024 == BSB, "copy cover");
   __shared__ __align__(16) char smem[ST * (ASB + BSB)];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int R = a.y1 - a.y0;
-  const int K = a.B * R * a.Wv;
+  const int R = a.y1 - a.y0, Wp = a.Wp;
+  const int K = a.B * R * Wp;  // padded pixels
   const int N = a.kh * a.kw * a.Ci;
   const TileId tl = xcd_tile(false);
   const int m0 = tl.x * WBM, n0 = tl.y * BN;
@@ -355,77 +362,103 @@ __global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_dma_kernel(WgradA
   const long long srow = (long long)a.src.W * a.src.C;
   constexpr long long ES = 2;
 
-  // A: k row lane / VA of each copy, output-channel vector fixed per thread
-  const int ka = lane / VA;
-  const int ova = m0 + E * ((lane % VA) ^ (KM<T, WBM>::sw(ka) << 2));
+  // per-lane constants. A: group place kbA[j] (a lane whose channel vector
+  // is past C_out gets a place no group reaches), channel vector at ova
+  constexpr int FAR = 1 << 30;
+  int kbA[NIA];
+  uint32_t lA[NIA];
+  const int ova = m0 + E * ((lane % VA) ^ (KM<T, WBM>::sw(lane / VA) << 2));
   const bool ovok = ova < a.Co;
-  long long aoff[NIA];
-  int kar[NIA];
 #pragma unroll
   for (int j = 0; j < NIA; ++j) {
-    kar[j] = (wave * NIA + j) * RA + ka;
-    aoff[j] = ((long long)(kbeg + kar[j]) * a.Co + ova) * ES;
+    kbA[j] = j * RA + lane / VA;
+    lA[j] = (uint32_t)(((long long)kbA[j] * a.Co + ova) * ES);
+    kbA[j] = ovok ? kbA[j] : FAR;
   }
-  const long long adk = (long long)BK * a.Co * ES;
-  // B: (tap, channel) vector fixed per thread, two pixels walked per step
-  const int kb = lane / VB;
-  const int nb = n0 + E * ((lane % VB) ^ (KM<T, BN>::sw(kb) << 2));
+  // B: group place kbB[j], (tap, channel) vector nb; column offset of the
+  // pixel under the tap relative to the group's first pixel
+  const int nb = n0 + E * ((lane % 16) ^ (KM<T, BN>::sw(lane / 16) << 2));
   const int tap = nb / a.Ci;
   const int bti = tap / a.kw, btj = tap - (tap / a.kw) * a.kw;
   const bool bnok = nb < N;
-  const long long btoff =
-      ((long long)bti * srow + (long long)btj * a.src.C + (nb - tap * a.Ci)) * ES;
-  const int dxb = a.wdx * a.sw, wxb = a.Wv * a.sw;
-  const int dyb = a.wdy * a.sh, ryb = R * a.sh;
-  const long long pd0 =
-      ((long long)a.wdb * a.src.bs + (long long)dyb * srow + (long long)dxb * a.src.C) * ES;
-  const long long pd1 = ((long long)a.sh * srow - (long long)wxb * a.src.C) * ES;
-  const long long pd2 = (a.src.bs - (long long)ryb * srow) * ES;
-  int wx[NIB], wy[NIB], ybase[NIB], xbase[NIB], kbr[NIB];
-  long long poff[NIB];
+  int kbB[NIB], bx[NIB];
+  uint32_t lB[NIB];
 #pragma unroll
   for (int j = 0; j < NIB; ++j) {
-    kbr[j] = (wave * NIB + j) * RB + kb;
-    uint32_t t, x, yy, b;
-    fdiv_qr((uint32_t)(kbeg + kbr[j]), a.fw, t, x);
-    fdiv_qr(t, a.fr, b, yy);
-    wx[j] = (int)x, wy[j] = (int)yy;
-    ybase[j] = (a.y0 + wy[j]) * a.sh - a.ph + bti;
-    xbase[j] = wx[j] * a.sw - a.pw + btj;
-    poff[j] = ((long long)b * a.src.bs + (long long)(ybase[j] - bti - a.src.row0) * srow +
-               (long long)(xbase[j] - btj) * a.src.C) * ES + btoff;
+    kbB[j] = 4 * j + lane / 16;
+    bx[j] = btj + kbB[j] * a.sw;
+    lB[j] = (uint32_t)(((long long)bti * srow + (long long)bx[j] * a.src.C + (nb - tap * a.Ci)) *
+                       ES);
+    kbB[j] = bnok ? kbB[j] : FAR;
   }
+  // the wave's group: first pixel q = kbeg + 8 wave of the first tile
+  int xs, ys, bs_;
+  {
+    uint32_t t, x, yy, b;
+    fdiv_qr((uint32_t)(kbeg + 8 * wave), a.fw, t, x);
+    fdiv_qr(t, a.fr, b, yy);
+    xs = __builtin_amdgcn_readfirstlane((int)x);
+    ys = __builtin_amdgcn_readfirstlane((int)yy);
+    bs_ = __builtin_amdgcn_readfirstlane((int)b);
+  }
+  // scalar walk state: A byte offset of the group's first pixel, B byte
+  // offset of the source position under tap (0, 0), that position's row
+  // and column, and the pixels of the launch's range left from the group
+  long long offA = ((long long)(bs_ * R + ys) * a.Wv + xs) * a.Co * ES;
+  int sy = (a.y0 + ys) * a.sh - a.ph, sx = xs * a.sw - a.pw;
+  long long offB = ((long long)bs_ * a.src.bs + (long long)(sy - a.src.row0) * srow +
+                    (long long)sx * a.src.C) * ES;
+  int kl = kend - (kbeg + 8 * wave);  // pixels of the range from the group on
+  // per-step increments (BK = wdb (R Wp) + wdy Wp + wdx padded pixels)
+  const long long dA0 = ((long long)(a.wdb * R + a.wdy) * a.Wv + a.wdx) * a.Co * ES;
+  const long long dA1 = (long long)(a.Wv - Wp) * a.Co * ES;
+  const int dyb = a.wdy * a.sh, ryb = R * a.sh;
+  const long long dB0 =
+      ((long long)a.wdb * a.src.bs + (long long)dyb * srow + (long long)a.wdx * a.sw * a.src.C) *
+      ES;
+  const long long dB1 = ((long long)a.sh * srow - (long long)Wp * a.sw * a.src.C) * ES;
+  const long long dB2 = (a.src.bs - (long long)ryb * srow) * ES;
+  const int dsx = a.wdx * a.sw, wsx = Wp * a.sw;
   const uint32_t lds_a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
   const uint32_t lds_b = lds_a + ST * ASB;
   const void *zblk = &g_zero16[0];
   asm volatile("" : "+s"(zblk));
-  int k0 = kbeg;
-  // copies of the tile at pixels [k0, k0 + BK) into stage st
+  // (bounds as unsigned compares: v in [0, L) iff (unsigned)v < L)
   auto gload = [&](int st) {
+    const int lim = min(a.Wv - xs, kl);  // group places inside the row and the range
+    const uint32_t yy = (uint32_t)(sy + bti);
 #pragma unroll
-    for (int j = 0; j < NIA; ++j) {
-      load16_lds_a(dc + aoff[j], (k0 + kar[j] < kend) & ovok,
+    for (int j = 0; j < NIA; ++j)
+      load16_lds_a(dc + offA + lA[j], kbA[j] < lim,
                    lds_a + st * ASB + (uint32_t)(wave * NIA + j) * 1024u, zblk);
-      aoff[j] += adk;
-    }
 #pragma unroll
     for (int j = 0; j < NIB; ++j) {
-      const bool ok = (k0 + kbr[j] < kend) & bnok & (ybase[j] >= 0) & (ybase[j] < a.Hs) &
-                      (xbase[j] >= 0) & (xbase[j] < a.Ws);
-      load16_lds_a(src + poff[j], ok, lds_b + st * BSB + (uint32_t)(wave * NIB + j) * 1024u,
-                   zblk);
-      // next K step: pixel + BK (column and row carries select the wraps)
-      wx[j] += a.wdx;
-      const bool cx = wx[j] >= a.Wv;
-      wx[j] -= cx ? a.Wv : 0;
-      xbase[j] += dxb - (cx ? wxb : 0);
-      wy[j] += a.wdy + (cx ? 1 : 0);
-      const bool cy = wy[j] >= R;
-      wy[j] -= cy ? R : 0;
-      ybase[j] += dyb + (cx ? a.sh : 0) - (cy ? ryb : 0);
-      poff[j] += pd0 + (pd1 & -(long long)cx) + (pd2 & -(long long)cy);
+      const bool ok = (kbB[j] < lim) & (yy < (uint32_t)a.Hs) & ((uint32_t)(sx + bx[j]) < (uint32_t)a.Ws);
+      load16_lds_a(src + offB + lB[j], ok,
+                   lds_b + st * BSB + (uint32_t)(wave * NIB + j) * 1024u, zblk);
     }
-    k0 += BK;
+    // next tile: the group moves BK padded pixels on (scalar; the row and
+    // image carries are rare unless rows are shorter than a K step)
+    xs += a.wdx;
+    ys += a.wdy;
+    offA += dA0;
+    offB += dB0;
+    sy += dyb;
+    sx += dsx;
+    kl -= BK;
+    if (__builtin_expect(xs >= Wp, 0)) {
+      xs -= Wp;
+      ys += 1;
+      offA += dA1;
+      offB += dB1;
+      sy += a.sh;
+      sx -= wsx;
+    }
+    if (__builtin_expect(ys >= R, 0)) {
+      ys -= R;
+      offB += dB2;
+      sy -= ryb;
+    }
   };
   auto As = [&](int st) { return (const T *)(smem + st * ASB); };
   auto Bs = [&](int st) { return (const T *)(smem + ST * ASB + st * BSB); };
@@ -442,10 +475,6 @@ __global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_dma_kernel(WgradA
   const int n = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
   using FR = Frag<T, FBN, 4, 1, 1, WBM, BN>;
   FR f0, f1;
-  // Tile t+ST is copied into the stage of tile t once every wave has read
-  // tile t; a step waits only for tile t+1, so a copy has ST-1 steps to
-  // arrive. wait_tiles(k) leaves the copies of the k most recent tiles in
-  // flight.
   auto wait_tiles = [](int k) {
     if (ST > 3 && k >= 2) wait_vmcnt<(ST > 3 ? 2 : 0) * LD>();
     else if (k == 1) wait_vmcnt<LD>();
@@ -457,7 +486,7 @@ __global__ __launch_bounds__(256, LRCNN_WG_DMA_OCC) void wgrad_dma_kernel(WgradA
   wait_tiles(min(n, ST) - 1);
   __syncthreads();
   if (n > 0) f0.load(As(0), Bs(0), wm, wn, lane);
-  int sc = 0;  // stage of tile t
+  int sc = 0;
   auto dstep = [&](int t, FR &cur, FR &nxt) {
     const int s1 = sc == ST - 1 ? 0 : sc + 1;
     if (t + 1 < n) {
@@ -558,6 +587,7 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
   // the partial sums; a wide K step rounds each chunk up to its own width,
   // which never adds splits)
   const bool wide = LRCNN_WG_KR == 8 && sizeof(T) == 2 && avec && bvec;
+  const bool rowg = LRCNN_WG_DMA && sizeof(T) == 2 && avec && bvec && !wide;
   const int BKL = wide ? 8 * Cfg<T>::E : BK;
   a.wdx = BKL % a.Wv;
   a.wdy = (BKL / a.Wv) % (a.y1 - a.y0);
@@ -575,9 +605,24 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
     pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                          (avec && bvec ? ", vec>" : ", scalar>"),
                      2.0 * K * a.Co * N, s);
-  if (LRCNN_WG_DMA && sizeof(T) == 2 && avec && bvec && !wide) {
-    if (wbm == 64) launch_timed(wgrad_dma_kernel<64>, grid, s, pr, a, kchunk, dw);
-    else launch_timed(wgrad_dma_kernel<128>, grid, s, pr, a, kchunk, dw);
+  if (rowg) {
+    // padded pixels: rows of Wp = Wv rounded up to 8 columns; the split
+    // count is the estimate's, each chunk a whole number of K steps
+    a.Wp = (a.Wv + 7) / 8 * 8;
+    a.fw = fast_div((uint32_t)a.Wp);
+    a.wdx = BK % a.Wp;
+    a.wdy = (BK / a.Wp) % (a.y1 - a.y0);
+    a.wdb = BK / (a.Wp * (a.y1 - a.y0));
+    const long long Kp = (long long)a.B * (a.y1 - a.y0) * a.Wp;
+    if (Kp >= (1ll << 31)) return (int)hipErrorInvalidValue;
+    const long long KTp = (Kp + BK - 1) / BK;
+    const int kchunk_p = (int)((KTp + wt.splits - 1) / wt.splits * BK);
+    const int splits_p = (int)((Kp + kchunk_p - 1) / kchunk_p);
+    if (!split_fits(splits_p, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
+    dim3 gp((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits_p);
+    if (wbm == 64) launch_timed(wgrad_rowg_kernel<64>, gp, s, pr, a, kchunk_p, dw);
+    else launch_timed(wgrad_rowg_kernel<128>, gp, s, pr, a, kchunk_p, dw);
+    splits = splits_p;
   } else if (wide) {
     if (wbm == 64) launch_timed(wgrad_kernel<T, 64, true, true, 8>, grid, s, pr, a, kchunk, dw);
     else launch_timed(wgrad_kernel<T, 128, true, true, 8>, grid, s, pr, a, kchunk, dw);

@@ -108,6 +108,8 @@ def _load():
     lib.lrcnn_debug_fp_pipeline.restype = None
     lib.lrcnn_debug_act_fusion.argtypes = [C.c_int]
     lib.lrcnn_debug_act_fusion.restype = None
+    lib.lrcnn_debug_serial_wgrad.argtypes = [C.c_int]
+    lib.lrcnn_debug_serial_wgrad.restype = None
     lib.lrcnn_debug_dgrad_phases.argtypes = [C.c_int]
     lib.lrcnn_debug_dgrad_phases.restype = None
     lib.lrcnn_debug_profile.argtypes = [C.c_int]
@@ -139,7 +141,7 @@ EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_forward_rows_static",
            "lrcnn_backward_rows", "lrcnn_layerwise_reference_gpu", "lrcnn_last_error",
            "lrcnn_debug_dry_run", "lrcnn_debug_fp_pipeline", "lrcnn_debug_act_fusion",
-           "lrcnn_debug_dgrad_phases",
+           "lrcnn_debug_dgrad_phases", "lrcnn_debug_serial_wgrad",
            "lrcnn_debug_profile",
            "lrcnn_debug_profile_collect", "lrcnn_debug_profile_entry",
            "lrcnn_debug_layerwise_map")
@@ -323,6 +325,12 @@ def lrcnn_debug_fp_pipeline(on):
     """Test hook: forward bands pipelined on two streams (on) or sequential (off,
     the default)."""
     LIB.lrcnn_debug_fp_pipeline(1 if on else 0)
+
+
+def lrcnn_debug_serial_wgrad(on):
+    """Test hook: weight gradients on the caller's stream (on) or on the plan's
+    side stream beside the input gradients (off, the default)."""
+    LIB.lrcnn_debug_serial_wgrad(1 if on else 0)
 
 
 def lrcnn_debug_act_fusion(on):

@@ -224,3 +224,20 @@ def test_backward_without_forward_is_rejected():
         L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, ws)
     assert e.value.code == -5
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", [F32, BF16])
+def test_serial_weight_gradients_equal_overlapped(dtype):
+    """Weight gradients on the caller's stream (the profiling schedule) give
+    the same bits as the default schedule on the side stream."""
+    nodes, inp = _inputs("resnet_like", dtype, seed=17)
+    base = gpu_run(nodes, inp, L.CARRY, 4, twin=False)
+    L.lrcnn_debug_serial_wgrad(True)
+    try:
+        ser = gpu_run(nodes, inp, L.CARRY, 4, twin=False)
+    finally:
+        L.lrcnn_debug_serial_wgrad(False)
+    np.testing.assert_array_equal(base["dx"], ser["dx"])
+    for v in range(1, len(nodes)):
+        if base["dw"][v] is not None:
+            np.testing.assert_array_equal(base["dw"][v], ser["dw"][v])

@@ -50,6 +50,8 @@ def bench_name(mangled: str) -> str:
                 "1x1" if m.group(6) == "true" else "vec")
         return (f"conv_gemm_kernel<{m.group(1)}, {m.group(2)}, "
                 f"{'dgrad' if m.group(3) == 'true' else 'fwd'}, {kind}>")
+    if re.match(r"wgrad_rowg_kernel<\d+>", n):
+        return "wgrad_kernel<bf16, vec>"
     m = re.match(r"wgrad_kernel<(\w+), (?:\d+, )?(true|false), (true|false)(?:, \d+)?>", n)
     if m:
         vec = m.group(2) == "true" and m.group(3) == "true"
