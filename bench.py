@@ -158,6 +158,10 @@ def timed_steps(torch, step, steps, warmup, eager, profile=None):
     the graph and hold the last replay's times. Returns (ms, profiled steps,
     graph)."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # an idle gap before each timed phase, so that a kernel trace of the
+    # run can tell the phases apart
+    torch.cuda.synchronize()
+    time.sleep(0.1)
     if eager:
         for _ in range(warmup):
             step()

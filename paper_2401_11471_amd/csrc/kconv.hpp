@@ -207,6 +207,30 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   asm volatile("" : "+s"(zblk));
 
   uint4 ra[NA], rb[NBL];
+  // 1x1 forward with a fused residual add (64-wide tiles): the epilogue's
+  // residual vectors are fetched here, before the K loop, so their latency
+  // overlaps it instead of following it (a 1x1 layer's loop is a few
+  // steps). Thread rows r = tid / (BN / E) + i * RPR, as in the epilogue.
+  constexpr bool PRE = ONE && !DGRAD && BN == 64 && HR == BM && sizeof(T) == 2;
+  constexpr int PCR = BN / E, RPR = 256 / PCR, PRN = PRE ? BM / RPR : 1;
+  uint4 pre_res[PRN];
+  const bool pre = PRE && a.res.p && (a.N % E) == 0;
+  if (PRE && pre) {
+    const long long drw = (long long)a.dst.W * a.N;
+    const int pn = n0 + (tid % PCR) * E;
+#pragma unroll
+    for (int i = 0; i < PRN; ++i) {
+      const int m = m0 + tid / PCR + RPR * i;
+      const bool ok = m < M && pn < a.N;
+      uint32_t t_, x_, b_, y_;
+      fdiv_qr((uint32_t)(ok ? m : 0), a.fw, t_, x_);
+      fdiv_qr(t_, a.fr, b_, y_);
+      const int x = a.px0 + (int)x_, y = a.y0 + (int)y_, b = (int)b_;
+      const long long ro = b * a.res.bs + (y - a.res.row0) * drw + (long long)x * a.N + pn;
+      pre_res[i] = load16z(a.res.p, ro * (long long)sizeof(T), ok);
+    }
+  }
+
   // bounds tests use non-short-circuit '&' so that no test becomes a branch
   // (st: the LDS stage a direct copy writes)
   auto gload = [&](int st) {
@@ -557,7 +581,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       }
     }
     __syncthreads();
-    for (int r = h0 + tid / CPR; r < h0 + HR; r += RPP) {
+#pragma unroll
+    for (int i = 0; i < HR / RPP; ++i) {
+      const int r = h0 + tid / CPR + RPP * i;
       const int m = m0 + r;
       if (m >= M || n >= a.N) continue;
       uint32_t t_, x_, b_, y_;
@@ -568,14 +594,16 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
       uint4 q = *(const uint4 *)&Ct[(r - h0) * CP + cc * E];
       if (a.res.p) {
         // fused residual add: the stored conv value plus the add's other
-        // input, then the add's ReLU
+        // input (prefetched for 1x1 layers), then the add's ReLU
         union {
           uint4 u;
           T e[E];
         } cv, rv;
         cv.u = q;
-        rv.u = *(const uint4 *)((const T *)a.res.p + b * a.res.bs + (y - a.res.row0) * drow +
-                                (long long)x * a.N + n);
+        if (PRE) rv.u = pre_res[i];
+        else
+          rv.u = *(const uint4 *)((const T *)a.res.p + b * a.res.bs +
+                                  (y - a.res.row0) * drow + (long long)x * a.N + n);
 #pragma unroll
         for (int e = 0; e < E; ++e) {
           float v = ldf(&cv.e[e]) + ldf(&rv.e[e]);
