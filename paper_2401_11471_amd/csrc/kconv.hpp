@@ -30,9 +30,9 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // forward with 16-byte rows: both operands copied straight from global
   // memory into their LDS stage (no registers, no LDS writes by the wave).
   // The K vector of a thread's tile rows is then chosen so that its
-  // swizzled LDS slot is lane & 3: each wave's rows fill 1 KiB of LDS in
+  // swizzled LDS slot is lane mod KR: each wave's rows fill 1 KiB of LDS in
   // lane order, the layout of a direct copy.
-  constexpr bool LANE_SLOT = KR == 4 && LRCNN_SWZ;
+  constexpr bool LANE_SLOT = (KR == 4 || KR == 8) && KR == LRCNN_CONV_KR && LRCNN_SWZ;
   // Input gradient, stride 1, bfloat16: the same, with the weights' k-major
   // tile copied in lane order too (k rows of BN unpadded elements; a
   // thread's column vector is the one its lane's swizzled slot holds).
@@ -73,8 +73,12 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   const bool tpk = !VEC && !DGRAD && a.tpack;
   const int KT = tpk ? (taps + KR - 1) / KR : taps * CB;
   // K vector of this thread's tile rows: (l & 3) ^ ((l >> 4) & 3) for lane
-  // l puts it in LDS slot l & 3 (the swizzle is an XOR with (row >> 2) & 3)
-  const int kv = LANE_SLOT ? ((tid & 3) ^ ((tid >> 4) & 3)) : tid % KR;
+  // l puts it in LDS slot l & 3 (the swizzle is an XOR with (row >> 2) & 3;
+  // rows are l / 4 + 64 i); with 8 vectors per row (l & 7) ^ ((l >> 4) & 7)
+  // puts it in slot l & 7 (XOR with (row >> 1) & 7, rows l / 8 + 32 i)
+  const int kv = !LANE_SLOT ? tid % KR
+                 : KR == 8   ? ((tid & 7) ^ ((tid >> 4) & 7))
+                             : ((tid & 3) ^ ((tid >> 4) & 3));
   const int wrow = wave * (64 / KR);  // first tile row of this wave's pass
   const T *src = (const T *)a.src.p;
   const T *w = (const T *)a.w;

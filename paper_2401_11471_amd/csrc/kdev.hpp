@@ -92,11 +92,15 @@ struct Cfg {
   static constexpr int LDK = LRCNN_SWZ ? BK : BK + E;  // LDS pitch in elements
 };
 // Row-major LDS tiles with LRCNN_SWZ: no padding; the 16-byte vector v of
-// row r is stored at slot v ^ ((r >> 2) & 3), which keeps the 16-lane
-// phases of 16-byte reads (16 consecutive rows, one vector) and writes (4
-// rows x 4 vectors) on distinct banks. Needs 4 vectors per row.
+// row r is stored at slot v ^ ((r >> 2) & 3) (4 vectors per row), which
+// keeps the 16-lane phases of 16-byte reads (16 consecutive rows, one
+// vector) and writes (4 rows x 4 vectors) on distinct banks. With 8 vectors
+// per row (LRCNN_CONV_KR = 8) the slot is v ^ ((r >> 1) & 7): the 8 rows of
+// one parity among 16 consecutive rows then take 8 distinct slots, and the
+// two parities sit in the two 32-bank halves.
 __device__ __forceinline__ int swz(int row, int vec) {
-  return LRCNN_SWZ ? (vec ^ ((row >> 2) & 3)) : vec;
+  if (!LRCNN_SWZ) return vec;
+  return LRCNN_CONV_KR == 8 ? (vec ^ ((row >> 1) & 7)) : (vec ^ ((row >> 2) & 3));
 }
 
 constexpr int BM = 128;
