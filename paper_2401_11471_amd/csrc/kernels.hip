@@ -478,12 +478,36 @@ __global__ void rows_copy_batch_kernel(CopyBatch cb) {
   }
 }
 
+// The same copy in whole 16-byte vectors (storage dtype unchanged, every
+// row and view base 16-byte aligned): one load and one store per thread.
+template <typename T>
+__global__ void rows_copy_batch16_kernel(CopyBatch cb) {
+  constexpr int V = 16 / (int)sizeof(T);
+  GRID_STRIDE(idx, cb.start[cb.n]) {
+    int s = 0;
+    while (s + 1 < cb.n && idx >= cb.start[s + 1]) ++s;
+    const CopySeg &g = cb.seg[s];
+    int b, y, in;
+    cb.it[s].at(idx - cb.start[s], V, b, y, in);
+    *(uint4 *)((T *)g.dst.p + view_off(g.dst, b, y, in)) =
+        *(const uint4 *)((const T *)g.src.p + view_off(g.src, b, y, in));
+  }
+}
+
 int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream) {
   if (n <= 0) return 0;
   if (n > kMaxCopySegs) return (int)hipErrorInvalidValue;
   CopyBatch cb{};
-  int V = 4;
+  // 16-byte vectors when every row holds whole vectors and every view base
+  // is 16-byte aligned, else 4 or 1 elements per thread
+  const int V16 = dt == DT_F32 ? 4 : 8;
+  bool wide = true;
   for (int i = 0; i < n; ++i)
+    wide = wide && ((long long)segs[i].W * segs[i].C) % V16 == 0 &&
+           segs[i].src.bs % V16 == 0 && segs[i].dst.bs % V16 == 0 &&
+           ((uintptr_t)segs[i].src.p & 15) == 0 && ((uintptr_t)segs[i].dst.p & 15) == 0;
+  int V = wide ? V16 : 4;
+  for (int i = 0; i < n && !wide; ++i)
     if (((long long)segs[i].W * segs[i].C) % 4 != 0) V = 1;
   cb.n = n;
   cb.start[0] = 0;
@@ -496,10 +520,12 @@ int launch_rows_copy_batch(int dt, const CopySeg *segs, int n, void *stream) {
   hipStream_t s = (hipStream_t)stream;
   const unsigned g = grid_for(cb.start[n]);
   if (dt == DT_F32) {
-    if (V == 4) rows_copy_batch_kernel<float, 4><<<g, 256, 0, s>>>(cb);
+    if (wide) rows_copy_batch16_kernel<float><<<g, 256, 0, s>>>(cb);
+    else if (V == 4) rows_copy_batch_kernel<float, 4><<<g, 256, 0, s>>>(cb);
     else rows_copy_batch_kernel<float, 1><<<g, 256, 0, s>>>(cb);
   } else {
-    if (V == 4) rows_copy_batch_kernel<bf16, 4><<<g, 256, 0, s>>>(cb);
+    if (wide) rows_copy_batch16_kernel<bf16><<<g, 256, 0, s>>>(cb);
+    else if (V == 4) rows_copy_batch_kernel<bf16, 4><<<g, 256, 0, s>>>(cb);
     else rows_copy_batch_kernel<bf16, 1><<<g, 256, 0, s>>>(cb);
   }
   return (int)hipGetLastError();
@@ -566,11 +592,41 @@ __global__ void pad_channels_kernel(View src, View dst, int C, int Cp, RowIter i
   }
 }
 
+// One pixel per thread when the padded pixel is one 16-byte vector (bf16
+// with 8 channels, float32 with 4): C loads and one 16-byte store.
+template <typename T>
+__global__ void pad_channels16_kernel(View src, View dst, int C, RowIter it) {
+  constexpr int CP = 16 / (int)sizeof(T);
+  GRID_STRIDE(idx, it.total) {
+    int b, y, in;
+    it.at(idx, CP, b, y, in);
+    const int x = in / CP;
+    union {
+      uint4 u;
+      T e[CP];
+    } v;
+    const T *sp = (const T *)src.p + view_off(src, b, y, x * C);
+#pragma unroll
+    for (int c = 0; c < CP; ++c) v.e[c] = c < C ? sp[c] : (T)0;
+    *(uint4 *)((T *)dst.p + view_off(dst, b, y, in)) = v.u;
+  }
+}
+
 int launch_pad_channels(int dt, View src, View dst, int C, int Cp, int B, int r0, int r1,
                         int W, void *stream) {
+  hipStream_t s = (hipStream_t)stream;
+  if (Cp * (dt == DT_F32 ? 4 : 2) == 16 && C <= Cp && dst.bs % Cp == 0 &&
+      ((uintptr_t)dst.p & 15) == 0) {
+    RowIter iv = row_iter(B, r0, r1, W, Cp, Cp);
+    if (iv.total <= 0) return 0;
+    if (dt == DT_F32)
+      pad_channels16_kernel<float><<<grid_for(iv.total), 256, 0, s>>>(src, dst, C, iv);
+    else
+      pad_channels16_kernel<bf16><<<grid_for(iv.total), 256, 0, s>>>(src, dst, C, iv);
+    return (int)hipGetLastError();
+  }
   RowIter it = row_iter(B, r0, r1, W, Cp, 1);
   if (it.total <= 0) return 0;
-  hipStream_t s = (hipStream_t)stream;
   if (dt == DT_F32)
     pad_channels_kernel<float><<<grid_for(it.total), 256, 0, s>>>(src, dst, C, Cp, it);
   else
