@@ -32,7 +32,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   // The K vector of a thread's tile rows is then chosen so that its
   // swizzled LDS slot is lane mod KR: each wave's rows fill 1 KiB of LDS in
   // lane order, the layout of a direct copy.
-  constexpr bool LANE_SLOT = (KR == 4 || KR == 8) && KR == LRCNN_CONV_KR && LRCNN_SWZ;
+  constexpr bool LANE_SLOT = (KR == 4 || KR == 8) && LRCNN_SWZ;
   // Input gradient, stride 1, bfloat16: the same, with the weights' k-major
   // tile copied in lane order too (k rows of BN unpadded elements; a
   // thread's column vector is the one its lane's swizzled slot holds).
@@ -390,7 +390,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
   auto store = [&](int st) {
 #pragma unroll
     for (int i = 0; i < NA; ++i)
-      *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + swz(tid / KR + RS * i, kv) * E]) = ra[i];
+      *(uint4 *)(&As[st][(tid / KR + RS * i) * LDK + swz<KR>(tid / KR + RS * i, kv) * E]) = ra[i];
 #pragma unroll
     for (int j = 0; j < NBL; ++j) {
       if (BKM) {
@@ -405,7 +405,7 @@ __global__ __launch_bounds__(256, sizeof(T) == 2 ? 3 : 2) void conv_gemm_kernel(
         for (int e = 0; e < E; ++e)
           Bs[st][((tid % BV) * E + e) * LDK + bk0 + BKS * j] = t.e[e];
       } else {
-        *(uint4 *)(&Bs[st][(tid / KR + RS * j) * LDK + swz(tid / KR + RS * j, kv) * E]) = rb[j];
+        *(uint4 *)(&Bs[st][(tid / KR + RS * j) * LDK + swz<KR>(tid / KR + RS * j, kv) * E]) = rb[j];
       }
     }
   };
@@ -813,16 +813,18 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   if (M <= 0 || a.N <= 0) return 0;
   // (the 16-byte loaders test taps against a 64-bit mask: larger kernels
   // take the element-wise loader)
-  const bool vec = (a.KC % CF::E) == 0 && (!DGRAD || (a.N % CF::E) == 0) &&
-                   a.kh * a.kw <= 64 && a.kw < 64;
-  a.tpack = !vec && conv_tap_packed(a.KC, (int)sizeof(T), DGRAD);
+  const int es = (int)sizeof(T);
+  const bool vec = conv_vec(a.kh, a.kw, a.KC, a.N, es, DGRAD);
+  a.tpack = !vec && conv_tap_packed(a.KC, es, DGRAD);
   a.fkw = fast_div((uint32_t)a.kw);
-  const int KT = a.tpack ? (a.kh * a.kw + KR - 1) / KR : a.kh * a.kw * ((a.KC + CF::BK - 1) / CF::BK);
+  // K step width of this launch (the planner counts iterations the same way)
+  const int kr = conv_kr(a.kh, a.kw, a.KC, a.N, es, DGRAD);
+  const int KT = conv_k_iters(a.kh * a.kw, a.KC, es, DGRAD, kr);
   // a fixed split count (the layer's, for the forward) or the estimate's
   if (a.splits > 0 && !split_valid(KT, a.splits)) return (int)hipErrorInvalidValue;
   const ConvTiles ct = a.splits > 0
-                           ? conv_tiles_split(M, a.N, KT, a.splits, (int)sizeof(T))
-                           : conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, (int)sizeof(T));
+                           ? conv_tiles_split(M, a.N, KT, a.splits, es, kr)
+                           : conv_tiles(M, a.N, KT, a.part ? a.part_bytes : 0, es, kr);
   const int bn = ct.bn;
   const int splits = ct.splits;
   // a fused residual add needs the vector epilogues of the forward
@@ -853,7 +855,17 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   // (a phase of it is dense)
   const bool s1 = !DGRAD || (a.sh == 1 && a.sw == 1) || a.pst > 1;
   const bool one = vec && s1 && a.kh == 1 && a.kw == 1;
-  if (bn == 64) {
+  bool done = false;
+  if constexpr (!DGRAD && sizeof(T) == 2 && LRCNN_CONV_KR_WIN != KR) {
+    // bfloat16 forward of a windowed kernel: wider K steps, 64-wide tiles
+    if (kr != KR) {
+      if (bn != 64 || !vec || one) return (int)hipErrorInvalidValue;
+      launch_timed(conv_gemm_kernel<T, 64, LRCNN_CONV_KR_WIN, false, true, true>, grid, s, pr, a);
+      done = true;
+    }
+  }
+  if (done) {
+  } else if (bn == 64) {
     if (!s1) {
       if (vec) launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, true, false>, grid, s, pr, a);
       else launch_timed(conv_gemm_kernel<T, 64, KR, DGRAD, false, false>, grid, s, pr, a);

@@ -94,13 +94,14 @@ struct Cfg {
 // Row-major LDS tiles with LRCNN_SWZ: no padding; the 16-byte vector v of
 // row r is stored at slot v ^ ((r >> 2) & 3) (4 vectors per row), which
 // keeps the 16-lane phases of 16-byte reads (16 consecutive rows, one
-// vector) and writes (4 rows x 4 vectors) on distinct banks. With 8 vectors
-// per row (LRCNN_CONV_KR = 8) the slot is v ^ ((r >> 1) & 7): the 8 rows of
-// one parity among 16 consecutive rows then take 8 distinct slots, and the
-// two parities sit in the two 32-bank halves.
+// vector) and writes (4 rows x 4 vectors) on distinct banks. With KR = 8
+// vectors per row the slot is v ^ ((r >> 1) & 7): the 8 rows of one parity
+// among 16 consecutive rows then take 8 distinct slots, and the two
+// parities sit in the two 32-bank halves.
+template <int KR>
 __device__ __forceinline__ int swz(int row, int vec) {
   if (!LRCNN_SWZ) return vec;
-  return LRCNN_CONV_KR == 8 ? (vec ^ ((row >> 1) & 7)) : (vec ^ ((row >> 2) & 3));
+  return KR == 8 ? (vec ^ ((row >> 1) & 7)) : (vec ^ ((row >> 2) & 3));
 }
 
 constexpr int BM = 128;
@@ -168,7 +169,7 @@ struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
         const float4 *p = (const float4 *)(As + row * LDK);
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
-          const float4 t = p[swz(row, NV * g + q)];
+          const float4 t = p[swz<KR>(row, NV * g + q)];
           a[i][4 * q] = t.x, a[i][4 * q + 1] = t.y, a[i][4 * q + 2] = t.z, a[i][4 * q + 3] = t.w;
         }
       }
@@ -183,7 +184,7 @@ struct Frag<float, BN, KR, AKM, BKM, TA, TB> {
         const float4 *p = (const float4 *)(Bs + row * LDK);
 #pragma unroll
         for (int q = 0; q < NV; ++q) {
-          const float4 t = p[swz(row, NV * g + q)];
+          const float4 t = p[swz<KR>(row, NV * g + q)];
           b[j][4 * q] = t.x, b[j][4 * q + 1] = t.y, b[j][4 * q + 2] = t.z, b[j][4 * q + 3] = t.w;
         }
       }
@@ -244,7 +245,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
         const int row = wm + 32 * i + r;
         const bf16x8 *p = (const bf16x8 *)(As + row * LDK);
 #pragma unroll
-        for (int q = 0; q < NV; ++q) a[i][q] = p[swz(row, NV * g + q)];
+        for (int q = 0; q < NV; ++q) a[i][q] = p[swz<KR>(row, NV * g + q)];
       }
     }
 #pragma unroll
@@ -256,7 +257,7 @@ struct Frag<bf16, BN, KR, AKM, BKM, TA, TB> {
         const int row = wn + 32 * j + r;
         const bf16x8 *p = (const bf16x8 *)(Bs + row * LDK);
 #pragma unroll
-        for (int q = 0; q < NV; ++q) b[j][q] = p[swz(row, NV * g + q)];
+        for (int q = 0; q < NV; ++q) b[j][q] = p[swz<KR>(row, NV * g + q)];
       }
     }
   }

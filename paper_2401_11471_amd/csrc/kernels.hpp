@@ -161,6 +161,15 @@ void set_dgrad_phases(int mode);
 #ifndef LRCNN_NARROW_GAIN
 #define LRCNN_NARROW_GAIN 1.5  // narrow tiles are taken unless wide ones are 1.5x faster
 #endif
+// 16-byte vectors per K iteration of a convolution launch: LRCNN_CONV_KR
+// (4 or 8), and LRCNN_CONV_KR_WIN for the bfloat16 forward of windowed
+// kernels (conv_kr below)
+#ifndef LRCNN_CONV_KR
+#define LRCNN_CONV_KR 4
+#endif
+#ifndef LRCNN_CONV_KR_WIN
+#define LRCNN_CONV_KR_WIN 8
+#endif
 struct SplitCost {
   double step_us;   // one K iteration of a lone workgroup
   int occ;          // workgroups one CU holds (LDS bound)
@@ -229,12 +238,16 @@ struct ConvTiles {
   int bn, splits;
   double us;  // estimated duration
 };
-inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es) {
-  const double f = es == 2 ? 0.75 : 1.0;
+// (kr: 16-byte vectors per K iteration; an iteration of 8 costs about twice
+// one of 4, and its 72 KiB LDS ring fits two 64-wide workgroups per CU;
+// 8-vector launches use 64-wide tiles only)
+inline ConvTiles conv_tiles(long long M, int N, int KT, size_t cap, int es,
+                            int kr = LRCNN_CONV_KR) {
+  const double f = (es == 2 ? 0.75 : 1.0) * kr / 4.0;
   const long long mt = (M + 127) / 128;
   SplitChoice n64 = split_choice(mt * ((N + 63) / 64), KT, M * (long long)N, cap,
-                                 SplitCost{LRCNN_STEP_N64 * f, 3, 5.0});
-  if (N <= 64) return ConvTiles{64, n64.s, n64.us};
+                                 SplitCost{LRCNN_STEP_N64 * f, kr > 4 ? 2 : 3, 5.0});
+  if (N <= 64 || kr > 4) return ConvTiles{64, n64.s, n64.us};
   SplitChoice n128 = split_choice(mt * ((N + 127) / 128), KT, M * (long long)N, cap,
                                   SplitCost{LRCNN_STEP_N128 * f, 2, 5.0});
   return n64.us < n128.us * LRCNN_NARROW_GAIN ? ConvTiles{64, n64.s, n64.us}
@@ -247,28 +260,39 @@ inline int conv_split_count(long long M, int N, int KT, size_t cap, int es) {
 // Tile width of a convolution launch whose split count is fixed (the
 // forward launches of one layer all use the layer's count, so every output
 // element sums K in the same chunks whatever the band); `us` its estimate.
-inline ConvTiles conv_tiles_split(long long M, int N, int KT, int s, int es) {
-  const double f = es == 2 ? 0.75 : 1.0;
+inline ConvTiles conv_tiles_split(long long M, int N, int KT, int s, int es,
+                                  int kr = LRCNN_CONV_KR) {
+  const double f = (es == 2 ? 0.75 : 1.0) * kr / 4.0;
   const long long mt = (M + 127) / 128;
   const double u64 = split_cost(mt * ((N + 63) / 64), KT, M * (long long)N,
-                                SplitCost{LRCNN_STEP_N64 * f, 3, 5.0}, s);
-  if (N <= 64) return ConvTiles{64, s, u64};
+                                SplitCost{LRCNN_STEP_N64 * f, kr > 4 ? 2 : 3, 5.0}, s);
+  if (N <= 64 || kr > 4) return ConvTiles{64, s, u64};
   const double u128 = split_cost(mt * ((N + 127) / 128), KT, M * (long long)N,
                                  SplitCost{LRCNN_STEP_N128 * f, 2, 5.0}, s);
   return u64 < u128 * LRCNN_NARROW_GAIN ? ConvTiles{64, s, u64} : ConvTiles{128, s, u128};
 }
 // K iterations of a conv for storage element size es (bytes); one
-// iteration covers LRCNN_CONV_KR 16-byte vectors of a tile row.
-#ifndef LRCNN_CONV_KR
-#define LRCNN_CONV_KR 4
-#endif
+// iteration covers kr 16-byte vectors of a tile row (LRCNN_CONV_KR, or
+// LRCNN_CONV_KR_WIN for the bfloat16 forward of a windowed kernel whose
+// channels fill whole vectors: twice the MFMAs per K step there).
 // A forward convolution whose input channels fit in one 16-byte vector
 // (kc * es < 16, e.g. a 3-channel image) packs LRCNN_CONV_KR taps into one
 // iteration instead (tap_packed).
 inline bool conv_tap_packed(int kc, int es, bool dgrad) { return !dgrad && kc * es < 16; }
-inline int conv_k_iters(int taps, int kc, int es, bool dgrad = false) {
+// the 16-byte loaders (taps tested against a 64-bit mask)
+inline bool conv_vec(int kh, int kw, int kc, int n, int es, bool dgrad) {
+  const int E = 16 / es;
+  return kc % E == 0 && (!dgrad || n % E == 0) && kh * kw <= 64 && kw < 64;
+}
+inline int conv_kr(int kh, int kw, int kc, int n, int es, bool dgrad) {
+  return !dgrad && es == 2 && kh * kw > 1 && conv_vec(kh, kw, kc, n, es, dgrad)
+             ? LRCNN_CONV_KR_WIN
+             : LRCNN_CONV_KR;
+}
+inline int conv_k_iters(int taps, int kc, int es, bool dgrad = false,
+                        int kr = LRCNN_CONV_KR) {
   if (conv_tap_packed(kc, es, dgrad)) return (taps + LRCNN_CONV_KR - 1) / LRCNN_CONV_KR;
-  const int bk = 16 * LRCNN_CONV_KR / es;
+  const int bk = 16 * kr / es;
   return taps * ((kc + bk - 1) / bk);
 }
 

@@ -350,7 +350,8 @@ static void forward_splits(Plan &P,
     const lrcnn_node &d = P.nodes[v];
     if (d.op != LRCNN_OP_CONV) continue;
     const Shape &su = P.shp[d.in0], &sv = P.shp[v];
-    const int KT = conv_k_iters(d.kh * d.kw, su.c, P.es);
+    const int kr = conv_kr(d.kh, d.kw, su.c, sv.c, P.es, false);
+    const int KT = conv_k_iters(d.kh * d.kw, su.c, P.es, false, kr);
     std::vector<long long> ms;
     long long mmax = 0;
     for (auto *tab : tabs)
@@ -365,14 +366,14 @@ static void forward_splits(Plan &P,
       if (!split_valid(KT, sp)) continue;
       if (sp > 1 && (size_t)sp * (size_t)mmax * sv.c * 4 > kPartCap) break;
       double t = 0;
-      for (long long m : ms) t += conv_tiles_split(m, sv.c, KT, sp, P.es).us;
+      for (long long m : ms) t += conv_tiles_split(m, sv.c, KT, sp, P.es, kr).us;
       // the layer-wise launch, in chunks of rows
       const size_t row_part = (size_t)sp * B * sv.w * sv.c * 4;
       const int rows = sp > 1 ? (int)std::min<size_t>(sv.h, std::max<size_t>(1, kPartCap / row_part))
                               : sv.h;
       const int full = sv.h / rows, rest = sv.h - full * rows;
-      t += full * conv_tiles_split(B * rows * sv.w, sv.c, KT, sp, P.es).us;
-      if (rest) t += conv_tiles_split(B * rest * sv.w, sv.c, KT, sp, P.es).us;
+      t += full * conv_tiles_split(B * rows * sv.w, sv.c, KT, sp, P.es, kr).us;
+      if (rest) t += conv_tiles_split(B * rest * sv.w, sv.c, KT, sp, P.es, kr).us;
       if (best < 0 || t < best * 0.98) {
         best = t;
         best_s = sp;
