@@ -31,6 +31,32 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"f32": ("mfma", 157.3, "TFLOP/s"), "bf16": ("mfma", 2500.0, "TFLOP/s")}
+HBM_GBS = 8000.0  # MI355X HBM3E
+
+
+def kernel_roofline(entry, dts):
+    """Roofline of one kernel name from the library's profile aggregate
+    (launches, ms, FLOPs, algorithmic bytes, roofline ms). The bound is the
+    one that dominates its launches' algorithmic work: matrix-core time
+    (FLOPs at the dtype's dense peak) or HBM time (bytes at 8 TB/s);
+    `achieved` is FLOP/s or bytes/s against that bound's peak. Also given:
+    the matrix-core fraction, and the fraction of the launches' roofline
+    time (per launch the larger of the two) that the measured time
+    reaches."""
+    n, ms, fl, by, rf = entry
+    _, pk, unit = PEAK[dts]
+    t_mfma = fl / (pk * 1e12)
+    t_hbm = by / (HBM_GBS * 1e9)
+    tflops = fl / (ms * 1e-3) / 1e12
+    if t_hbm > t_mfma:
+        achieved, peak, unit, bound = by / (ms * 1e-3) / 1e9, HBM_GBS, "GB/s", "hbm"
+    else:
+        achieved, peak, bound = tflops, pk, "mfma"
+    return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "avg_launch_ms": round(ms / n, 4),
+            "algorithmic_bytes_per_launch": round(by / n), "flops_per_launch": round(fl / n),
+            "tflops": round(tflops, 2), "mfma_frac": round(tflops / pk, 4),
+            "roofline_time_frac": round(rf / ms, 4) if ms > 0 else None}
 
 
 def parse():
@@ -247,14 +273,14 @@ def compact_workload(args, cid):
         prof = None
         if profile:
             _, ps, _ = timed_steps(torch, step, args.steps, 0, True, L.lrcnn_debug_profile)
-            prof = (L.lrcnn_debug_profile_collect(), ps)
+            prof = (L.lrcnn_debug_profile_collect(roofline=True), ps)
         del ws, y
         return ms, int(peak), prof
 
     ms, peak, (kern, ps) = run(base, profile=True)
-    dom_name, (dom_n, dom_ms, dom_fl) = max(kern.items(), key=lambda kv: kv[1][2])
-    bound, pk, unit = PEAK[dts]
-    achieved = dom_fl / (dom_ms * 1e-3) / 1e12
+    dom_name, dom = max(kern.items(), key=lambda kv: kv[1][2])
+    roof = kernel_roofline(dom, dts)
+    roof.update({"kernel": dom_name, "launches_per_step": dom[0] // ps})
     lw_ms, lw_peak, _ = run(base, layerwise=True)
     res = {"value": round(B * 1000.0 / ms, 3), "unit": "images/s", "ms_per_step": round(ms, 3),
            "dtype": dts,
@@ -263,10 +289,7 @@ def compact_workload(args, cid):
                       "policy": ["even", "balanced"][preset.get("policy", 0)],
                       "bp_bands": base.info()["bp_bands"],
                       "hybrid_from": base.info()["hybrid_from"]},
-           "roofline": {"bound": bound, "achieved": round(achieved, 2), "peak": pk,
-                        "unit": unit, "frac": round(achieved / pk, 4), "kernel": dom_name,
-                        "launches_per_step": dom_n // ps,
-                        "avg_launch_ms": round(dom_ms / dom_n, 4)},
+           "roofline": roof,
            "peak_act_bytes": peak,
            "layerwise": {"images_per_s": round(B * 1000.0 / lw_ms, 3),
                          "ms_per_step": round(lw_ms, 3), "peak_act_bytes": lw_peak},
@@ -601,7 +624,7 @@ def main():
         # library's events attached to every matrix-core dispatch
         _, psteps, _ = timed_steps(torch, lambda: rc_step(bufs), args.steps, 0, True,
                                    L.lrcnn_debug_profile)
-    kern = L.lrcnn_debug_profile_collect()
+    kern = L.lrcnn_debug_profile_collect(roofline=True)
     # the same eager steps with the weight gradients on the caller's stream:
     # every kernel then has the GPU to itself (the default schedule overlaps
     # each weight gradient with an input gradient, and their event times
@@ -612,15 +635,15 @@ def main():
                                              L.lrcnn_debug_profile)
     finally:
         L.lrcnn_debug_serial_wgrad(False)
-    kern_serial = L.lrcnn_debug_profile_collect()
+    kern_serial = L.lrcnn_debug_profile_collect(roofline=True)
 
     # dominant kernel: the largest share of the algorithmic FLOPs (the
     # weight gradient at the ResNet-50 workloads, whose event times in the
     # default schedule include sharing the GPU with an input gradient; the
     # serial pass above times it alone)
-    dom_name, (dom_n, dom_ms, dom_fl) = max(kern.items(), key=lambda kv: kv[1][2])
-    bound, peak, unit = PEAK[dts]
-    achieved = dom_fl / (dom_ms * 1e-3) / 1e12
+    dom_name, dom = max(kern.items(), key=lambda kv: kv[1][2])
+    dom_n = dom[0]
+    peak = PEAK[dts][1]
     traffic = None
     tpath = os.path.join(ROOT, "profiles", "traffic.json")
     if os.path.exists(tpath):
@@ -631,24 +654,19 @@ def main():
                 traffic = ent["bytes_per_launch"]
         except (ValueError, KeyError):
             traffic = None
-    roofline = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": traffic,
-                "kernel": dom_name, "launches_per_step": dom_n // psteps,
-                "timing": ("HIP events attached to every matrix-core dispatch "
-                           "(hipExtLaunchKernelGGL) " +
-                           ("in the timed region" if args.eager else
-                            "in an eager pass of the same steps after the timed graph "
-                            "replays")),
-                "avg_launch_ms": round(dom_ms / dom_n, 4)}
+    roofline = kernel_roofline(dom, dts)
+    roofline.update({
+        "traffic": traffic, "kernel": dom_name, "launches_per_step": dom_n // psteps,
+        "timing": ("HIP events attached to every matrix-core dispatch "
+                   "(hipExtLaunchKernelGGL) " +
+                   ("in the timed region" if args.eager else
+                    "in an eager pass of the same steps after the timed graph replays"))})
     if dom_name in kern_serial:
-        sn, sms, sfl = kern_serial[dom_name]
-        iso = sfl / (sms * 1e-3) / 1e12
-        roofline["alone"] = {
-            "achieved": round(iso, 2), "frac": round(iso / peak, 4),
-            "avg_launch_ms": round(sms / sn, 4),
-            "step_ms": round(ms_serial, 3),
-            "timing": "eager steps with the weight gradients on the caller's stream "
-                      "(no kernel overlaps another)"}
+        alone = kernel_roofline(kern_serial[dom_name], dts)
+        alone.update({"step_ms": round(ms_serial, 3),
+                      "timing": "eager steps with the weight gradients on the caller's "
+                                "stream (no kernel overlaps another)"})
+        roofline["alone"] = alone
     all_mfma_ms = sum(v[1] for k, v in kern.items() if "reduce" not in k) / psteps
     all_mfma_fl = sum(v[2] for v in kern.values()) / psteps
 

@@ -70,6 +70,14 @@ int lrcnn_debug_profile_collect(void);
 int lrcnn_debug_profile_entry(int32_t i, const char **name, int64_t *launches,
                               double *ms, double *flops);
 
+/* Entry i's summed algorithmic HBM bytes (operands read once, outputs and
+ * split partial sums written once, read-modify-writes counted twice) and
+ * summed roofline times in milliseconds: per launch the larger of its FLOPs
+ * at MI355X's dense matrix-core peak for its storage type (bf16 2.5
+ * PFLOP/s, fp32 157.3 TFLOP/s) and its bytes at 8 TB/s. Returns 0, or -1 if
+ * i is out of range or a pointer is null. */
+int lrcnn_debug_profile_roofline(int32_t i, double *bytes, double *roofline_ms);
+
 /* Byte offset in the layer-wise workspace of node `node`'s full feature map
  * ([B][H][W][C], dense, the plan's storage dtype) as
  * lrcnn_layerwise_reference_gpu leaves it: its forward, which equals

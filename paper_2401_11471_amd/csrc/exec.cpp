@@ -1082,3 +1082,7 @@ extern "C" int lrcnn_debug_profile_entry(int32_t i, const char **name, int64_t *
                                          double *ms, double *flops) {
   return lrcnn::profile_entry(i, name, launches, ms, flops);
 }
+extern "C" int lrcnn_debug_profile_roofline(int32_t i, double *bytes, double *roofline_ms) {
+  if (!bytes || !roofline_ms) return -1;
+  return lrcnn::profile_entry_roofline(i, bytes, roofline_ms);
+}

@@ -804,6 +804,34 @@ __global__ __launch_bounds__(256) void conv_split_epilogue(ConvArgs a, int split
 #define LRCNN_CONV_KR 4
 #endif
 
+// Algorithmic HBM bytes of a convolution launch (M output pixels): the
+// source rows under the taps and the weights read once, and the output:
+// forward, the stored map (plus the fused add's other input and the mask
+// when present); input gradient, the float32 error window (read and
+// written unless the launch initializes it). A split launch writes its
+// partial sums instead, which its epilogue (epi) reads back before writing
+// the output.
+template <typename T, bool DGRAD>
+static double conv_bytes(const ConvArgs &a, long long M, int splits, bool epi) {
+  const double es = sizeof(T), mn = (double)M * a.N;
+  const double out = DGRAD ? mn * 4.0 * (a.dst_init ? 1.0 : 2.0)
+                           : mn * es * (a.res.p ? 2.0 : 1.0) + (a.mask ? mn : 0.0);
+  if (epi) return splits * mn * 4.0 + out;
+  int lo, hi;
+  if (DGRAD) {
+    const int s = a.sh > 0 ? a.sh : 1;
+    const int t = a.y0 + a.ph - a.kh + 1;
+    lo = std::max(a.sy0, t > 0 ? (t + s - 1) / s : 0);
+    hi = std::min(a.sy1, (a.y1 - 1 + a.ph) / s + 1);
+  } else {
+    lo = std::max(a.sy0, a.y0 * a.sh - a.ph);
+    hi = std::min(a.sy1, (a.y1 - 1) * a.sh - a.ph + a.kh);
+  }
+  const double in = (double)a.B * std::max(0, hi - lo) * a.Ws * a.KC * es;
+  const double w = (double)a.N * a.kh * a.kw * a.KC * es;
+  return in + w + (splits > 1 ? splits * mn * 4.0 : out);
+}
+
 template <typename T, bool DGRAD>
 static int conv_launch(const ConvArgs &a0, hipStream_t s) {
   constexpr int KR = LRCNN_CONV_KR;
@@ -849,7 +877,7 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
     std::string nm = std::string("conv_gemm_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
                      ", " + std::to_string(bn) + (DGRAD ? ", dgrad" : ", fwd") +
                      (!vec ? ", scalar>" : one_ ? ", 1x1>" : ", vec>");
-    pr = prof::begin(nm, fl, s);
+    pr = prof::begin(nm, fl, s, conv_bytes<T, DGRAD>(a, M, splits, false), es);
   }
   // the input gradient of a strided convolution divides by the stride
   // (a phase of it is dense)
@@ -889,7 +917,8 @@ static int conv_launch(const ConvArgs &a0, hipStream_t s) {
     }
   }
   if (splits > 1) {
-    int p2 = prof::begin("conv_split_epilogue", 0.0, s);
+    int p2 = prof::begin("conv_split_epilogue", 0.0, s, conv_bytes<T, DGRAD>(a, M, splits, true),
+                         es);
     const int G = splits >= 8 ? 8 : splits >= 4 ? 4 : 2;
     const long long vecs = a.N % 4 == 0 ? (long long)M * a.N / 4 : (long long)M * a.N;
     const unsigned blocks = (unsigned)((vecs + 256 / G - 1) / (256 / G));

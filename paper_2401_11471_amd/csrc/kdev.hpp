@@ -20,7 +20,10 @@ namespace lrcnn {
 // off); the launch carries the index's start and stop events.
 namespace prof {
 extern bool on;
-int begin(const std::string &name, double flops, hipStream_t s);
+// (bytes: the launch's algorithmic HBM bytes; es: storage element size,
+// which selects the matrix-core peak of its roofline time)
+int begin(const std::string &name, double flops, hipStream_t s, double bytes = 0.0,
+          int es = 0);
 hipEvent_t start(int i);
 hipEvent_t stop(int i);
 }  // namespace prof

@@ -24,6 +24,7 @@
 #include <cstdint>
 #include <map>
 #include <string>
+#include <algorithm>
 #include <vector>
 
 #include "kdev.hpp"
@@ -39,7 +40,7 @@ namespace prof {
 struct Rec {
   std::string name;
   hipEvent_t a, b;
-  double flops;
+  double flops, bytes, roof_ms;
 };
 bool on = false;
 static std::vector<Rec> recs;
@@ -54,18 +55,23 @@ static hipEvent_t take() {
   }
   return pool[used++];
 }
-int begin(const std::string &name, double flops, hipStream_t) {
+// Roofline time of a launch on MI355X: the larger of its FLOPs at the dense
+// matrix-core peak of its storage type (bf16 2.5 PFLOP/s, fp32 157.3
+// TFLOP/s) and its algorithmic bytes at the HBM3E peak (8 TB/s).
+int begin(const std::string &name, double flops, hipStream_t, double bytes, int es) {
   if (!on) return -1;
   hipEvent_t a = take(), b = take();
   if (!a || !b) return -1;
-  recs.push_back(Rec{name, a, b, flops});
+  const double peak = es == 2 ? 2.5e15 : es == 4 ? 157.3e12 : 0.0;
+  const double roof_ms = 1e3 * std::max(peak > 0 ? flops / peak : 0.0, bytes / 8e12);
+  recs.push_back(Rec{name, a, b, flops, bytes, roof_ms});
   return (int)recs.size() - 1;
 }
 hipEvent_t start(int i) { return recs[i].a; }
 hipEvent_t stop(int i) { return recs[i].b; }
 struct Agg {
   int64_t launches = 0;
-  double ms = 0, flops = 0;
+  double ms = 0, flops = 0, bytes = 0, roof_ms = 0;
 };
 static std::vector<std::pair<std::string, Agg>> table;
 }  // namespace prof
@@ -89,9 +95,18 @@ int profile_collect() {
     g.launches += 1;
     g.ms += ms;
     g.flops += r.flops;
+    g.bytes += r.bytes;
+    g.roof_ms += r.roof_ms;
   }
   prof::table.assign(m.begin(), m.end());
   return (int)prof::table.size();
+}
+
+int profile_entry_roofline(int i, double *bytes, double *roof_ms) {
+  if (i < 0 || i >= (int)prof::table.size()) return -1;
+  *bytes = prof::table[i].second.bytes;
+  *roof_ms = prof::table[i].second.roof_ms;
+  return 0;
 }
 
 int profile_entry(int i, const char **name, int64_t *launches, double *ms, double *flops) {

@@ -442,5 +442,7 @@ int launch_compact_dw(const float *pad, float *dw, int C, int Cp, long long n, v
 void profile_enable(int enable);
 int profile_collect();
 int profile_entry(int i, const char **name, int64_t *launches, double *ms, double *flops);
+// summed algorithmic bytes and roofline times of entry i's launches
+int profile_entry_roofline(int i, double *bytes, double *roof_ms);
 
 }  // namespace lrcnn

@@ -599,12 +599,7 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
   splits = (K + kchunk - 1) / kchunk;
   if (!split_fits(splits, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
   const int wbm = wt.rows;
-  dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
-  int pr = -1;
-  if (prof::on)
-    pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
-                         (avec && bvec ? ", vec>" : ", scalar>"),
-                     2.0 * K * a.Co * N, s);
+  int kchunk_l = kchunk;
   if (rowg) {
     // padded pixels: rows of Wp = Wv rounded up to 8 columns; the split
     // count is the estimate's, each chunk a whole number of K steps
@@ -616,13 +611,27 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
     const long long Kp = (long long)a.B * (a.y1 - a.y0) * a.Wp;
     if (Kp >= (1ll << 31)) return (int)hipErrorInvalidValue;
     const long long KTp = (Kp + BK - 1) / BK;
-    const int kchunk_p = (int)((KTp + wt.splits - 1) / wt.splits * BK);
-    const int splits_p = (int)((Kp + kchunk_p - 1) / kchunk_p);
-    if (!split_fits(splits_p, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
-    dim3 gp((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits_p);
-    if (wbm == 64) launch_timed(wgrad_rowg_kernel<64>, gp, s, pr, a, kchunk_p, dw);
-    else launch_timed(wgrad_rowg_kernel<128>, gp, s, pr, a, kchunk_p, dw);
-    splits = splits_p;
+    kchunk_l = (int)((KTp + wt.splits - 1) / wt.splits * BK);
+    splits = (int)((Kp + kchunk_l - 1) / kchunk_l);
+    if (!split_fits(splits, a.Co, N, a.out, a.part_bytes)) return (int)hipErrorInvalidValue;
+  }
+  dim3 grid((a.Co + wbm - 1) / wbm, (N + 127) / 128, splits);
+  // algorithmic bytes: the error operand, the source rows under the taps
+  // (once), and the partial sums (split) or dW (read and written unless
+  // this band's launch initializes it)
+  const long long rin =
+      std::max(0, std::min(a.Hs, (a.y1 - 1) * a.sh - a.ph + a.kh) - std::max(0, a.y0 * a.sh - a.ph));
+  const double mnb = 4.0 * a.Co * N;
+  const double wbytes = (double)K * a.Co * sizeof(T) + (double)a.B * rin * a.Ws * a.Ci * sizeof(T) +
+                        (splits > 1 ? splits * mnb : (a.overwrite ? 1.0 : 2.0) * mnb);
+  int pr = -1;
+  if (prof::on)
+    pr = prof::begin(std::string("wgrad_kernel<") + (sizeof(T) == 4 ? "float" : "bf16") +
+                         (avec && bvec ? ", vec>" : ", scalar>"),
+                     2.0 * K * a.Co * N, s, wbytes, (int)sizeof(T));
+  if (rowg) {
+    if (wbm == 64) launch_timed(wgrad_rowg_kernel<64>, grid, s, pr, a, kchunk_l, dw);
+    else launch_timed(wgrad_rowg_kernel<128>, grid, s, pr, a, kchunk_l, dw);
   } else if (wide) {
     if (wbm == 64) launch_timed(wgrad_kernel<T, 64, true, true, 8>, grid, s, pr, a, kchunk, dw);
     else launch_timed(wgrad_kernel<T, 128, true, true, 8>, grid, s, pr, a, kchunk, dw);
@@ -637,7 +646,8 @@ static int wgrad_dispatch(const WgradArgs &a0, float *dw, hipStream_t s) {
   }
   if (splits > 1) {
     long long mn = (long long)a.Co * N;
-    int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s);
+    int p2 = prof::begin("wgrad_reduce_kernel", 0.0, s,
+                         4.0 * mn * (splits + (a.overwrite ? 1 : 2)), 4);
     if (mn % 4 == 0)
       launch_timed(wgrad_reduce_kernel<4>, dim3((unsigned)((mn / 4 + 31) / 32)), s, p2,
                    (const float *)a.out, dw, mn, splits, a.overwrite);

@@ -119,6 +119,9 @@ def _load():
                                               C.POINTER(C.c_int64),
                                               C.POINTER(C.c_double), C.POINTER(C.c_double)]
     lib.lrcnn_debug_profile_entry.restype = C.c_int
+    lib.lrcnn_debug_profile_roofline.argtypes = [i32, C.POINTER(C.c_double),
+                                                 C.POINTER(C.c_double)]
+    lib.lrcnn_debug_profile_roofline.restype = C.c_int
     lib.lrcnn_debug_layerwise_map.argtypes = [vp, i32, C.POINTER(sz)]
     lib.lrcnn_debug_layerwise_map.restype = C.c_int
     for f in ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
@@ -144,6 +147,7 @@ EXPORTS = ("lrcnn_plan", "lrcnn_plan_query", "lrcnn_plan_node_shape",
            "lrcnn_debug_dgrad_phases", "lrcnn_debug_serial_wgrad",
            "lrcnn_debug_profile",
            "lrcnn_debug_profile_collect", "lrcnn_debug_profile_entry",
+           "lrcnn_debug_profile_roofline",
            "lrcnn_debug_layerwise_map")
 
 
@@ -349,9 +353,11 @@ def lrcnn_debug_profile(on):
     LIB.lrcnn_debug_profile(1 if on else 0)
 
 
-def lrcnn_debug_profile_collect():
+def lrcnn_debug_profile_collect(roofline=False):
     """Per-kernel aggregate of the recorded launches (streams synchronised
-    by the caller): {name: (launches, ms, flops)}."""
+    by the caller): {name: (launches, ms, flops)}, with roofline also the
+    summed algorithmic bytes and roofline ms: (launches, ms, flops, bytes,
+    roofline_ms)."""
     n = LIB.lrcnn_debug_profile_collect()
     if n < 0:
         raise LrcnnError(-7, "profile collection failed")
@@ -359,7 +365,12 @@ def lrcnn_debug_profile_collect():
     for i in range(n):
         nm, la, ms, fl = C.c_char_p(), C.c_int64(), C.c_double(), C.c_double()
         LIB.lrcnn_debug_profile_entry(i, C.byref(nm), C.byref(la), C.byref(ms), C.byref(fl))
-        out[nm.value.decode()] = (la.value, ms.value, fl.value)
+        if roofline:
+            by, rf = C.c_double(), C.c_double()
+            LIB.lrcnn_debug_profile_roofline(i, C.byref(by), C.byref(rf))
+            out[nm.value.decode()] = (la.value, ms.value, fl.value, by.value, rf.value)
+        else:
+            out[nm.value.decode()] = (la.value, ms.value, fl.value)
     return out
 
 

@@ -146,4 +146,5 @@ int launch_compact_dw(const float *, float *, int, int, long long, void *s) {
 void profile_enable(int) {}
 int profile_collect() { return 0; }
 int profile_entry(int, const char **, int64_t *, double *, double *) { return -1; }
+int profile_entry_roofline(int, double *, double *) { return -1; }
 }  // namespace lrcnn

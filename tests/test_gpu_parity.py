@@ -241,3 +241,32 @@ def test_serial_weight_gradients_equal_overlapped(dtype):
     for v in range(1, len(nodes)):
         if base["dw"][v] is not None:
             np.testing.assert_array_equal(base["dw"][v], ser["dw"][v])
+
+
+def test_profile_roofline_entries():
+    """The profiling hook's per-kernel aggregates: every matrix-core kernel
+    and reduction of a step carries algorithmic bytes and a roofline time,
+    and the roofline time (per launch the larger of FLOPs at the matrix-core
+    peak and bytes at the HBM peak) never exceeds the measured time."""
+    from paper_2401_11471_amd.device import DeviceModel
+    nodes, inp = _inputs("resnet_like", BF16, seed=19)
+    b, h, w, c = inp.x.shape
+    plan = L.lrcnn_plan(nodes, b, c, h, w, BF16, L.CARRY, 4)
+    dm = DeviceModel.from_inputs(nodes, inp)
+    oshape = (b,) + plan.node_shape(len(nodes) - 1)
+    y = dm.empty(oshape)
+    dy = dm.to_device(inp.grad(oshape))
+    ws = dm.workspace(plan.info()["workspace_bytes"])
+    L.lrcnn_debug_profile(True)
+    try:
+        L.lrcnn_forward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, y, ws)
+        L.lrcnn_backward_rows(plan, dm.x, dm.w, dm.sc, dm.sf, dy, dm.dw, None, ws)
+        torch.cuda.synchronize()
+    finally:
+        L.lrcnn_debug_profile(False)
+    kern = L.lrcnn_debug_profile_collect(roofline=True)
+    assert any(k.startswith("wgrad_kernel") for k in kern)
+    assert any(k.startswith("conv_gemm_kernel") for k in kern)
+    for name, (n, ms, fl, by, rf) in kern.items():
+        assert n > 0 and ms > 0 and by > 0 and rf > 0, name
+        assert rf <= ms, (name, rf, ms)
