@@ -393,10 +393,10 @@ struct Run {
 
   // Error window of node u for band r: its view, and, in CARRY mode, the
   // rows [t, b) whose error band r+1 carried (returns false if none).
-  // carry buffer of node u written by band `band` (and read by band - 1)
+  // carry buffer of node u written by band `band` (and read by band - 1):
+  // a node with two buffers alternates them by band parity
   char *carry_ptr(int u, int band) const {
-    (void)band;
-    return ws + L.carry[u];
+    return ws + ((band & 1) && L.carry2[u] ? L.carry2[u] : L.carry[u]);
   }
 
   bool delta_view(int r, int u, View &cv, int &t) {
@@ -416,9 +416,11 @@ struct Run {
 
   // When v's backward launch (rows [y0, y1) of u) completes u's error and v
   // is u's only consumer, the launch forms u's error operand and carried
-  // rows itself (eo); the carried-out rows are staged in u's error window
-  // and moved to `stage` (u's carry buffer) after the launch, which reads
-  // the rows carried in from that buffer. stage_a = 0 when nothing is staged.
+  // rows itself (eo). With two carry buffers (band parity) it writes the
+  // carried-out rows into this band's buffer while it reads the rows carried
+  // in from the other; with one, they are staged in u's error window and
+  // moved to `stage` (u's carry buffer) after the launch, which reads the
+  // rows carried in from that buffer. stage_a = 0 when nothing is staged.
   int fuse_err(int r, int v, int u, int y0, int y1, ErrOut &eo, View &stage, int &stage_a) {
     stage_a = 0;
     if (F.act[u] != v) return LRCNN_OK;
@@ -439,13 +441,21 @@ struct Run {
     if (oa > qu.lo) {
       if (sched != S_CARRY || r == 0)
         return lrcnn_fail(LRCNN_EINVAL, "internal: rows below a band without carry");
-      eo.carry = View{ws + L.delta[u], (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo, sh.w,
-                      sh.c, L.carry_cap[u]};
       stage = View{carry_ptr(u, r), (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo, sh.w, sh.c,
                    L.carry_cap[u]};
-      if (!holds(eo.carry, qu.lo, oa) || !holds(stage, qu.lo, oa))
-        return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
-      stage_a = oa;
+      if (L.carry2[u]) {
+        // the rows carried in come from the other parity's buffer: the
+        // launch writes the carried-out rows straight into this band's
+        eo.carry = stage;
+        if (!holds(eo.carry, qu.lo, oa))
+          return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+      } else {
+        eo.carry = View{ws + L.delta[u], (long long)L.carry_cap[u] * sh.w * sh.c, qu.lo, sh.w,
+                        sh.c, L.carry_cap[u]};
+        if (!holds(eo.carry, qu.lo, oa) || !holds(stage, qu.lo, oa))
+          return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
+        stage_a = oa;
+      }
     }
     act_done[u] = 1;
     return LRCNN_OK;

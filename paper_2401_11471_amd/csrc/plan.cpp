@@ -402,6 +402,7 @@ static void layout(Plan &P, Layout &L, const Fuse &F, const std::vector<int> &ca
   L.argmax_cap.assign(n, 0);
   L.delta.assign(n, 0);
   L.carry.assign(n, 0);
+  L.carry2.assign(n, 0);
   L.carry_cap = carry;
   L.strip.assign(P.nb, std::vector<size_t>(n, 0));
   L.fwin.assign(n, 0);
@@ -503,7 +504,10 @@ static void layout(Plan &P, Layout &L, const Fuse &F, const std::vector<int> &ca
     }
   size_t k0 = A.top;
   for (int v = 0; v < n; ++v)
-    if (carry[v] > 0) L.carry[v] = A.take(P.elems(v, carry[v]) * 4);
+    if (carry[v] > 0) {
+      L.carry[v] = A.take(P.elems(v, carry[v]) * 4);
+      if (F.act[v] != 0) L.carry2[v] = A.take(P.elems(v, carry[v]) * 4);
+    }
   L.carry_bytes = A.top - k0;
   // BP arena, packed by lifetime over the backward steps (step s handles
   // node n-1-s):

@@ -32,6 +32,11 @@ struct Layout {
   std::vector<int> argmax_cap;
   std::vector<size_t> delta;     // per node: float32 error window
   std::vector<size_t> carry;     // per node: float32 error carried to band r-1
+  // per node whose consumer's backward launch writes its carried rows: a
+  // second carry buffer; bands of odd index write (and the band below
+  // reads) this one, so that launch never writes the buffer it reads the
+  // rows carried in from (0: one buffer)
+  std::vector<size_t> carry2;
   std::vector<int> carry_cap;
   std::vector<std::vector<size_t>> strip;  // [band][node]: shared rows kept
   size_t part = 0, part_bytes = 0;  // split-K partial sums (forward, input gradient)
