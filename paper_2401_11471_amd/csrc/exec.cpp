@@ -478,9 +478,11 @@ struct Run {
     if (u == 0 && !want_dx) return false;
     if (d.op == LRCNN_OP_ADD) {
       // the add's backward writes its own rows of each input (not when both
-      // inputs are the same node: the second side adds to the first)
+      // inputs are the same node: the second side adds to the first), and
+      // the initial value of the window rows above them (a consumer with
+      // later own rows, such as the next block's first conv, reaches them)
       const Rows qv = band_rows(r, v), qu = band_rows(r, u);
-      return d.in0 != d.in1 && qv.b > qv.a && qv.a == qu.lo && qv.b == qu.hi;
+      return d.in0 != d.in1 && qv.b > qv.a && qv.a == qu.lo && qv.b <= qu.hi;
     }
     if (d.op != LRCNN_OP_CONV && d.op != LRCNN_OP_MAXPOOL) return false;
     const Rows qv = band_rows(r, v), qu = band_rows(r, u);
@@ -667,12 +669,14 @@ struct Run {
       for (int k = 0; k < 2; ++k) {
         const int x = in_ids[k];
         AddSide &sd = side_in[k];
-        sd = AddSide{dlt[x], nullptr, nullptr, sv.c, 0, View{}, 0};
+        sd = AddSide{dlt[x], nullptr, nullptr, sv.c, 0, View{}, 0, 0};
         if (dinit[x]) {
           // this launch writes every row of x's window: no zeroing pass
+          const Rows qx = band_rows(r, x);
           sd.init = 1;
+          sd.init_hi = qx.hi;
           if (dinit_carry[x]) {
-            if (!holds(dinit_cv[x], dinit_t[x], band_rows(r, x).b))
+            if ((qx.hi > b && qx.b != qx.hi) || !holds(dinit_cv[x], dinit_t[x], qx.b))
               return lrcnn_fail(LRCNN_EINVAL, "internal: carry rows not held");
             sd.cinit = dinit_cv[x];
             sd.cinit_t = dinit_t[x];

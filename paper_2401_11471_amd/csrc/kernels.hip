@@ -345,10 +345,29 @@ __device__ __forceinline__ void add_bwd_side(const AddSide &sd, long long idx, i
   }
 }
 
+// A window row above the add's rows: its initial value (carry or zero).
+template <int V>
+__device__ __forceinline__ void add_init_row(const AddSide &sd, const RowIter &e, long long j) {
+  int b, y, in;
+  e.at(j, V, b, y, in);
+  float x[4] = {0.f, 0.f, 0.f, 0.f};
+  float *p = (float *)sd.win.p + view_off(sd.win, b, y, in);
+  const float *bp = err_base(1, sd.cinit, sd.cinit_t, b, y, in, p);
+  if (bp) ldv<float, V>(bp, x);
+  stv<float, V>(p, x);
+}
+
 template <typename T, int V>
-__global__ void add_bwd_kernel(View dz, View z, AddSide sa, AddSide sb, int relu, RowIter it) {
-  GRID_STRIDE(idx, it.total) {
+__global__ void add_bwd_kernel(View dz, View z, AddSide sa, AddSide sb, int relu, RowIter it,
+                               RowIter ea, RowIter eb) {
+  GRID_STRIDE(idx, it.total + ea.total + eb.total) {
     int b, y, in;
+    if (idx >= it.total) {
+      const long long j = idx - it.total;
+      if (j < ea.total) add_init_row<V>(sa, ea, j);
+      else add_init_row<V>(sb, eb, j - ea.total);
+      continue;
+    }
     it.at(idx, V, b, y, in);
     float d[4], zz[4];
     ldv<float, V>((const float *)dz.p + view_off(dz, b, y, in), d);
@@ -368,14 +387,19 @@ int launch_add_bwd(int dt, View dz, View z, const AddSide &sa, const AddSide &sb
   const int V = ((long long)W * C) % 4 == 0 ? 4 : 1;
   RowIter it = row_iter(B, y0, y1, W, C, V);
   if (it.total <= 0) return 0;
+  // initialised rows above the add's rows: window sides with init only
+  for (const AddSide *sd : {&sa, &sb})
+    if (sd->init_hi > y1 && (!sd->init || sd->dc)) return (int)hipErrorInvalidValue;
+  const RowIter ea = row_iter(B, y1, std::max(y1, sa.init_hi), W, C, V);
+  const RowIter eb = row_iter(B, y1, std::max(y1, sb.init_hi), W, C, V);
   hipStream_t s = (hipStream_t)stream;
-  const unsigned g = grid_for(it.total);
+  const unsigned g = grid_for(it.total + ea.total + eb.total);
   if (dt == DT_F32) {
-    if (V == 4) add_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
-    else add_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
+    if (V == 4) add_bwd_kernel<float, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it, ea, eb);
+    else add_bwd_kernel<float, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it, ea, eb);
   } else {
-    if (V == 4) add_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
-    else add_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it);
+    if (V == 4) add_bwd_kernel<bf16, 4><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it, ea, eb);
+    else add_bwd_kernel<bf16, 1><<<g, 256, 0, s>>>(dz, z, sa, sb, relu, it, ea, eb);
   }
   return (int)hipGetLastError();
 }

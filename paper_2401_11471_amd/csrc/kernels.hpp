@@ -402,6 +402,10 @@ struct AddSide {
   int init;
   View cinit;
   int cinit_t;
+  // with init = 1: rows [y1, init_hi) of the window, above the add's rows,
+  // get their initial value alone in the same launch (the window's rows
+  // start at y0 and end at init_hi); 0 = none
+  int init_hi;
 };
 int launch_add_bwd(int dt, View dz, View z, const AddSide &sa, const AddSide &sb, int relu,
                    int B, int y0, int y1, int W, int C, void *stream);
