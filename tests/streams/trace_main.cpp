@@ -16,6 +16,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstdio>
+#include <cstring>
 #include <map>
 #include <set>
 #include <vector>
@@ -79,9 +80,14 @@ static int check(const std::vector<TraceOp> &t, uintptr_t origin, int ncase) {
                   (unsigned long)kv.first, kv.second, t[kv.second].what);
       ++bad;
     }
+  // separate error-window initialisation launches (zeroing, carry copy-in)
+  int inits = 0;
+  for (const TraceOp &o : t)
+    if (o.kind == 'K' && (!std::strcmp(o.what, "rows_init") || !std::strcmp(o.what, "rows_zero")))
+      ++inits;
   std::printf("case %d: ops %zu streams %zu", ncase, t.size(), nops.size());
   for (auto &kv : nops) std::printf(" [%s %d]", kv.first == origin ? "origin" : "side", kv.second);
-  std::printf(" violations %d\n", bad);
+  std::printf(" inits %d violations %d\n", inits, bad);
   return bad;
 }
 

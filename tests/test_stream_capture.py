@@ -15,6 +15,7 @@ Covered: the weight-gradient side stream of the backward, and the opt-in
 forward pass pipelined over bands on two streams, at the five workloads
 (with the step presets of the 224-pixel ones) and on small nets."""
 import os
+import re
 import shutil
 import subprocess
 from pathlib import Path
@@ -85,6 +86,22 @@ def test_captured_step_schedule_is_joined_and_ordered(checker):
     # the pipelined forward does put bands on a second stream
     piped = [l for l in r.stdout.splitlines() if "side" in l]
     assert piped, r.stdout[-2000:]
+
+
+def test_block_outputs_need_no_separate_window_initialisation(checker):
+    # ResNet-50 bf16 at 2400x3600, 32 CARRY bands: each residual block's
+    # output window (the add's rows plus the row carried in from the band
+    # above) is stored by the add's backward, so the separate zeroing and
+    # carry copy-in launches are not one per block and band (16 blocks x 32
+    # bands alone would be 512; the step makes 186)
+    c = CONFIGS[5]
+    line = _line(net_nodes(c["net"]), c["batch"], c["h"], c["w"], c["dtype"], L.CARRY,
+                 c["bands"])
+    r = _run(checker, [line])
+    assert r.returncode == 0, (r.stdout[-4000:], r.stderr[-4000:])
+    assert "failures 0" in r.stdout
+    inits = [int(m) for m in re.findall(r"inits (\d+)", r.stdout)]
+    assert inits and max(inits) < 16 * c["bands"], r.stdout[-2000:]
 
 
 def _planted(tmp_path, old, new, name):
